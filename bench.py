@@ -1,0 +1,248 @@
+#!/usr/bin/env python3
+"""Benchmark of the tandem co-generation rollout on one MI355X.
+
+One bench step = one whole rollout of the batch through the hot path:
+prefill of both models on every prompt, then max_new tandem decode steps
+(dual forward, owner sampling, senior log-probs, handoff rule).  Inputs
+(weights, prompts, KV arena) are resident in HBM before the timed region.
+
+Prints ONE JSON line:
+  value            co-generated tokens / s over the whole job (prefill + decode)
+  roofline         decode attention (the dominant kernel): algorithmic K/V
+                   bytes per launch / its average launch time (HIP events on
+                   the library's stream over the timed region) vs 8 TB/s
+  cpu_baseline     the CPU oracle timed on a bounded sample of the same
+                   workload on this host's cores
+  decode_*         decode-only tokens/s and whole-decode-step HBM fraction
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+METRIC = "co-generated tokens/sec on 1 MI355X; decode HBM GB/s as % of peak"
+
+DESCRIPTIONS = {
+    "qwen": "Qwen3-4B-shaped senior + Qwen3-0.6B-shaped junior, bf16, 16 prompts x G=8, prompt 256, 2048 new tokens, switch p=0.1",
+    "small": "8-layer d=1024 senior + 4-layer d=512 junior, bf16, 8 prompts x G=8, prompt 128, 512 new tokens, switch p=0.1",
+    "wide": "small shapes, 64 prompts x G=16 = 1024 sequences, prompt 256, 4096 new tokens, switch p=0.5",
+    "tiny": "2-layer d=128 senior + 1-layer d=64 junior, fp32, 1 prompt x G=4, 32 new tokens",
+}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+# ----------------------------------------------------------- algorithmic bytes
+def kv_bytes_per_token(s: W.ModelShape) -> int:
+    """K and V bytes of one position over all layers of one model."""
+    esz = 2 if s.dtype == "bf16" else 4
+    return 2 * s.n_layers * s.n_kv_heads * s.head_dim * esz
+
+
+def weight_bytes(s: W.ModelShape) -> int:
+    esz = 2 if s.dtype == "bf16" else 4
+    d, hd = s.d_model, s.head_dim
+    body = s.n_layers * (d * (s.n_q_heads + 2 * s.n_kv_heads) * hd + s.n_q_heads * hd * d + 3 * d * s.ffn_dim)
+    return esz * (body + d * s.vocab)
+
+
+def decode_step_bytes(wl: W.Workload, plens, t: int) -> int:
+    """Bytes the decode step t must move: both models' weights once, every row's
+    K/V context for both models, the K/V append and the embedding rows."""
+    rows = [p for p in plens for _ in range(wl.group)]
+    kv = kv_bytes_per_token(wl.senior) + kv_bytes_per_token(wl.junior)
+    esz_s = 2 if wl.senior.dtype == "bf16" else 4
+    esz_j = 2 if wl.junior.dtype == "bf16" else 4
+    ctx = sum(P + t - 1 for P in rows)
+    return (weight_bytes(wl.senior) + weight_bytes(wl.junior) + ctx * kv + len(rows) * kv
+            + len(rows) * (esz_s * wl.senior.d_model + esz_j * wl.junior.d_model))
+
+
+def attention_bytes(wl: W.Workload, plens, steps: int) -> int:
+    """K/V bytes the decode attention kernels read over `steps` decode steps."""
+    rows = [p for p in plens for _ in range(wl.group)]
+    kv = kv_bytes_per_token(wl.senior) + kv_bytes_per_token(wl.junior)
+    return sum(kv * (P + t - 1) for P in rows for t in range(1, steps + 1))
+
+
+def prefill_flops(wl: W.Workload, plens) -> float:
+    f = 0.0
+    for s in (wl.senior, wl.junior):
+        d, hd = s.d_model, s.head_dim
+        body = s.n_layers * (d * (s.n_q_heads + 2 * s.n_kv_heads) * hd + s.n_q_heads * hd * d + 3 * d * s.ffn_dim)
+        M = sum(P - 1 for P in plens)
+        f += 2.0 * M * body
+        f += sum(4.0 * (P - 1) * P / 2 * s.n_q_heads * hd * s.n_layers for P in plens)
+    return f
+
+
+# ------------------------------------------------------------------ CPU oracle
+def cpu_baseline(wl: W.Workload, ws, wj, prompts, steps: int):
+    """The oracle (float64 NumPy) on prompt 0's G rows: its prefill plus `steps` decode steps."""
+    from oracle.rollout import rollout, build_models
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+    sen, jun = build_models(wl, ws, wj)
+    t0 = time.perf_counter()
+    rollout(sen, jun, prompts, wl.group, wl.switch, wl.sample, wl.philox_seed, W.make_boundary(wl),
+            seq_subset=list(range(wl.group)), max_steps=steps)
+    dt = time.perf_counter() - t0
+    return {"value": wl.group * steps / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"prompt 0 x G={wl.group} rows: prefill of {len(prompts[0]) - 1} prompt tokens + "
+                      f"{steps} decode steps ({wl.group * steps} co-generated tokens) in {dt:.1f} s",
+            "host_cpus": os.cpu_count(), "affinity": len(os.sched_getaffinity(0))}
+
+
+# ------------------------------------------------------------------------ main
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="qwen", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--max-new", type=int, default=None, help="shorter rollouts (development only)")
+    ap.add_argument("--cpu-steps", type=int, default=4, help="decode steps of the CPU-oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true", help="also time every kernel class (extra pass)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus > 1 or world > 1:
+        print(json.dumps({"error": "this build runs on one GPU only: the tandem rollout shards over prompt "
+                                   "groups with no per-step exchange, and no multi-GPU path is built"}))
+        sys.exit(2)
+
+    import torch
+    from paper_2606_28166_amd.engine import TandemEngine
+
+    wl = W.workload(args.workload)
+    if args.max_new:
+        wl.sample.max_new = args.max_new
+    t0 = time.time()
+    ws, wj, prompts, bnd = W.make_all(wl)
+    plens = [len(p) for p in prompts]
+    log(f"[bench] weights generated in {time.time() - t0:.1f}s")
+    max_ctx = max(plens) - 1 + wl.sample.max_new
+    eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed,
+                       max_seqs=wl.n_seqs, max_ctx=max_ctx, max_prefill_tokens=4096,
+                       boundary_words=W.boundary_bits(bnd))
+    log(f"[bench] engine ready: KV arena {eng.kv_bytes / 2**30:.1f} GiB, scratch {eng.scratch_bytes / 2**30:.2f} GiB")
+    stream = eng.stream
+    L = wl.sample.max_new
+    n = wl.n_seqs
+
+    def rollout_once(timed_attention=False):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(stream)
+        eng.prefill(prompts, wl.group)
+        ev[1].record(stream)
+        if timed_attention:
+            eng.timing(1 << 0)
+        for _ in range(L):
+            eng.step()
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        att = eng.timing_read()["attention"] if timed_attention else None
+        if timed_attention:
+            eng.timing(0)
+        return ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), att
+
+    for i in range(args.warmup):
+        p_ms, d_ms, _ = rollout_once()
+        log(f"[bench] warmup {i}: prefill {p_ms:.1f} ms, decode {d_ms:.1f} ms")
+
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    pre, dec, att_ms, att_n = [], [], 0.0, 0
+    for i in range(args.steps):
+        p_ms, d_ms, att = rollout_once(timed_attention=True)
+        pre.append(p_ms)
+        dec.append(d_ms)
+        att_ms += att[0]
+        att_n += att[1]
+        log(f"[bench] step {i}: prefill {p_ms:.1f} ms, decode {d_ms:.1f} ms, attention {att[0]:.1f} ms/{att[1]} launches")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+
+    out = eng.outputs()
+    senior_share = float(out["owner"][:, :L].mean())
+    toks = n * L * args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    value = toks / wall
+    dec_s = sum(dec) / 1e3
+    dec_bytes = sum(decode_step_bytes(wl, plens, t) for t in range(1, L + 1)) * args.steps
+    att_bytes = attention_bytes(wl, plens, L) * args.steps
+    att_gbs = att_bytes / (att_ms / 1e3) / 1e9
+    pf = prefill_flops(wl, plens)
+    pre_ms = float(np.mean(pre))
+
+    breakdown = None
+    if args.breakdown:
+        eng.prefill(prompts, wl.group)
+        eng.timing(0b1111)
+        for _ in range(L):
+            eng.step()
+        breakdown = {k: {"ms": round(v[0], 3), "launches": v[1]} for k, v in eng.timing_read().items()}
+        eng.timing(0)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        eng_models = None
+        log("[bench] timing the CPU oracle sample")
+        cpu = cpu_baseline(wl, ws, wj, prompts, args.cpu_steps)
+
+    res = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.senior.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": DESCRIPTIONS[wl.name], "name": wl.name, "rows": n, "prompt_len": plens[0],
+                   "max_new": L, "senior_layers": wl.senior.n_layers, "junior_layers": wl.junior.n_layers,
+                   "vocab": wl.senior.vocab},
+        "roofline": {"bound": "hbm", "kernel": "decode attention (both models)",
+                     "achieved": round(att_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(att_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "launches": att_n, "avg_launch_us": round(att_ms * 1e3 / max(att_n, 1), 2),
+                     "bytes_per_launch": int(att_bytes / max(att_n, 1))},
+        "cpu_baseline": cpu,
+        "decode_tokens_per_s": round(n * L * args.steps / dec_s, 2),
+        "decode_ms_per_token_step": round(sum(dec) / (L * args.steps), 4),
+        "decode_hbm_gbs": round(dec_bytes / dec_s / 1e9, 1),
+        "decode_hbm_frac": round(dec_bytes / dec_s / 1e9 / HBM_PEAK_GBS, 4),
+        "prefill_ms": round(pre_ms, 3),
+        "prefill_tflops": round(pf / (pre_ms / 1e3) / 1e12, 1),
+        "prefill_mfma_frac": round(pf / (pre_ms / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        "senior_share": round(senior_share, 4),
+        "breakdown": breakdown,
+    }
+    eng.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,218 @@
+/*
+ * tandem.h — C ABI of the MI355X tandem co-generation library (libtandem.so).
+ *
+ * What it computes (Tandem RL with Verifiable Rewards):
+ *   Section 3.3 and Algorithm 1 (rollout half): a trained senior and a frozen
+ *   junior causal LM with one shared vocabulary co-generate each response.
+ *   At every step BOTH models forward the shared history x . y_<t, the
+ *   current owner a_t samples y_t from its own next-token distribution, the
+ *   token is appended to both models' KV caches, and ownership is redrawn
+ *   with a Bernoulli(p) coin after boundary tokens or once the span counter
+ *   reaches the cap K.  Each step records y_t, the authorship bit
+ *   m_t = 1[a_t = senior] and log pi_sen(y_t | x . y_<t), the quantity the
+ *   senior-only GRPO loss of Section 3.4 (the L_TRL equation) consumes.
+ *   The reproducibility appendix describes the same step inside a serving
+ *   engine: shared per-step position metadata, one KV cache per model,
+ *   a per-request seeded generator and a small per-request sampler state.
+ *
+ * Memory ownership: the CALLER owns every device buffer (weights, KV arena,
+ * scratch, output arenas, boundary bitmap, prompts, forced tokens, debug
+ * buffers).  The library borrows the pointers until tandem_destroy and owns
+ * only host-side state.  Sizes of the KV arena and the scratch buffer come
+ * from tandem_workspace_size.
+ *
+ * Streams: every call enqueues its work on the stream given to tandem_init
+ * (a hipStream_t passed as void*) and returns without synchronising, except
+ * when a host result is requested (n_active, tandem_get_state).
+ *
+ * Errors: every call returns a tandem_status; tandem_last_error(handle) (or
+ * tandem_last_error(NULL) for calls that failed before a handle existed)
+ * gives a message.  Arguments are validated before any HIP call.  A failing
+ * HIP call returns TANDEM_E_HIP and poisons the handle: later calls return
+ * TANDEM_E_STATE.  One handle must not be used from two threads at once.
+ */
+#ifndef TANDEM_H
+#define TANDEM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TANDEM_OK = 0,
+  TANDEM_E_ARG = -1,          /* NULL pointer, bad enum, p outside [0,1], T <= 0, ... */
+  TANDEM_E_SHAPE = -2,        /* inconsistent model shapes (vocab mismatch, n_q % n_kv, ...) */
+  TANDEM_E_CAPACITY = -3,     /* request exceeds the capacity given at init / buffer too small */
+  TANDEM_E_STATE = -4,        /* call out of order (step before prefill) or poisoned handle */
+  TANDEM_E_HIP = -5,          /* a HIP runtime call failed */
+  TANDEM_E_UNSUPPORTED = -6   /* a shape this build has no kernel for (head_dim, ...) */
+} tandem_status;
+
+/* first owner a_1 (Algorithm 1 draws it with the same Bernoulli(p) coin) */
+enum { TANDEM_JUNIOR = 0, TANDEM_SENIOR = 1, TANDEM_DRAW = 2 };
+
+/* What happens at a decision point (boundary token or span cap reached):
+ *   REDRAW    next owner = senior with probability p (the paper's rule);
+ *   SWITCH    owner flips with probability p ("per-token switch probability");
+ *   ALTERNATE owner always flips (the deterministic reasoning-step schedule). */
+enum { TANDEM_REDRAW = 0, TANDEM_SWITCH = 1, TANDEM_ALTERNATE = 2 };
+
+/* element type of the weights and of the KV cache (activations are always fp32) */
+enum { TANDEM_BF16 = 0, TANDEM_F32 = 1 };
+
+/* Shape of one pre-norm decoder: RMSNorm, grouped-query attention with
+ * NeoX-style rotary embedding (optional per-head q/k RMSNorm), SwiGLU FFN,
+ * final RMSNorm and an untied LM head. */
+typedef struct {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  float rope_theta;           /* rotary base theta */
+  float rms_eps;              /* RMSNorm epsilon */
+  int32_t qk_norm;            /* 1: per-head RMSNorm of q and k before RoPE */
+  int32_t weight_dtype;       /* TANDEM_BF16 or TANDEM_F32 */
+} tandem_model_cfg;
+
+/* Device pointers to one model's weights.  Matrices are row-major
+ * [out][in] in weight_dtype; norm gains are float32.
+ *   embed      [vocab][d_model]
+ *   layers     HOST array of n_layers * 8 device pointers, per layer in order:
+ *              attn_norm [d], w_qkv [(n_q + 2 n_kv) * hd][d] (rows: q heads,
+ *              then k heads, then v heads), q_norm [hd], k_norm [hd] (both
+ *              NULL unless qk_norm), w_o [d][n_q * hd], ffn_norm [d],
+ *              w_gate_up [2 ffn][d] (gate rows, then up rows), w_down [d][ffn]
+ *   final_norm [d_model]
+ *   lm_head    [vocab][d_model]
+ * The layers array is copied at tandem_init; the weights are borrowed. */
+typedef struct {
+  tandem_model_cfg cfg;
+  const void* embed;
+  const void* const* layers;
+  const void* final_norm;
+  const void* lm_head;
+} tandem_model;
+
+/* Handoff rule (Algorithm 1's boundary-or-cap block). */
+typedef struct {
+  int32_t mode;                    /* TANDEM_REDRAW / TANDEM_SWITCH / TANDEM_ALTERNATE */
+  double p;                        /* coin probability, 0 <= p <= 1 */
+  int32_t cap_k;                   /* span cap K; < 0 disables the cap */
+  const uint32_t* boundary_bits;   /* device bitmap, bit (v & 31) of word v >> 5 marks a
+                                      boundary token; NULL = every token is a boundary */
+  int32_t first_owner;             /* TANDEM_JUNIOR / TANDEM_SENIOR / TANDEM_DRAW */
+} tandem_switch_cfg;
+
+/* Sampling: scores s_m = (z_m + b_m * e_eos) / T; the owner's scores are
+ * sampled by Gumbel-max with Philox4x32-10 noise keyed by (seed, sequence id,
+ * step, vocab index); the handoff coin uses a separate Philox stream. */
+typedef struct {
+  float temperature;               /* T > 0 */
+  int32_t eos_id;                  /* < 0: no end-of-sequence token */
+  float eos_bias_senior;           /* logit bias added to eos_id (senior) */
+  float eos_bias_junior;           /* logit bias added to eos_id (junior) */
+  int32_t max_new_tokens;          /* L: tokens generated per sequence at most */
+  uint64_t seed;                   /* request seed: Philox key (low word, high word) */
+} tandem_sample_cfg;
+
+typedef struct {
+  int32_t max_seqs;                /* >= n_prompts * G */
+  int32_t max_ctx;                 /* >= longest prompt - 1 + max_new_tokens */
+  int32_t max_prefill_tokens;      /* rows of one prefill pass (prompts are chunked to fit) */
+} tandem_capacity;
+
+/* Caller-owned device output arenas, sequence-major [max_seqs][max_new_tokens].
+ * Entry [s][t-1] is written at step t of sequence s (s = j * G + i). */
+typedef struct {
+  int32_t* tokens;                 /* y_t */
+  uint8_t* owner;                  /* m_t = 1 if the senior emitted y_t */
+  float* senior_logprob;           /* log softmax(s_sen)[y_t], every position */
+  int32_t* length;                 /* [max_seqs] tokens recorded so far */
+} tandem_outputs;
+
+/* Optional device buffers filled by tandem_step_forced (any may be NULL). */
+typedef struct {
+  int32_t* sampled;                /* [max_seqs] the library's own sample of this step */
+  float* margin;                   /* [max_seqs] best - second Gumbel score of the owner */
+  float* logits_senior;            /* [max_seqs][vocab] raw senior logits z_sen */
+  float* logits_junior;            /* [max_seqs][vocab] raw junior logits z_jun */
+} tandem_debug;
+
+typedef struct tandem_handle tandem_handle;
+
+/* Bytes of KV arena and scratch that tandem_init needs for these shapes and
+ * this capacity.  Both buffers must be 256-byte aligned device memory. */
+tandem_status tandem_workspace_size(const tandem_model_cfg* senior, const tandem_model_cfg* junior,
+                                    const tandem_capacity* cap, size_t* kv_bytes,
+                                    size_t* scratch_bytes);
+
+/* Validate the pair (shared vocabulary, supported head_dim, ...), bind the
+ * weights, arenas and stream, and build per-model tables.  stream is a
+ * hipStream_t (NULL = the null stream).  On success *out_handle is set. */
+tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior,
+                          const tandem_switch_cfg* sw, const tandem_sample_cfg* smp,
+                          const tandem_capacity* cap, void* kv_arena, size_t kv_bytes,
+                          void* scratch, size_t scratch_bytes, const tandem_outputs* out,
+                          void* stream, tandem_handle** out_handle);
+
+/* Prefill both models on every prompt but its last token, replicate the
+ * prompt's KV into its G sequences, and set each sequence's state: pending
+ * token = last prompt token, position = P_j - 1, step t = 1, span counter 0,
+ * first owner per first_owner.
+ *   prompt_tokens  device int32, prompts concatenated
+ *   prompt_offsets HOST int32 [n_prompts + 1], CSR offsets into prompt_tokens
+ * Every prompt needs >= 1 token.  Sequence ids are s = j * G + i.  A new
+ * prefill starts a new batch (all previous sequence state is replaced). */
+tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens,
+                             const int32_t* prompt_offsets, int32_t n_prompts, int32_t G);
+
+/* One tandem decode step for every unfinished sequence: forward the pending
+ * token through both models (appending to both caches), sample y_t from the
+ * owner, write (y_t, m_t, senior log-prob) to the output arenas, stop at EOS
+ * or at t = max_new_tokens, apply the handoff rule.  If n_active is not NULL
+ * the call synchronises and stores the number of unfinished sequences. */
+tandem_status tandem_step(tandem_handle* h, int32_t* n_active);
+
+/* As tandem_step, but the appended token of sequence s is forced[s] (device
+ * int32 [max_seqs]; entries < 0 keep the library's own sample).  The owner
+ * rule and the outputs follow the appended token; dbg (may be NULL) receives
+ * the library's own sample, its margin and the raw logits of this step. */
+tandem_status tandem_step_forced(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg,
+                                 int32_t* n_active);
+
+/* Copy the per-sequence sampler state to HOST int32 arrays of n_seqs
+ * entries (any pointer may be NULL): owner (1 = senior), span counter c,
+ * next step t, next position, done flag.  Synchronises the stream. */
+tandem_status tandem_get_state(tandem_handle* h, int32_t* owner, int32_t* c, int32_t* t,
+                               int32_t* pos, int32_t* done);
+
+/* Instrumentation (the benchmark's roofline and the per-kernel breakdown).
+ * class_mask bit k enables class k: the library then records a hipEvent pair
+ * around every launch of that class on its stream; tandem_timing_read
+ * synchronises and returns the summed device milliseconds and the number of
+ * launches of one class since the last tandem_timing_enable.  Every call to
+ * tandem_timing_enable resets the sums (mask 0 switches timing off).  Each
+ * event pair adds a few microseconds of stream time. */
+enum { TANDEM_K_ATTENTION = 0,    /* decode / prompt attention            */
+       TANDEM_K_GEMM = 1,         /* projection and LM-head GEMMs         */
+       TANDEM_K_SAMPLE = 2,       /* sampling, log-prob, handoff rule     */
+       TANDEM_K_OTHER = 3,        /* norms, QKV post-processing, copies   */
+       TANDEM_K_CLASSES = 4 };
+tandem_status tandem_timing_enable(tandem_handle* h, int32_t class_mask);
+tandem_status tandem_timing_read(tandem_handle* h, int32_t kernel_class, double* total_ms, int64_t* launches);
+
+/* Message of the last failure on this handle (or of this thread's last
+ * handle-less failure when h is NULL).  Never NULL. */
+const char* tandem_last_error(const tandem_handle* h);
+
+/* Human-readable name of a status code. */
+const char* tandem_status_string(tandem_status s);
+
+/* Release host-side state; device buffers stay with the caller.  NULL is a no-op. */
+void tandem_destroy(tandem_handle* h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TANDEM_H */

@@ -7,7 +7,8 @@ per-head RMSNorm of q and k (Qwen3), and a SwiGLU feed-forward, followed by a
 final RMSNorm and an untied LM head.  Each model keeps its own cache and both
 consume every token of the shared history x . y_<t (Section 3.3; the
 dual-decoder backend of the reproducibility appendix keeps the two caches in
-lockstep).
+lockstep).  A bf16 model keeps its cache in bf16 (its storage format; the
+paper does not state the rollout precision).
 
 One function, ``forward``, serves prefill and decode: it takes a list of
 tokens, each with its own cache and position.  Within a layer every token's
@@ -48,6 +49,25 @@ def silu(x: np.ndarray) -> np.ndarray:
     return x / (1.0 + np.exp(-x))
 
 
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest bf16 (ties to even), returned as float64.
+
+    Correct single rounding: first round to float32 by round-to-odd (truncate,
+    then set the last bit if anything was dropped), which keeps the second
+    rounding to bf16 (round to nearest even on the top 16 bits) exact.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    t = x.astype(np.float32)
+    away = np.abs(t.astype(np.float64)) > np.abs(x)
+    t = np.where(away, np.nextafter(t, np.float32(0)), t)        # truncation toward zero
+    u = t.view(np.uint32).copy()
+    inexact = t.astype(np.float64) != x
+    u |= inexact.astype(np.uint32)                                # sticky bit
+    u = u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))
+    u &= np.uint32(0xFFFF0000)
+    return u.view(np.float32).astype(np.float64)
+
+
 class KVCache:
     """One sequence's cache for one model: K and V as [layer, kv_head, ctx, hd]."""
 
@@ -64,9 +84,15 @@ class KVCache:
 
 class OracleModel:
     def __init__(self, shape, weights: Dict[str, np.ndarray]):
-        """shape: workloads.ModelShape; weights: float64 arrays keyed as in workloads."""
+        """shape: workloads.ModelShape; weights: float64 arrays keyed as in workloads.
+
+        A bf16 model stores its weights AND its KV cache in bf16: keys and
+        values are rounded to bf16 when they are appended (the storage format
+        of the model, as for the weights); everything else is float64.
+        """
         self.s = shape
         self.w = weights
+        self.kv_round = round_bf16 if getattr(shape, "dtype", "f32") == "bf16" else (lambda a: a)
 
     def new_cache(self, max_ctx: int) -> KVCache:
         s = self.s
@@ -114,6 +140,8 @@ class OracleModel:
                 k = rmsnorm(k, w[p + "k_norm"], s.rms_eps)
             q = rope(q, pos, s.rope_theta)
             k = rope(k, pos, s.rope_theta)
+            k = self.kv_round(k)
+            v = self.kv_round(v)
             for i in range(n):
                 caches[i].k[li, :, pos[i], :] = k[i]
                 caches[i].v[li, :, pos[i], :] = v[i]

@@ -1,0 +1,426 @@
+// Row-wise kernels of the tandem step: embedding + RMSNorm, residual +
+// RMSNorm, QKV post-processing with the KV append, sampling, the handoff
+// rule, prompt-KV replication and per-sequence state set-up.
+#include "common.h"
+#include "kernels.h"
+
+namespace tandem {
+
+namespace {
+
+constexpr int kNT = 256;
+constexpr int kMaxPer = 32;        // d_model <= 8192
+
+// ------------------------------------------------------------------ norms
+template <typename WT>
+__global__ __launch_bounds__(kNT) void embed_norm_kernel(const int32_t* __restrict__ tok,
+                                                         const WT* __restrict__ E, int d,
+                                                         const float* __restrict__ gain, float eps,
+                                                         float* __restrict__ h, float* __restrict__ x) {
+  __shared__ float red[kNT / 64];
+  const int r = blockIdx.x, tid = threadIdx.x;
+  const WT* e = E + (size_t)tok[r] * d;
+  float v[kMaxPer];
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < kMaxPer; ++k) {
+    const int i = tid + k * kNT;
+    v[k] = i < d ? ld(e + i) : 0.f;
+    ss += v[k] * v[k];
+  }
+  const float tot = block_sum<kNT>(ss, red);
+  const float rs = 1.f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int k = 0; k < kMaxPer; ++k) {
+    const int i = tid + k * kNT;
+    if (i < d) {
+      h[(size_t)r * d + i] = v[k];
+      x[(size_t)r * d + i] = v[k] * rs * gain[i];
+    }
+  }
+}
+
+__global__ __launch_bounds__(kNT) void resid_norm_kernel(const float* __restrict__ ws, int S,
+                                                         long ws_stride, float* __restrict__ h,
+                                                         const float* __restrict__ gain, float eps,
+                                                         float* __restrict__ x, int d) {
+  __shared__ float red[kNT / 64];
+  const int r = blockIdx.x, tid = threadIdx.x;
+  float v[kMaxPer];
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < kMaxPer; ++k) {
+    const int i = tid + k * kNT;
+    float a = 0.f;
+    if (i < d) {
+      const size_t off = (size_t)r * d + i;
+      a = h[off];
+      for (int s = 0; s < S; ++s) a += ws[s * ws_stride + off];
+    }
+    v[k] = a;
+    ss += a * a;
+  }
+  const float tot = block_sum<kNT>(ss, red);
+  const float rs = 1.f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int k = 0; k < kMaxPer; ++k) {
+    const int i = tid + k * kNT;
+    if (i < d) {
+      h[(size_t)r * d + i] = v[k];
+      x[(size_t)r * d + i] = v[k] * rs * gain[i];
+    }
+  }
+}
+
+// ------------------------------------------------------------ qkv post
+// One workgroup per row.  Sums the split-K partials, applies the optional
+// per-head q/k RMSNorm and NeoX rotary embedding (lane i rotates the pair
+// (i, i + hd/2)), writes q, and appends k (row-major [pos][hd]) and v
+// (transposed [hd][pos]) at the row's (slot, pos).
+template <typename KT>
+__global__ __launch_bounds__(kNT) void qkv_post_kernel(
+    const float* __restrict__ ws, int S, long ws_stride, int nq, int nkv, int hd,
+    const float* __restrict__ q_norm, const float* __restrict__ k_norm, float eps,
+    const float2* __restrict__ rope, const int32_t* __restrict__ row_slot,
+    const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
+    float* __restrict__ q_out, KT* __restrict__ kc, KT* __restrict__ vc, int ctx_stride, long slot_stride) {
+  extern __shared__ float buf[];
+  const int r = blockIdx.x, tid = threadIdx.x;
+  if (row_done && row_done[r]) return;
+  const int dim = (nq + 2 * nkv) * hd;
+  const size_t rbase = (size_t)r * dim;
+  for (int i = tid; i < dim; i += kNT) {
+    float a = 0.f;
+    for (int s = 0; s < S; ++s) a += ws[s * ws_stride + rbase + i];
+    buf[i] = a;
+  }
+  __syncthreads();
+  const int slot = row_slot[r], pos = row_pos[r];
+  const int half = hd / 2;
+  const int lane = tid & 63, wave = tid >> 6;
+  for (int head = wave; head < nq + nkv; head += kNT / 64) {
+    const bool isq = head < nq;
+    const float* src = buf + head * hd;
+    float x1 = 0.f, x2 = 0.f;
+    if (lane < half) {
+      x1 = src[lane];
+      x2 = src[lane + half];
+    }
+    const float* gn = isq ? q_norm : k_norm;
+    if (gn) {
+      const float ss = wave_sum(x1 * x1 + x2 * x2);
+      const float rs = 1.f / sqrtf(ss / (float)hd + eps);
+      if (lane < half) {
+        x1 *= rs * gn[lane];
+        x2 *= rs * gn[lane + half];
+      }
+    }
+    if (lane < half) {
+      const float2 cs = rope[(size_t)pos * half + lane];
+      const float y1 = x1 * cs.x - x2 * cs.y;
+      const float y2 = x2 * cs.x + x1 * cs.y;
+      if (isq) {
+        float* qo = q_out + ((size_t)r * nq + head) * hd;
+        qo[lane] = y1;
+        qo[lane + half] = y2;
+      } else {
+        KT* ko = kc + (size_t)slot * slot_stride + ((size_t)(head - nq) * ctx_stride + pos) * hd;
+        st(ko + lane, y1);
+        st(ko + lane + half, y2);
+      }
+    }
+  }
+  for (int e = tid; e < nkv * hd; e += kNT) {
+    const int kh = e / hd, d = e % hd;
+    KT* vo = vc + (size_t)slot * slot_stride + ((size_t)kh * hd + d) * ctx_stride + pos;
+    st(vo, buf[(nq + nkv) * hd + e]);
+  }
+}
+
+__global__ void rope_table_kernel(double theta, int hd, int n_pos, float2* __restrict__ out) {
+  const int half = hd / 2;
+  const long n = (long)n_pos * half;
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < n; e += (long)gridDim.x * blockDim.x) {
+    const int p = (int)(e / half), i = (int)(e % half);
+    const double inv = pow(theta, -2.0 * i / (double)hd);
+    double s, c;
+    sincos((double)p * inv, &s, &c);
+    out[e] = make_float2((float)c, (float)s);
+  }
+}
+
+// --------------------------------------------------------------- sampling
+struct Top2 {
+  float b; int i; float s;
+};
+__device__ __forceinline__ bool beats(float vb, int ib, float va, int ia) {
+  return vb > va || (vb == va && ib < ia);
+}
+__device__ __forceinline__ Top2 merge_top2(Top2 A, Top2 B) {
+  Top2 out;
+  if (beats(B.b, B.i, A.b, A.i)) {
+    out.b = B.b; out.i = B.i; out.s = fmaxf(fmaxf(A.s, B.s), A.b);
+  } else {
+    out.b = A.b; out.i = A.i; out.s = fmaxf(fmaxf(A.s, B.s), B.b);
+  }
+  return out;
+}
+__device__ __forceinline__ void merge_lse(float& m, float& l, float m2, float l2) {
+  const float M = fmaxf(m, m2);
+  if (M == -INFINITY) { m = M; l = 0.f; return; }
+  l = l * expf(m - M) + l2 * expf(m2 - M);
+  m = M;
+}
+
+// Per (chunk of the vocabulary, row): online log-sum-exp of the senior's
+// scores and the top-2 of the owner's Gumbel-perturbed scores.
+__global__ __launch_bounds__(kNT) void sample_partials_kernel(SampleArgs a) {
+  __shared__ float sm[kNT / 64][5];
+  const int ch = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
+  if (a.done[r]) return;
+  const int s = r, tt = a.t[s];
+  const bool own_sen = a.owner[s] != 0;
+  const float* zs = a.z_sen + (size_t)r * a.V;
+  const float* zj = a.z_jun + (size_t)r * a.V;
+  const int v0 = ch * a.chunk, v1 = min(a.V, v0 + a.chunk);
+  float ms = -INFINITY, ls = 0.f;
+  Top2 top{-INFINITY, 0x7FFFFFFF, -INFINITY};
+  for (int base = v0 + tid * 4; base < v1; base += kNT * 4) {
+    const u32x4 ph = philox4x32_10(u32x4{(uint32_t)(base >> 2), (uint32_t)tt, (uint32_t)s, 0u}, a.key0, a.key1);
+    const uint32_t w[4] = {ph.x, ph.y, ph.z, ph.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int v = base + e;
+      if (v < v1) {
+        const float sv = (zs[v] + (v == a.eos_id ? a.eos_bias_sen : 0.f)) / a.temp;
+        if (sv > ms) { ls = ls * expf(ms - sv) + 1.f; ms = sv; }
+        else ls += expf(sv - ms);
+        const float so = own_sen ? sv : (zj[v] + (v == a.eos_id ? a.eos_bias_jun : 0.f)) / a.temp;
+        const float val = so + gumbel(w[e]);
+        top = merge_top2(top, Top2{val, v, -INFINITY});
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(ms, o, 64), l2 = __shfl_xor(ls, o, 64);
+    merge_lse(ms, ls, m2, l2);
+    Top2 B{__shfl_xor(top.b, o, 64), __shfl_xor(top.i, o, 64), __shfl_xor(top.s, o, 64)};
+    top = merge_top2(top, B);
+  }
+  const int lane = tid & 63, wave = tid >> 6;
+  if (lane == 0) {
+    sm[wave][0] = ms; sm[wave][1] = ls; sm[wave][2] = top.b;
+    sm[wave][3] = __int_as_float(top.i); sm[wave][4] = top.s;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < kNT / 64; ++w) {
+      merge_lse(ms, ls, sm[w][0], sm[w][1]);
+      top = merge_top2(top, Top2{sm[w][2], __float_as_int(sm[w][3]), sm[w][4]});
+    }
+    float* p = a.partials + ((size_t)r * gridDim.x + ch) * 5;
+    p[0] = ms; p[1] = ls; p[2] = top.b; p[3] = __int_as_float(top.i); p[4] = top.s;
+  }
+}
+
+// One wave per row: merge the chunk partials, pick the token, compute the
+// senior log-prob, write the outputs and apply the handoff rule.
+__global__ __launch_bounds__(64) void sample_finish_kernel(FinishArgs a) {
+  const int r = blockIdx.x, lane = threadIdx.x;
+  const int s = r;
+  if (a.done[s]) return;
+  float ms = -INFINITY, ls = 0.f;
+  Top2 top{-INFINITY, 0x7FFFFFFF, -INFINITY};
+  for (int c = lane; c < a.n_chunks; c += 64) {
+    const float* p = a.partials + ((size_t)r * a.n_chunks + c) * 5;
+    merge_lse(ms, ls, p[0], p[1]);
+    top = merge_top2(top, Top2{p[2], __float_as_int(p[3]), p[4]});
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(ms, o, 64), l2 = __shfl_xor(ls, o, 64);
+    merge_lse(ms, ls, m2, l2);
+    Top2 B{__shfl_xor(top.b, o, 64), __shfl_xor(top.i, o, 64), __shfl_xor(top.s, o, 64)};
+    top = merge_top2(top, B);
+  }
+  if (lane != 0) return;
+  // a row whose scores are all NaN never updates the argmax: keep the index in range
+  const int y_hat = (top.i >= 0 && top.i < a.V) ? top.i : 0;
+  int y = y_hat;
+  if (a.forced) {
+    const int f = a.forced[s];
+    if (f >= 0 && f < a.V) y = f;
+  }
+  const float sy = (a.z_sen[(size_t)r * a.V + y] + (y == a.eos_id ? a.eos_bias_sen : 0.f)) / a.temp;
+  const float lp = sy - (ms + logf(ls));
+  const int tt = a.t[s];
+  const int own = a.owner[s];
+  const size_t o = (size_t)s * a.ld_out + (tt - 1);
+  a.out_tok[o] = y;
+  a.out_own[o] = (uint8_t)(own != 0);
+  a.out_lp[o] = lp;
+  a.out_len[s] = tt;
+  if (a.dbg_sampled) a.dbg_sampled[s] = y_hat;
+  if (a.dbg_margin) a.dbg_margin[s] = top.b - top.s;
+  const bool is_eos = a.eos_id >= 0 && y == a.eos_id;
+  if (!is_eos) {
+    const bool is_b = a.bnd ? ((a.bnd[y >> 5] >> (y & 31)) & 1u) != 0 : true;
+    const bool at_cap = a.cap_k >= 0 && a.c[s] >= a.cap_k;
+    if (is_b || at_cap) {
+      const u32x4 ph = philox4x32_10(u32x4{0u, (uint32_t)tt, (uint32_t)s, 1u}, a.key0, a.key1);
+      const bool fire = (unsigned long long)ph.x < a.thr;
+      int nxt = own;
+      if (a.mode == 0) nxt = fire ? 1 : 0;
+      else if (a.mode == 1) nxt = fire ? 1 - own : own;
+      else nxt = 1 - own;
+      a.owner[s] = nxt;
+      a.c[s] = 0;
+    } else {
+      a.c[s] += 1;
+    }
+  }
+  if (is_eos || tt >= a.max_new) a.done[s] = 1;
+  a.pending[s] = y;
+  a.pos[s] += 1;
+  a.t[s] = tt + 1;
+}
+
+// ----------------------------------------------------- replication / state
+template <typename T>
+__global__ __launch_bounds__(kNT) void kv_replicate_kernel(T* kc, T* vc, int nkv, int hd, int ctx_stride,
+                                                           long layer_stride, long slot_stride, int src,
+                                                           int dst0, int n_pos) {
+  const int lk = blockIdx.x;                 // layer * nkv + kv head
+  const int layer = lk / nkv, kh = lk % nkv;
+  const int dst = dst0 + blockIdx.y;
+  const size_t kh_off = (size_t)kh * ctx_stride * hd;
+  const T* ks = kc + layer * layer_stride + (size_t)src * slot_stride + kh_off;
+  T* kd = kc + layer * layer_stride + (size_t)dst * slot_stride + kh_off;
+  for (long e = threadIdx.x; e < (long)n_pos * hd; e += kNT) kd[e] = ks[e];
+  const T* vs = vc + layer * layer_stride + (size_t)src * slot_stride + kh_off;
+  T* vd = vc + layer * layer_stride + (size_t)dst * slot_stride + kh_off;
+  for (long e = threadIdx.x; e < (long)n_pos * hd; e += kNT) {
+    const long d = e / n_pos, p = e % n_pos;
+    vd[d * ctx_stride + p] = vs[d * ctx_stride + p];
+  }
+}
+
+__global__ void init_state_kernel(InitStateArgs a) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= a.n_seq) return;
+  const int j = s / a.G;
+  const int P = a.prompt_len[j];
+  a.pending[s] = a.prompt_tokens[a.prompt_end[j] - 1];
+  a.pos[s] = P - 1;
+  a.t[s] = 1;
+  a.c[s] = 0;
+  a.done[s] = 0;
+  a.out_len[s] = 0;
+  int own = a.first_owner;
+  if (own == 2) {
+    const u32x4 ph = philox4x32_10(u32x4{0u, 0u, (uint32_t)s, 1u}, a.key0, a.key1);
+    own = ((unsigned long long)ph.x < a.thr) ? 1 : 0;
+  }
+  a.owner[s] = own;
+}
+
+__global__ void count_active_kernel(const int32_t* done, int n, int32_t* out) {
+  __shared__ float red[kNT / 64];
+  float c = 0.f;
+  for (int i = threadIdx.x; i < n; i += kNT) c += done[i] ? 0.f : 1.f;
+  c = block_sum<kNT>(c, red);
+  if (threadIdx.x == 0) *out = (int32_t)c;
+}
+
+__global__ void gather_i32_kernel(const int32_t* src, const int32_t* idx, int n, int32_t* dst) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[idx[i]];
+}
+
+}  // namespace
+
+hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, const float* gain,
+                             float eps, float* h, float* x, int R, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL((embed_norm_kernel<bf16_t>), dim3(R), dim3(kNT), 0, st, tok, (const bf16_t*)E, d,
+                       gain, eps, h, x);
+  else
+    hipLaunchKernelGGL((embed_norm_kernel<float>), dim3(R), dim3(kNT), 0, st, tok, (const float*)E, d,
+                       gain, eps, h, x);
+  return hipGetLastError();
+}
+
+hipError_t launch_resid_norm(const float* ws, int S, long ws_stride, float* h, const float* gain,
+                             float eps, float* x, int R, int d, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(resid_norm_kernel, dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_qkv_post(const QkvPostArgs& a, hipStream_t st) {
+  if (a.R <= 0) return hipSuccess;
+  const size_t shm = sizeof(float) * (size_t)(a.nq + 2 * a.nkv) * a.hd;
+  if (a.dt == DT_BF16)
+    hipLaunchKernelGGL((qkv_post_kernel<bf16_t>), dim3(a.R), dim3(kNT), shm, st, a.ws, a.S, a.ws_stride,
+                       a.nq, a.nkv, a.hd, a.q_norm, a.k_norm, a.eps, a.rope, a.row_slot, a.row_pos,
+                       a.row_done, a.q_out, (bf16_t*)a.cache.k, (bf16_t*)a.cache.v,
+                       a.cache.ctx_stride, a.cache.slot_stride);
+  else
+    hipLaunchKernelGGL((qkv_post_kernel<float>), dim3(a.R), dim3(kNT), shm, st, a.ws, a.S, a.ws_stride,
+                       a.nq, a.nkv, a.hd, a.q_norm, a.k_norm, a.eps, a.rope, a.row_slot, a.row_pos,
+                       a.row_done, a.q_out, (float*)a.cache.k, (float*)a.cache.v,
+                       a.cache.ctx_stride, a.cache.slot_stride);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_table(float theta, int hd, int n_pos, float2* out, hipStream_t st) {
+  hipLaunchKernelGGL(rope_table_kernel, dim3(256), dim3(256), 0, st, (double)theta, hd, n_pos, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_sample_partials(const SampleArgs& a, int n_chunks, hipStream_t st) {
+  if (a.R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(sample_partials_kernel, dim3(n_chunks, a.R), dim3(kNT), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_sample_finish(const FinishArgs& a, hipStream_t st) {
+  if (a.R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(sample_finish_kernel, dim3(a.R), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_replicate(int dt, void* kc, void* vc, int n_layers, long layer_stride,
+                               long slot_stride, int nkv, int hd, int ctx_stride, int src,
+                               int dst0, int n_dst, int n_pos, hipStream_t st) {
+  if (n_dst <= 0 || n_pos <= 0) return hipSuccess;
+  dim3 grid(n_layers * nkv, n_dst);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL((kv_replicate_kernel<bf16_t>), grid, dim3(kNT), 0, st, (bf16_t*)kc, (bf16_t*)vc,
+                       nkv, hd, ctx_stride, layer_stride, slot_stride, src, dst0, n_pos);
+  else
+    hipLaunchKernelGGL((kv_replicate_kernel<float>), grid, dim3(kNT), 0, st, (float*)kc, (float*)vc,
+                       nkv, hd, ctx_stride, layer_stride, slot_stride, src, dst0, n_pos);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_state(const InitStateArgs& a, hipStream_t st) {
+  if (a.n_seq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(init_state_kernel, dim3((a.n_seq + 255) / 256), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_count_active(const int32_t* done, int n, int32_t* out, hipStream_t st) {
+  hipLaunchKernelGGL(count_active_kernel, dim3(1), dim3(kNT), 0, st, done, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_i32(const int32_t* src, const int32_t* idx, int n, int32_t* dst, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, st, src, idx, n, dst);
+  return hipGetLastError();
+}
+
+}  // namespace tandem

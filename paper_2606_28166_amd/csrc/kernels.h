@@ -1,0 +1,132 @@
+// Host-side launchers of the gfx950 kernels (internal to libtandem).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tandem {
+
+enum DType { DT_BF16 = 0, DT_F32 = 1 };
+enum Epi { EPI_PARTIAL = 0, EPI_STORE = 1, EPI_SWIGLU = 2 };
+
+// C[M x N] = A[M x K] . W[N x K]^T, A fp32, W in the weight dtype.
+//   EPI_PARTIAL: split-K partial sums to out + split * split_stride, row stride ldo
+//   EPI_STORE:   out[m * ldo + n], splits must be 1
+//   EPI_SWIGLU:  W has 2N rows (gate rows then up rows); out[m * ldo + j] =
+//                silu(gate_j) * up_j for j < N
+// splits is the number of K slices (>= 1); *splits_used returns the number
+// actually used (may be lower when K is short).
+struct GemmArgs {
+  int dt;                 // weight dtype
+  const float* A;         // activations [M][K]
+  const void* W;          // weights [rows][K]
+  int M, N, K;
+  int epi;
+  float* out;
+  int ldo;
+  long split_stride;
+  int splits;
+};
+hipError_t launch_gemm(const GemmArgs& a, int* splits_used, hipStream_t st);
+
+// The K dimension granule of the MFMA path; other K use the VALU path.
+constexpr int kGemmBK = 64;
+
+// h[r] = E[tok[r]], x[r] = rmsnorm(h[r]) * gain (both fp32).
+hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, const float* gain,
+                             float eps, float* h, float* x, int R, hipStream_t st);
+
+// h[r] += sum_s ws[s][r] (fixed order), then x[r] = rmsnorm(h[r]) * gain.
+hipError_t launch_resid_norm(const float* ws, int S, long ws_stride, float* h,
+                             const float* gain, float eps, float* x, int R, int d, hipStream_t st);
+
+struct CacheGeom {
+  void* k;                // layer base of the K cache  [slot][kvh][ctx_stride][hd]
+  void* v;                // layer base of the V cache  [slot][kvh][hd][ctx_stride] (transposed)
+  int ctx_stride;
+  long slot_stride;       // elements between slots (= n_kv * ctx_stride * hd)
+};
+
+// Sum the QKV split-K partials, per-head RMSNorm of q and k (optional), RoPE,
+// write q (fp32) and append k, v to the cache (weight dtype, rounded to
+// nearest even for bf16) at (slot, pos).
+struct QkvPostArgs {
+  int dt;
+  const float* ws; int S; long ws_stride;
+  int R, nq, nkv, hd;
+  const float* q_norm; const float* k_norm; float eps;
+  const float2* rope;     // [ctx_stride][hd/2] (cos, sin)
+  const int32_t* row_slot; const int32_t* row_pos; const int32_t* row_done;
+  float* q_out;           // [R][nq][hd]
+  CacheGeom cache;
+};
+hipError_t launch_qkv_post(const QkvPostArgs& a, hipStream_t st);
+
+// Decode/prefill attention of every row's query heads over positions
+// 0..row_pos[r] of its slot; out[r][h * hd + d] (fp32).
+struct AttnArgs {
+  int dt;
+  const float* q; int R, nq, nkv, hd;
+  CacheGeom cache;
+  const int32_t* row_slot; const int32_t* row_pos; const int32_t* row_done;
+  float* out;
+};
+hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
+
+// rope table [n_pos][hd/2] of (cos, sin)(pos * theta^(-2i/hd)), computed in fp64.
+hipError_t launch_rope_table(float theta, int hd, int n_pos, float2* out, hipStream_t st);
+
+// Sampling.
+struct SampleArgs {
+  const float* z_sen;     // [R][V]
+  const float* z_jun;     // [R][V]
+  int R, V;
+  float temp; int eos_id; float eos_bias_sen, eos_bias_jun;
+  uint32_t key0, key1;
+  const int32_t* owner; const int32_t* t; const int32_t* done;   // per sequence (row == seq)
+  float* partials;        // [R][n_chunks][5]
+  int chunk;              // vocab entries per chunk
+};
+hipError_t launch_sample_partials(const SampleArgs& a, int n_chunks, hipStream_t st);
+
+struct FinishArgs {
+  const float* z_sen; int R, V;
+  float temp; int eos_id; float eos_bias_sen;
+  const float* partials; int n_chunks;
+  const int32_t* forced;                      // [R] or NULL
+  uint32_t key0, key1; unsigned long long thr; int mode; int cap_k;
+  const uint32_t* bnd;                        // NULL = all boundaries
+  int max_new;
+  int32_t* owner; int32_t* c; int32_t* t; int32_t* pos; int32_t* pending; int32_t* done;
+  int32_t* out_tok; uint8_t* out_own; float* out_lp; int32_t* out_len; int ld_out;
+  int32_t* dbg_sampled; float* dbg_margin;
+  int32_t* n_active;                          // device counter or NULL
+};
+hipError_t launch_sample_finish(const FinishArgs& a, hipStream_t st);
+
+// Copy positions [0, n_pos) of slot src into slots dst0 .. dst0 + n_dst - 1
+// for every layer and kv head (K and transposed V).
+hipError_t launch_kv_replicate(int dt, void* kc, void* vc, int n_layers, long layer_stride,
+                               long slot_stride, int nkv, int hd, int ctx_stride, int src,
+                               int dst0, int n_dst, int n_pos, hipStream_t st);
+
+// Per-sequence state after prefill.
+struct InitStateArgs {
+  int n_seq, G;
+  const int32_t* prompt_tokens; const int32_t* prompt_end;   // device [n_prompts] exclusive ends
+  const int32_t* prompt_len;                                 // device [n_prompts]
+  uint32_t key0, key1; unsigned long long thr; int first_owner;
+  int32_t* owner; int32_t* c; int32_t* t; int32_t* pos; int32_t* pending; int32_t* done;
+  int32_t* out_len;
+};
+hipError_t launch_init_state(const InitStateArgs& a, hipStream_t st);
+
+hipError_t launch_count_active(const int32_t* done, int n, int32_t* out, hipStream_t st);
+
+// dst[i] = src[idx[i]]
+hipError_t launch_gather_i32(const int32_t* src, const int32_t* idx, int n, int32_t* dst, hipStream_t st);
+
+// true when the MFMA attention kernel covers this (dtype, head_dim, group size)
+bool attention_has_mfma(int dt, int hd, int gqa);
+
+}  // namespace tandem

@@ -1,0 +1,690 @@
+// libtandem: C ABI and host runtime of the tandem co-generation step.
+//
+// One handle holds a senior and a junior decoder (borrowed device weights),
+// one KV cache per model inside the caller's KV arena, activation and
+// per-sequence state buffers inside the caller's scratch buffer, and the
+// caller's stream.  A step forwards the pending token of every sequence
+// through BOTH models (each appends to its own cache: the caches stay in
+// lockstep with the shared history), samples the owner's next token,
+// records (token, authorship bit, senior log-prob) and applies the handoff
+// rule — the rollout half of Algorithm 1, one token at a time for all
+// sequences of the batch.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "tandem.h"
+#include "kernels.h"
+
+using namespace tandem;
+
+namespace {
+
+thread_local std::string g_err = "no error";
+
+constexpr int kSplitMax = 8;          // split-K slices of a decode projection
+constexpr int kTargetGroups = 512;    // workgroups a projection launch aims for
+constexpr int kVocabChunk = 4096;     // vocabulary entries per sampling workgroup
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct Layer {
+  const float* attn_norm;
+  const void* w_qkv;
+  const float* q_norm;
+  const float* k_norm;
+  const void* w_o;
+  const float* ffn_norm;
+  const void* w_gate_up;
+  const void* w_down;
+};
+
+struct ModelPlan {            // byte offsets / sizes of one model's buffers
+  size_t esz;
+  int qkv_dim, att_dim, rmax;
+  size_t ws_floats;
+  size_t kv_half;             // bytes of the K (= V) cache
+  size_t off_h, off_xa, off_xf, off_q, off_ws, off_logits, off_rope;
+};
+
+struct Plan {
+  int ctx_stride;
+  int n_chunks;
+  ModelPlan m[2];
+  size_t kv_bytes;
+  size_t off_state, off_seq_slot, off_rows, off_prompt, off_partials, off_count;
+  size_t scratch_bytes;
+};
+
+struct Model {
+  tandem_model_cfg cfg;
+  ModelPlan p;
+  const void* embed;
+  std::vector<Layer> layers;
+  const float* final_norm;
+  const void* lm_head;
+  char* kc;
+  char* vc;
+  long layer_stride;          // elements
+  long slot_stride;           // elements
+  float* h;
+  float* xa;
+  float* xf;
+  float* q;
+  float* ws;
+  float* logits;
+  float2* rope;
+};
+
+tandem_status fail(std::string* where, tandem_status s, const std::string& msg) {
+  if (where) *where = msg;
+  g_err = msg;
+  return s;
+}
+
+tandem_status check_cfg(const tandem_model_cfg* c, const char* who, std::string* err) {
+  char b[256];
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->head_dim < 1 ||
+      c->ffn_dim < 1 || c->vocab < 2) {
+    snprintf(b, sizeof b, "%s: every size must be positive (vocab >= 2)", who);
+    return fail(err, TANDEM_E_SHAPE, b);
+  }
+  if (c->n_q_heads % c->n_kv_heads != 0) {
+    snprintf(b, sizeof b, "%s: n_q_heads (%d) must be a multiple of n_kv_heads (%d)", who, c->n_q_heads,
+             c->n_kv_heads);
+    return fail(err, TANDEM_E_SHAPE, b);
+  }
+  if (c->weight_dtype != TANDEM_BF16 && c->weight_dtype != TANDEM_F32) {
+    snprintf(b, sizeof b, "%s: weight_dtype must be TANDEM_BF16 or TANDEM_F32", who);
+    return fail(err, TANDEM_E_ARG, b);
+  }
+  if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128) {
+    snprintf(b, sizeof b, "%s: head_dim %d unsupported (32, 64 or 128)", who, c->head_dim);
+    return fail(err, TANDEM_E_UNSUPPORTED, b);
+  }
+  if (c->d_model > 8192 || (long)(c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim > 16384) {
+    snprintf(b, sizeof b, "%s: d_model <= 8192 and (n_q + 2 n_kv) * head_dim <= 16384 required", who);
+    return fail(err, TANDEM_E_UNSUPPORTED, b);
+  }
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f) || !std::isfinite(c->rope_theta)) {
+    snprintf(b, sizeof b, "%s: rms_eps must be >= 0 and rope_theta finite and > 0", who);
+    return fail(err, TANDEM_E_ARG, b);
+  }
+  return TANDEM_OK;
+}
+
+tandem_status check_cap(const tandem_capacity* cap, std::string* err) {
+  if (cap->max_seqs < 1 || cap->max_ctx < 1 || cap->max_prefill_tokens < 1)
+    return fail(err, TANDEM_E_CAPACITY, "capacity: max_seqs, max_ctx and max_prefill_tokens must be >= 1");
+  if (cap->max_ctx > (1 << 24) || cap->max_seqs > (1 << 24) || cap->max_prefill_tokens > (1 << 24))
+    return fail(err, TANDEM_E_CAPACITY, "capacity: sizes above 2^24 are not supported");
+  return TANDEM_OK;
+}
+
+Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const tandem_capacity* cap) {
+  Plan P{};
+  P.ctx_stride = (int)align_up((size_t)cap->max_ctx, 64);
+  P.n_chunks = (sen->vocab + kVocabChunk - 1) / kVocabChunk;
+  const tandem_model_cfg* cf[2] = {sen, jun};
+  size_t kv = 0, sc = 0;
+  for (int i = 0; i < 2; ++i) {
+    const tandem_model_cfg* c = cf[i];
+    ModelPlan& m = P.m[i];
+    m.esz = c->weight_dtype == TANDEM_BF16 ? 2 : 4;
+    m.qkv_dim = (c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim;
+    m.att_dim = c->n_q_heads * c->head_dim;
+    m.rmax = cap->max_seqs > cap->max_prefill_tokens ? cap->max_seqs : cap->max_prefill_tokens;
+    const size_t nmax = (size_t)(m.qkv_dim > c->d_model ? m.qkv_dim : c->d_model);
+    const size_t rows_ws = (size_t)kSplitMax * cap->max_seqs > (size_t)cap->max_prefill_tokens
+                               ? (size_t)kSplitMax * cap->max_seqs
+                               : (size_t)cap->max_prefill_tokens;
+    m.ws_floats = rows_ws * nmax;
+    m.kv_half = align_up((size_t)c->n_layers * cap->max_seqs * c->n_kv_heads * P.ctx_stride * c->head_dim * m.esz,
+                         kAlign);
+    kv += 2 * m.kv_half;
+    const size_t R = (size_t)m.rmax;
+    const size_t xa_w = (size_t)(m.att_dim > c->d_model ? m.att_dim : c->d_model);
+    m.off_h = sc; sc = align_up(sc + R * c->d_model * 4, kAlign);
+    m.off_xa = sc; sc = align_up(sc + R * xa_w * 4, kAlign);
+    m.off_xf = sc; sc = align_up(sc + R * c->ffn_dim * 4, kAlign);
+    m.off_q = sc; sc = align_up(sc + R * m.att_dim * 4, kAlign);
+    m.off_ws = sc; sc = align_up(sc + m.ws_floats * 4, kAlign);
+    m.off_logits = sc; sc = align_up(sc + (size_t)cap->max_seqs * c->vocab * 4, kAlign);
+    m.off_rope = sc; sc = align_up(sc + (size_t)P.ctx_stride * (c->head_dim / 2) * 8, kAlign);
+  }
+  P.kv_bytes = kv;
+  const size_t S = (size_t)cap->max_seqs;
+  P.off_state = sc; sc = align_up(sc + 6 * S * 4, kAlign);
+  P.off_seq_slot = sc; sc = align_up(sc + S * 4, kAlign);
+  P.off_rows = sc; sc = align_up(sc + 4 * (size_t)cap->max_prefill_tokens * 4, kAlign);
+  P.off_prompt = sc; sc = align_up(sc + 2 * S * 4, kAlign);
+  P.off_partials = sc; sc = align_up(sc + S * P.n_chunks * 5 * 4, kAlign);
+  P.off_count = sc; sc = align_up(sc + 4, kAlign);
+  P.scratch_bytes = sc;
+  return P;
+}
+
+}  // namespace
+
+struct tandem_handle {
+  Model m[2];                 // 0: senior, 1: junior
+  Plan plan;
+  tandem_switch_cfg sw;
+  tandem_sample_cfg smp;
+  tandem_capacity cap;
+  tandem_outputs out;
+  unsigned long long thr;
+  uint32_t key0, key1;
+  hipStream_t stream;
+  int32_t *owner, *c, *t, *pos, *pending, *done;
+  int32_t* seq_slot;
+  int32_t *row_slot, *row_pos, *row_tok, *row_src;
+  int32_t *p_end, *p_len;
+  float* partials;
+  int32_t* d_count;
+  int32_t* h_count;           // pinned
+  int n_seq = 0;
+  bool prefilled = false;
+  bool poisoned = false;
+  std::string err = "no error";
+  std::vector<int32_t> hbuf;  // host staging of prefill metadata
+  // instrumentation: event pairs per kernel class
+  int timing = 0;             // class mask
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  std::vector<std::pair<int, size_t>> ev_marks[TANDEM_K_CLASSES];   // (class, index of the begin event)
+};
+
+namespace {
+
+// Record a begin event for a kernel class (no-op unless timing is enabled).
+hipError_t tim_begin(tandem_handle* h, int klass, size_t* idx) {
+  *idx = SIZE_MAX;
+  if (!(h->timing & (1 << klass))) return hipSuccess;
+  while (h->ev_pool.size() < h->ev_used + 2) {
+    hipEvent_t e;
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) return r;
+    h->ev_pool.push_back(e);
+  }
+  *idx = h->ev_used;
+  h->ev_used += 2;
+  h->ev_marks[klass].push_back({klass, *idx});
+  return hipEventRecord(h->ev_pool[*idx], h->stream);
+}
+hipError_t tim_end(tandem_handle* h, size_t idx) {
+  if (idx == SIZE_MAX) return hipSuccess;
+  return hipEventRecord(h->ev_pool[idx + 1], h->stream);
+}
+
+}  // namespace
+
+// Launch one kernel class between timing events.
+#define TIMED(klass, expr)                                                                 \
+  do {                                                                                     \
+    size_t ti_ = 0;                                                                        \
+    HIPCHK(tim_begin(h, (klass), &ti_));                                                   \
+    HIPCHK(expr);                                                                          \
+    HIPCHK(tim_end(h, ti_));                                                               \
+  } while (0)
+
+#define HIPCHK(expr)                                                                       \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess) {                                                                \
+      h->poisoned = true;                                                                  \
+      return fail(&h->err, TANDEM_E_HIP, std::string("HIP error in ") + #expr + ": " +     \
+                                             hipGetErrorString(e_));                       \
+    }                                                                                      \
+  } while (0)
+
+namespace {
+
+int choose_splits(int M, int N, int K, size_t ws_floats) {
+  const int m_tiles = (M + 127) / 128, n_tiles = (N + 127) / 128;
+  const int base = m_tiles * n_tiles;
+  int S = (kTargetGroups + base - 1) / base;
+  // keep the partial-sum traffic (S * M * N * 4 bytes) below half the weight bytes (N * K * 2)
+  const int traffic_cap = K / (4 * (M > 0 ? M : 1));
+  if (S > traffic_cap) S = traffic_cap;
+  if (S > kSplitMax) S = kSplitMax;
+  const size_t cap_ws = ws_floats / ((size_t)M * N);
+  if ((size_t)S > cap_ws) S = (int)cap_ws;
+  if (S < 1) S = 1;
+  return S;
+}
+
+// Forward R rows through one model.  Rows read their token, cache slot and
+// position from the row arrays; done rows (row_done != NULL) skip the cache
+// append and produce zero attention.  With lm_head the logits land in m.logits.
+tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok, const int32_t* row_slot,
+                      const int32_t* row_pos, const int32_t* row_done, bool lm_head) {
+  const tandem_model_cfg& c = m.cfg;
+  const int dt = c.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32;
+  const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads;
+  const int qkv = m.p.qkv_dim, att = m.p.att_dim;
+  hipStream_t st = h->stream;
+  TIMED(TANDEM_K_OTHER, launch_embed_norm(dt, row_tok, m.embed, d, m.layers[0].attn_norm, c.rms_eps, m.h, m.xa, R, st));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const Layer& L = m.layers[l];
+    CacheGeom cg;
+    cg.k = m.kc + (size_t)l * m.layer_stride * m.p.esz;
+    cg.v = m.vc + (size_t)l * m.layer_stride * m.p.esz;
+    cg.ctx_stride = h->plan.ctx_stride;
+    cg.slot_stride = m.slot_stride;
+
+    GemmArgs g{};
+    g.dt = dt;
+    g.A = m.xa; g.W = L.w_qkv; g.M = R; g.N = qkv; g.K = d; g.epi = EPI_PARTIAL;
+    g.out = m.ws; g.ldo = qkv; g.split_stride = (long)R * qkv;
+    g.splits = choose_splits(R, qkv, d, m.p.ws_floats);
+    int S = 1;
+    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+
+    QkvPostArgs qp{};
+    qp.dt = dt; qp.ws = m.ws; qp.S = S; qp.ws_stride = (long)R * qkv;
+    qp.R = R; qp.nq = nq; qp.nkv = nkv; qp.hd = hd;
+    qp.q_norm = c.qk_norm ? L.q_norm : nullptr; qp.k_norm = c.qk_norm ? L.k_norm : nullptr;
+    qp.eps = c.rms_eps; qp.rope = m.rope;
+    qp.row_slot = row_slot; qp.row_pos = row_pos; qp.row_done = row_done;
+    qp.q_out = m.q; qp.cache = cg;
+    TIMED(TANDEM_K_OTHER, launch_qkv_post(qp, st));
+
+    AttnArgs aa{};
+    aa.dt = dt; aa.q = m.q; aa.R = R; aa.nq = nq; aa.nkv = nkv; aa.hd = hd; aa.cache = cg;
+    aa.row_slot = row_slot; aa.row_pos = row_pos; aa.row_done = row_done; aa.out = m.xa;
+    TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
+
+    g = GemmArgs{};
+    g.dt = dt; g.A = m.xa; g.W = L.w_o; g.M = R; g.N = d; g.K = att; g.epi = EPI_PARTIAL;
+    g.out = m.ws; g.ldo = d; g.split_stride = (long)R * d;
+    g.splits = choose_splits(R, d, att, m.p.ws_floats);
+    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+    TIMED(TANDEM_K_OTHER, launch_resid_norm(m.ws, S, (long)R * d, m.h, L.ffn_norm, c.rms_eps, m.xa, R, d, st));
+
+    g = GemmArgs{};
+    g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = R; g.N = c.ffn_dim; g.K = d; g.epi = EPI_SWIGLU;
+    g.out = m.xf; g.ldo = c.ffn_dim; g.splits = 1;
+    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+
+    g = GemmArgs{};
+    g.dt = dt; g.A = m.xf; g.W = L.w_down; g.M = R; g.N = d; g.K = c.ffn_dim; g.epi = EPI_PARTIAL;
+    g.out = m.ws; g.ldo = d; g.split_stride = (long)R * d;
+    g.splits = choose_splits(R, d, c.ffn_dim, m.p.ws_floats);
+    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+    const float* next_gain = (l + 1 < c.n_layers) ? m.layers[l + 1].attn_norm : m.final_norm;
+    TIMED(TANDEM_K_OTHER, launch_resid_norm(m.ws, S, (long)R * d, m.h, next_gain, c.rms_eps, m.xa, R, d, st));
+  }
+  if (lm_head) {
+    GemmArgs g{};
+    g.dt = dt; g.A = m.xa; g.W = m.lm_head; g.M = R; g.N = c.vocab; g.K = d; g.epi = EPI_STORE;
+    g.out = m.logits; g.ldo = c.vocab; g.splits = 1;
+    int S = 1;
+    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+  }
+  return TANDEM_OK;
+}
+
+tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg, int32_t* n_active) {
+  if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
+  if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
+  if (!h->prefilled) return fail(&h->err, TANDEM_E_STATE, "tandem_step before tandem_prefill");
+  const int R = h->n_seq;
+  hipStream_t st = h->stream;
+  for (int i = 0; i < 2; ++i) {
+    tandem_status s = forward(h, h->m[i], R, h->pending, h->seq_slot, h->pos, h->done, true);
+    if (s != TANDEM_OK) return s;
+  }
+  const int V = h->m[0].cfg.vocab;
+  SampleArgs sa{};
+  sa.z_sen = h->m[0].logits; sa.z_jun = h->m[1].logits; sa.R = R; sa.V = V;
+  sa.temp = h->smp.temperature; sa.eos_id = h->smp.eos_id;
+  sa.eos_bias_sen = h->smp.eos_bias_senior; sa.eos_bias_jun = h->smp.eos_bias_junior;
+  sa.key0 = h->key0; sa.key1 = h->key1;
+  sa.owner = h->owner; sa.t = h->t; sa.done = h->done;
+  sa.partials = h->partials; sa.chunk = kVocabChunk;
+  TIMED(TANDEM_K_SAMPLE, launch_sample_partials(sa, h->plan.n_chunks, st));
+  if (dbg) {
+    if (dbg->logits_senior)
+      HIPCHK(hipMemcpyAsync(dbg->logits_senior, h->m[0].logits, (size_t)R * V * 4, hipMemcpyDeviceToDevice, st));
+    if (dbg->logits_junior)
+      HIPCHK(hipMemcpyAsync(dbg->logits_junior, h->m[1].logits, (size_t)R * V * 4, hipMemcpyDeviceToDevice, st));
+  }
+  FinishArgs fa{};
+  fa.z_sen = h->m[0].logits; fa.R = R; fa.V = V;
+  fa.temp = h->smp.temperature; fa.eos_id = h->smp.eos_id; fa.eos_bias_sen = h->smp.eos_bias_senior;
+  fa.partials = h->partials; fa.n_chunks = h->plan.n_chunks;
+  fa.forced = forced;
+  fa.key0 = h->key0; fa.key1 = h->key1; fa.thr = h->thr; fa.mode = h->sw.mode; fa.cap_k = h->sw.cap_k;
+  fa.bnd = h->sw.boundary_bits; fa.max_new = h->smp.max_new_tokens;
+  fa.owner = h->owner; fa.c = h->c; fa.t = h->t; fa.pos = h->pos; fa.pending = h->pending; fa.done = h->done;
+  fa.out_tok = h->out.tokens; fa.out_own = h->out.owner; fa.out_lp = h->out.senior_logprob;
+  fa.out_len = h->out.length; fa.ld_out = h->smp.max_new_tokens;
+  fa.dbg_sampled = dbg ? dbg->sampled : nullptr; fa.dbg_margin = dbg ? dbg->margin : nullptr;
+  TIMED(TANDEM_K_SAMPLE, launch_sample_finish(fa, st));
+  if (n_active) {
+    HIPCHK(launch_count_active(h->done, R, h->d_count, st));
+    HIPCHK(hipMemcpyAsync(h->h_count, h->d_count, 4, hipMemcpyDeviceToHost, st));
+    HIPCHK(hipStreamSynchronize(st));
+    *n_active = *h->h_count;
+  }
+  return TANDEM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tandem_status_string(tandem_status s) {
+  switch (s) {
+    case TANDEM_OK: return "TANDEM_OK";
+    case TANDEM_E_ARG: return "TANDEM_E_ARG";
+    case TANDEM_E_SHAPE: return "TANDEM_E_SHAPE";
+    case TANDEM_E_CAPACITY: return "TANDEM_E_CAPACITY";
+    case TANDEM_E_STATE: return "TANDEM_E_STATE";
+    case TANDEM_E_HIP: return "TANDEM_E_HIP";
+    case TANDEM_E_UNSUPPORTED: return "TANDEM_E_UNSUPPORTED";
+  }
+  return "TANDEM_E_UNKNOWN";
+}
+
+const char* tandem_last_error(const tandem_handle* h) { return h ? h->err.c_str() : g_err.c_str(); }
+
+tandem_status tandem_workspace_size(const tandem_model_cfg* senior, const tandem_model_cfg* junior,
+                                    const tandem_capacity* cap, size_t* kv_bytes, size_t* scratch_bytes) {
+  if (!senior || !junior || !cap || !kv_bytes || !scratch_bytes)
+    return fail(nullptr, TANDEM_E_ARG, "tandem_workspace_size: NULL argument");
+  tandem_status s;
+  if ((s = check_cfg(senior, "senior", nullptr)) != TANDEM_OK) return s;
+  if ((s = check_cfg(junior, "junior", nullptr)) != TANDEM_OK) return s;
+  if (senior->vocab != junior->vocab)
+    return fail(nullptr, TANDEM_E_SHAPE, "senior and junior must share one vocabulary");
+  if ((s = check_cap(cap, nullptr)) != TANDEM_OK) return s;
+  Plan P = make_plan(senior, junior, cap);
+  *kv_bytes = P.kv_bytes;
+  *scratch_bytes = P.scratch_bytes;
+  return TANDEM_OK;
+}
+
+tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior, const tandem_switch_cfg* sw,
+                          const tandem_sample_cfg* smp, const tandem_capacity* cap, void* kv_arena,
+                          size_t kv_bytes, void* scratch, size_t scratch_bytes, const tandem_outputs* out,
+                          void* stream, tandem_handle** out_handle) {
+  if (!out_handle) return fail(nullptr, TANDEM_E_ARG, "tandem_init: out_handle is NULL");
+  *out_handle = nullptr;
+  if (!senior || !junior || !sw || !smp || !cap || !out)
+    return fail(nullptr, TANDEM_E_ARG, "tandem_init: NULL argument");
+  tandem_status s;
+  if ((s = check_cfg(&senior->cfg, "senior", nullptr)) != TANDEM_OK) return s;
+  if ((s = check_cfg(&junior->cfg, "junior", nullptr)) != TANDEM_OK) return s;
+  if (senior->cfg.vocab != junior->cfg.vocab)
+    return fail(nullptr, TANDEM_E_SHAPE, "senior and junior must share one vocabulary");
+  if ((s = check_cap(cap, nullptr)) != TANDEM_OK) return s;
+  const tandem_model* md[2] = {senior, junior};
+  for (int i = 0; i < 2; ++i) {
+    const tandem_model* m = md[i];
+    if (!m->embed || !m->layers || !m->final_norm || !m->lm_head)
+      return fail(nullptr, TANDEM_E_ARG, "tandem_init: a model weight pointer is NULL");
+    for (int l = 0; l < m->cfg.n_layers; ++l) {
+      const void* const* p = m->layers + 8 * l;
+      if (!p[0] || !p[1] || !p[4] || !p[5] || !p[6] || !p[7] || (m->cfg.qk_norm && (!p[2] || !p[3])))
+        return fail(nullptr, TANDEM_E_ARG, "tandem_init: a layer weight pointer is NULL");
+    }
+  }
+  if (sw->mode < TANDEM_REDRAW || sw->mode > TANDEM_ALTERNATE)
+    return fail(nullptr, TANDEM_E_ARG, "switch mode must be REDRAW, SWITCH or ALTERNATE");
+  if (!(sw->p >= 0.0 && sw->p <= 1.0)) return fail(nullptr, TANDEM_E_ARG, "switch p must lie in [0, 1]");
+  if (sw->first_owner < TANDEM_JUNIOR || sw->first_owner > TANDEM_DRAW)
+    return fail(nullptr, TANDEM_E_ARG, "first_owner must be JUNIOR, SENIOR or DRAW");
+  if (!(smp->temperature > 0.f) || !std::isfinite(smp->temperature))
+    return fail(nullptr, TANDEM_E_ARG, "temperature must be finite and > 0");
+  if (smp->eos_id >= senior->cfg.vocab) return fail(nullptr, TANDEM_E_ARG, "eos_id must be < vocab");
+  if (smp->max_new_tokens < 1) return fail(nullptr, TANDEM_E_ARG, "max_new_tokens must be >= 1");
+  if (smp->max_new_tokens > cap->max_ctx)
+    return fail(nullptr, TANDEM_E_CAPACITY, "max_new_tokens exceeds max_ctx");
+  if (!out->tokens || !out->owner || !out->senior_logprob || !out->length)
+    return fail(nullptr, TANDEM_E_ARG, "tandem_init: an output arena is NULL");
+  if (!kv_arena || !scratch) return fail(nullptr, TANDEM_E_ARG, "tandem_init: kv_arena or scratch is NULL");
+  if (((uintptr_t)kv_arena % kAlign) || ((uintptr_t)scratch % kAlign))
+    return fail(nullptr, TANDEM_E_ARG, "kv_arena and scratch must be 256-byte aligned");
+  Plan P = make_plan(&senior->cfg, &junior->cfg, cap);
+  if (kv_bytes < P.kv_bytes || scratch_bytes < P.scratch_bytes)
+    return fail(nullptr, TANDEM_E_CAPACITY, "kv_arena or scratch smaller than tandem_workspace_size");
+
+  tandem_handle* h = new tandem_handle();
+  h->plan = P;
+  h->sw = *sw;
+  h->smp = *smp;
+  h->cap = *cap;
+  h->out = *out;
+  h->stream = (hipStream_t)stream;
+  const double thr = std::floor(sw->p * 4294967296.0);
+  h->thr = thr >= 4294967296.0 ? (1ull << 32) : (unsigned long long)thr;
+  h->key0 = (uint32_t)(smp->seed & 0xFFFFFFFFull);
+  h->key1 = (uint32_t)(smp->seed >> 32);
+  char* kv = (char*)kv_arena;
+  char* sc = (char*)scratch;
+  size_t kv_off = 0;
+  for (int i = 0; i < 2; ++i) {
+    Model& m = h->m[i];
+    const tandem_model* src = md[i];
+    m.cfg = src->cfg;
+    m.p = P.m[i];
+    m.embed = src->embed;
+    m.final_norm = (const float*)src->final_norm;
+    m.lm_head = src->lm_head;
+    m.layers.resize(m.cfg.n_layers);
+    for (int l = 0; l < m.cfg.n_layers; ++l) {
+      const void* const* p = src->layers + 8 * l;
+      m.layers[l] = Layer{(const float*)p[0], p[1], (const float*)p[2], (const float*)p[3],
+                          p[4], (const float*)p[5], p[6], p[7]};
+    }
+    m.slot_stride = (long)m.cfg.n_kv_heads * P.ctx_stride * m.cfg.head_dim;
+    m.layer_stride = (long)cap->max_seqs * m.slot_stride;
+    m.kc = kv + kv_off;
+    m.vc = kv + kv_off + m.p.kv_half;
+    kv_off += 2 * m.p.kv_half;
+    m.h = (float*)(sc + m.p.off_h);
+    m.xa = (float*)(sc + m.p.off_xa);
+    m.xf = (float*)(sc + m.p.off_xf);
+    m.q = (float*)(sc + m.p.off_q);
+    m.ws = (float*)(sc + m.p.off_ws);
+    m.logits = (float*)(sc + m.p.off_logits);
+    m.rope = (float2*)(sc + m.p.off_rope);
+  }
+  const size_t S = (size_t)cap->max_seqs;
+  int32_t* stt = (int32_t*)(sc + P.off_state);
+  h->owner = stt; h->c = stt + S; h->t = stt + 2 * S; h->pos = stt + 3 * S; h->pending = stt + 4 * S;
+  h->done = stt + 5 * S;
+  h->seq_slot = (int32_t*)(sc + P.off_seq_slot);
+  int32_t* rows = (int32_t*)(sc + P.off_rows);
+  const size_t PT = (size_t)cap->max_prefill_tokens;
+  h->row_slot = rows; h->row_pos = rows + PT; h->row_tok = rows + 2 * PT; h->row_src = rows + 3 * PT;
+  int32_t* pr = (int32_t*)(sc + P.off_prompt);
+  h->p_end = pr; h->p_len = pr + S;
+  h->partials = (float*)(sc + P.off_partials);
+  h->d_count = (int32_t*)(sc + P.off_count);
+  h->h_count = nullptr;
+
+  // --- HIP work from here on
+  auto bail = [&](hipError_t e, const char* what) {
+    std::string msg = std::string("HIP error in tandem_init (") + what + "): " + hipGetErrorString(e);
+    if (h->h_count) (void)hipHostFree(h->h_count);
+    delete h;
+    return fail(nullptr, TANDEM_E_HIP, msg);
+  };
+  hipError_t e = hipHostMalloc((void**)&h->h_count, 4, hipHostMallocDefault);
+  if (e != hipSuccess) { h->h_count = nullptr; return bail(e, "hipHostMalloc"); }
+  for (int i = 0; i < 2; ++i) {
+    e = launch_rope_table(h->m[i].cfg.rope_theta, h->m[i].cfg.head_dim, P.ctx_stride, h->m[i].rope, h->stream);
+    if (e != hipSuccess) return bail(e, "rope table");
+  }
+  std::vector<int32_t> ident(S);
+  for (size_t i = 0; i < S; ++i) ident[i] = (int32_t)i;
+  e = hipMemcpyAsync(h->seq_slot, ident.data(), S * 4, hipMemcpyHostToDevice, h->stream);
+  if (e != hipSuccess) return bail(e, "seq slots");
+  e = hipMemsetAsync(stt, 0, 6 * S * 4, h->stream);
+  if (e != hipSuccess) return bail(e, "state");
+  e = hipStreamSynchronize(h->stream);
+  if (e != hipSuccess) return bail(e, "synchronize");
+  *out_handle = h;
+  return TANDEM_OK;
+}
+
+tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, const int32_t* prompt_offsets,
+                             int32_t n_prompts, int32_t G) {
+  if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
+  if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
+  if (!prompt_tokens || !prompt_offsets) return fail(&h->err, TANDEM_E_ARG, "prefill: NULL prompts");
+  if (n_prompts < 1 || G < 1) return fail(&h->err, TANDEM_E_ARG, "prefill: n_prompts and G must be >= 1");
+  if ((long)n_prompts * G > h->cap.max_seqs)
+    return fail(&h->err, TANDEM_E_CAPACITY, "prefill: n_prompts * G exceeds max_seqs");
+  if (prompt_offsets[0] != 0) return fail(&h->err, TANDEM_E_ARG, "prefill: prompt_offsets[0] must be 0");
+  for (int j = 0; j < n_prompts; ++j) {
+    const int P = prompt_offsets[j + 1] - prompt_offsets[j];
+    if (P < 1) return fail(&h->err, TANDEM_E_ARG, "prefill: every prompt needs at least one token");
+    if ((long)P - 1 + h->smp.max_new_tokens > h->cap.max_ctx)
+      return fail(&h->err, TANDEM_E_CAPACITY, "prefill: prompt length - 1 + max_new_tokens exceeds max_ctx");
+    if (P - 1 > h->cap.max_prefill_tokens)
+      return fail(&h->err, TANDEM_E_CAPACITY, "prefill: a prompt is longer than max_prefill_tokens + 1");
+  }
+  hipStream_t st = h->stream;
+  h->prefilled = false;
+  const int n_seq = n_prompts * G;
+  {
+    // token ids index the embedding tables: check them on the host before any kernel reads them
+    std::vector<int32_t> toks((size_t)prompt_offsets[n_prompts]);
+    HIPCHK(hipStreamSynchronize(st));
+    HIPCHK(hipMemcpy(toks.data(), prompt_tokens, toks.size() * 4, hipMemcpyDeviceToHost));
+    const int V = h->m[0].cfg.vocab;
+    for (int32_t tk : toks)
+      if (tk < 0 || tk >= V) return fail(&h->err, TANDEM_E_ARG, "prefill: a prompt token id is outside [0, vocab)");
+  }
+  // prompt metadata
+  h->hbuf.assign(2 * (size_t)n_prompts, 0);
+  for (int j = 0; j < n_prompts; ++j) {
+    h->hbuf[j] = prompt_offsets[j + 1];
+    h->hbuf[n_prompts + j] = prompt_offsets[j + 1] - prompt_offsets[j];
+  }
+  HIPCHK(hipMemcpyAsync(h->p_end, h->hbuf.data(), (size_t)n_prompts * 4, hipMemcpyHostToDevice, st));
+  HIPCHK(hipMemcpyAsync(h->p_len, h->hbuf.data() + n_prompts, (size_t)n_prompts * 4, hipMemcpyHostToDevice, st));
+  HIPCHK(hipStreamSynchronize(st));
+  // chunks of whole prompts whose (P - 1) rows fit max_prefill_tokens
+  int j0 = 0;
+  std::vector<int32_t> rows;
+  while (j0 < n_prompts) {
+    int j1 = j0, nr = 0;
+    while (j1 < n_prompts) {
+      const int add = prompt_offsets[j1 + 1] - prompt_offsets[j1] - 1;
+      if (nr + add > h->cap.max_prefill_tokens) break;
+      nr += add;
+      ++j1;
+    }
+    if (nr > 0) {
+      rows.assign(3 * (size_t)nr, 0);
+      int r = 0;
+      for (int j = j0; j < j1; ++j) {
+        const int P = prompt_offsets[j + 1] - prompt_offsets[j];
+        for (int i = 0; i < P - 1; ++i, ++r) {
+          rows[r] = j * G;                            // slot of the prompt's first sequence
+          rows[nr + r] = i;                           // position
+          rows[2 * nr + r] = prompt_offsets[j] + i;   // source token index
+        }
+      }
+      HIPCHK(hipMemcpyAsync(h->row_slot, rows.data(), (size_t)nr * 4, hipMemcpyHostToDevice, st));
+      HIPCHK(hipMemcpyAsync(h->row_pos, rows.data() + nr, (size_t)nr * 4, hipMemcpyHostToDevice, st));
+      HIPCHK(hipMemcpyAsync(h->row_src, rows.data() + 2 * nr, (size_t)nr * 4, hipMemcpyHostToDevice, st));
+      TIMED(TANDEM_K_OTHER, launch_gather_i32(prompt_tokens, h->row_src, nr, h->row_tok, st));
+      for (int i = 0; i < 2; ++i) {
+        tandem_status s = forward(h, h->m[i], nr, h->row_tok, h->row_slot, h->row_pos, nullptr, false);
+        if (s != TANDEM_OK) return s;
+      }
+      for (int j = j0; j < j1; ++j) {
+        const int P = prompt_offsets[j + 1] - prompt_offsets[j];
+        if (P - 1 <= 0 || G <= 1) continue;
+        for (int i = 0; i < 2; ++i) {
+          Model& m = h->m[i];
+          TIMED(TANDEM_K_OTHER, launch_kv_replicate(m.cfg.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32, m.kc, m.vc,
+                                     m.cfg.n_layers, m.layer_stride, m.slot_stride, m.cfg.n_kv_heads,
+                                     m.cfg.head_dim, h->plan.ctx_stride, j * G, j * G + 1, G - 1, P - 1, st));
+        }
+      }
+      HIPCHK(hipStreamSynchronize(st));   // the host row arrays are reused by the next chunk
+    }
+    j0 = j1;
+  }
+  InitStateArgs is{};
+  is.n_seq = n_seq; is.G = G; is.prompt_tokens = prompt_tokens; is.prompt_end = h->p_end; is.prompt_len = h->p_len;
+  is.key0 = h->key0; is.key1 = h->key1; is.thr = h->thr; is.first_owner = h->sw.first_owner;
+  is.owner = h->owner; is.c = h->c; is.t = h->t; is.pos = h->pos; is.pending = h->pending; is.done = h->done;
+  is.out_len = h->out.length;
+  HIPCHK(launch_init_state(is, st));
+  h->n_seq = n_seq;
+  h->prefilled = true;
+  return TANDEM_OK;
+}
+
+tandem_status tandem_step(tandem_handle* h, int32_t* n_active) { return step_impl(h, nullptr, nullptr, n_active); }
+
+tandem_status tandem_step_forced(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg,
+                                 int32_t* n_active) {
+  if (h && !forced) return fail(&h->err, TANDEM_E_ARG, "tandem_step_forced: forced is NULL");
+  return step_impl(h, forced, dbg, n_active);
+}
+
+tandem_status tandem_get_state(tandem_handle* h, int32_t* owner, int32_t* c, int32_t* t, int32_t* pos,
+                               int32_t* done) {
+  if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
+  if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
+  if (!h->prefilled) return fail(&h->err, TANDEM_E_STATE, "tandem_get_state before tandem_prefill");
+  const size_t n = (size_t)h->n_seq * 4;
+  HIPCHK(hipStreamSynchronize(h->stream));
+  if (owner) HIPCHK(hipMemcpy(owner, h->owner, n, hipMemcpyDeviceToHost));
+  if (c) HIPCHK(hipMemcpy(c, h->c, n, hipMemcpyDeviceToHost));
+  if (t) HIPCHK(hipMemcpy(t, h->t, n, hipMemcpyDeviceToHost));
+  if (pos) HIPCHK(hipMemcpy(pos, h->pos, n, hipMemcpyDeviceToHost));
+  if (done) HIPCHK(hipMemcpy(done, h->done, n, hipMemcpyDeviceToHost));
+  return TANDEM_OK;
+}
+
+tandem_status tandem_timing_enable(tandem_handle* h, int32_t class_mask) {
+  if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
+  if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
+  HIPCHK(hipStreamSynchronize(h->stream));
+  h->timing = class_mask & ((1 << TANDEM_K_CLASSES) - 1);
+  h->ev_used = 0;
+  for (auto& v : h->ev_marks) v.clear();
+  return TANDEM_OK;
+}
+
+tandem_status tandem_timing_read(tandem_handle* h, int32_t kernel_class, double* total_ms, int64_t* launches) {
+  if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
+  if (kernel_class < 0 || kernel_class >= TANDEM_K_CLASSES || !total_ms || !launches)
+    return fail(&h->err, TANDEM_E_ARG, "tandem_timing_read: bad kernel class or NULL output");
+  if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
+  HIPCHK(hipStreamSynchronize(h->stream));
+  double ms = 0.0;
+  for (const auto& mk : h->ev_marks[kernel_class]) {
+    float e = 0.f;
+    HIPCHK(hipEventElapsedTime(&e, h->ev_pool[mk.second], h->ev_pool[mk.second + 1]));
+    ms += e;
+  }
+  *total_ms = ms;
+  *launches = (int64_t)h->ev_marks[kernel_class].size();
+  return TANDEM_OK;
+}
+
+void tandem_destroy(tandem_handle* h) {
+  if (!h) return;
+  (void)hipStreamSynchronize(h->stream);
+  for (hipEvent_t e : h->ev_pool) (void)hipEventDestroy(e);
+  if (h->h_count) (void)hipHostFree(h->h_count);
+  delete h;
+}
+
+}  // extern "C"

@@ -1,0 +1,117 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared
+symbol, and rejects bad arguments before touching HIP."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tandem.h")
+
+L = pytest.importorskip("paper_2606_28166_amd._lib", reason="libtandem.so not built")
+
+import workloads as W  # noqa: E402
+from paper_2606_28166_amd.engine import model_cfg  # noqa: E402
+
+
+def _declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(tandem_[a-z_]+)\s*\(", txt)))
+
+
+def test_header_symbols_are_exported():
+    names = _declared()
+    assert "tandem_init" in names and "tandem_step" in names
+    for n in names:
+        assert hasattr(L.lib, n), n
+    assert set(L.EXPORTS) == set(names)
+
+
+def _cfgs(name="small"):
+    wl = W.workload(name)
+    return model_cfg(wl.senior), model_cfg(wl.junior)
+
+
+def test_workspace_size_matches_layout():
+    s, j = _cfgs("qwen")
+    cap = L.Capacity(128, 256 - 1 + 2048, 4096)
+    kv, sc = L.tandem_workspace_size(s, j, cap)
+    ctx = ((2303 + 63) // 64) * 64
+    want_kv = 2 * 2 * 128 * ctx * 128 * 8 * (36 + 28)
+    assert kv == want_kv
+    assert sc > 128 * 151936 * 4 * 2
+
+
+@pytest.mark.parametrize("mut,code", [
+    (lambda s, j: setattr(j, "vocab", s.vocab + 1), L.E_SHAPE),
+    (lambda s, j: setattr(s, "head_dim", 96), L.E_UNSUPPORTED),
+    (lambda s, j: setattr(s, "n_kv_heads", 3), L.E_SHAPE),
+    (lambda s, j: setattr(j, "weight_dtype", 7), L.E_ARG),
+    (lambda s, j: setattr(s, "d_model", 0), L.E_SHAPE),
+])
+def test_workspace_size_rejects_bad_shapes(mut, code):
+    s, j = _cfgs()
+    mut(s, j)
+    kv, sc = C.c_size_t(), C.c_size_t()
+    cap = L.Capacity(8, 64, 64)
+    st = L.lib.tandem_workspace_size(C.byref(s), C.byref(j), C.byref(cap), C.byref(kv), C.byref(sc))
+    assert st == code
+    assert L.lib.tandem_last_error(None)
+
+
+def test_capacity_and_null_checks():
+    s, j = _cfgs()
+    kv, sc = C.c_size_t(), C.c_size_t()
+    cap = L.Capacity(0, 64, 64)
+    assert L.lib.tandem_workspace_size(C.byref(s), C.byref(j), C.byref(cap), C.byref(kv), C.byref(sc)) == L.E_CAPACITY
+    assert L.lib.tandem_workspace_size(None, C.byref(j), C.byref(cap), C.byref(kv), C.byref(sc)) == L.E_ARG
+
+
+def _fake_model(cfg, fill=0x1000):
+    n = cfg.n_layers * 8
+    ptrs = (C.c_void_p * n)(*([fill] * n))
+    m = L.Model(cfg, fill, C.cast(ptrs, C.POINTER(C.c_void_p)), fill, fill)
+    return m, ptrs
+
+
+def _init(sen_cfg, jun_cfg, sw=None, smp=None, cap=None, kv_bytes=None, sc_bytes=None, kv_ptr=0x10000,
+          sc_ptr=0x20000):
+    cap = cap or L.Capacity(8, 64, 64)
+    ms, ps = _fake_model(sen_cfg)
+    mj, pj = _fake_model(jun_cfg)
+    sw = sw or L.SwitchCfg(L.SWITCH, 0.1, -1, None, L.SENIOR)
+    smp = smp or L.SampleCfg(1.0, -1, 0.0, 0.0, 16, 7)
+    out = L.Outputs(0x3000, 0x3000, 0x3000, 0x3000)
+    need_kv, need_sc = C.c_size_t(), C.c_size_t()
+    L.lib.tandem_workspace_size(C.byref(sen_cfg), C.byref(jun_cfg), C.byref(cap), C.byref(need_kv), C.byref(need_sc))
+    h = C.c_void_p()
+    st = L.lib.tandem_init(C.byref(ms), C.byref(mj), C.byref(sw), C.byref(smp), C.byref(cap), kv_ptr,
+                           kv_bytes if kv_bytes is not None else need_kv.value, sc_ptr,
+                           sc_bytes if sc_bytes is not None else need_sc.value, C.byref(out), None, C.byref(h))
+    return st, h
+
+
+def test_init_rejects_bad_arguments_before_hip():
+    s, j = _cfgs()
+    j2 = L.ModelCfg.from_buffer_copy(j)
+    j2.vocab = s.vocab - 1
+    assert _init(s, j2)[0] == L.E_SHAPE
+    assert _init(s, j, sw=L.SwitchCfg(L.SWITCH, 1.5, -1, None, L.SENIOR))[0] == L.E_ARG
+    assert _init(s, j, sw=L.SwitchCfg(5, 0.5, -1, None, L.SENIOR))[0] == L.E_ARG
+    assert _init(s, j, sw=L.SwitchCfg(L.SWITCH, 0.5, -1, None, 9))[0] == L.E_ARG
+    assert _init(s, j, smp=L.SampleCfg(0.0, -1, 0, 0, 16, 1))[0] == L.E_ARG
+    assert _init(s, j, smp=L.SampleCfg(1.0, s.vocab, 0, 0, 16, 1))[0] == L.E_ARG
+    assert _init(s, j, smp=L.SampleCfg(1.0, -1, 0, 0, 100, 1))[0] == L.E_CAPACITY     # max_new > max_ctx
+    assert _init(s, j, kv_bytes=16)[0] == L.E_CAPACITY
+    assert _init(s, j, sc_bytes=16)[0] == L.E_CAPACITY
+    assert _init(s, j, kv_ptr=0x10010)[0] == L.E_ARG                                  # misaligned
+    # (never call init with valid arguments on fake pointers: it would launch kernels on them)
+
+
+def test_null_handle_calls():
+    assert L.lib.tandem_step(None, None) == L.E_ARG
+    assert L.lib.tandem_prefill(None, None, None, 1, 1) == L.E_ARG
+    assert L.lib.tandem_get_state(None, None, None, None, None, None) == L.E_ARG
+    L.lib.tandem_destroy(None)
+    assert L.lib.tandem_status_string(L.E_CAPACITY) == b"TANDEM_E_CAPACITY"

@@ -1,0 +1,124 @@
+"""GPU parity of the tandem step against the CPU oracle, through the C ABI."""
+import numpy as np
+import pytest
+
+import workloads as W
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def _tiny(dtype="f32", **kw):
+    wl = W.workload("tiny").replace(gain_jitter=0.1, **kw)
+    wl.senior.dtype = dtype
+    wl.junior.dtype = dtype
+    return wl
+
+
+def _small_reduced(n_sen=2, n_jun=1, **kw):
+    wl = W.workload("small").replace(gain_jitter=0.05, n_prompts=2, group=4, prompt_len=140,
+                                     prompt_len_min=40, **kw)
+    wl.senior.n_layers, wl.junior.n_layers = n_sen, n_jun
+    wl.sample.max_new = 24
+    return wl
+
+
+def _qwen_reduced():
+    wl = W.workload("qwen").replace(gain_jitter=0.05, n_prompts=1, group=4, prompt_len=64)
+    wl.senior.n_layers, wl.junior.n_layers = 2, 2
+    wl.sample.max_new = 12
+    return wl
+
+
+def test_tiny_fp32_all_valu_paths():
+    P.log("case tiny fp32")
+    p = P.run(_tiny("f32"), logits_at=(1, 16, 32))
+    P.check(p, P.TOL_F32)
+
+
+def test_tiny_bf16_mfma_gemm_valu_attention():
+    P.log("case tiny bf16 (head_dim 32)")
+    p = P.run(_tiny("bf16"), logits_at=(1, 32))
+    P.check(p, P.TOL_BF16)
+
+
+def test_small_shapes_bf16_ragged_prompts():
+    P.log("case small-shaped bf16, ragged prompts, 2+1 layers")
+    wl = _small_reduced()
+    p = P.run(wl, logits_at=(1, 24), max_prefill_tokens=256)
+    P.check(p, P.TOL_BF16)
+
+
+def test_qwen_shapes_bf16_qk_norm():
+    P.log("case qwen-shaped bf16, qk-norm, head_dim 128, 2+2 layers")
+    p = P.run(_qwen_reduced(), logits_at=(1, 12))
+    P.check(p, P.TOL_BF16)
+
+
+def test_paper_schedule_redraw_word_boundaries_and_cap():
+    P.log("case paper schedule: REDRAW p=0.5, K=3, drawn first owner, 35% boundary bitmap, T=0.6")
+    wl = _tiny("bf16")
+    wl.switch = W.SwitchSettings(W.REDRAW, 0.5, 3, "random:0.351", W.DRAW)
+    wl.sample.temperature = 0.6
+    p = P.run(wl, logits_at=(5,))
+    P.check(p, P.TOL_BF16)
+    assert p.ref.decided.sum() > 0 and 0 < p.ref.owner.mean() < 1
+
+
+def test_eos_stops_sequences():
+    P.log("case EOS with logit bias")
+    wl = _tiny("f32")
+    wl.sample.eos_id, wl.sample.eos_bias_senior, wl.sample.eos_bias_junior = 5, 4.0, 3.0
+    p = P.run(wl, logits_at=(2,))
+    assert (p.ref.length < wl.sample.max_new).any()
+    P.check(p, P.TOL_F32)
+
+
+def test_free_running_is_deterministic_and_matches_oracle_fp32():
+    from paper_2606_28166_amd.engine import TandemEngine
+    from oracle.rollout import rollout, build_models
+    P.log("case free-running determinism")
+    wl = _tiny("f32")
+    ws, wj, prompts, bnd = W.make_all(wl)
+    outs = []
+    for _ in range(2):
+        eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed,
+                           max_seqs=wl.n_seqs, max_ctx=wl.prompt_len - 1 + wl.sample.max_new)
+        eng.prefill(prompts, wl.group)
+        n_active = None
+        for _ in range(wl.sample.max_new):
+            n_active = eng.step(want_active=True)
+        assert n_active == 0
+        outs.append(eng.outputs())
+        eng.close()
+    for k in outs[0]:
+        np.testing.assert_array_equal(outs[0][k], outs[1][k])
+    sen, jun = build_models(wl, ws, wj)
+    ref = rollout(sen, jun, prompts, wl.group, wl.switch, wl.sample, wl.philox_seed, bnd)
+    np.testing.assert_array_equal(outs[0]["tokens"], ref.tokens)
+    np.testing.assert_array_equal(outs[0]["owner"], ref.owner)
+
+
+def test_error_paths_on_device():
+    from paper_2606_28166_amd import _lib as L
+    from paper_2606_28166_amd.engine import TandemEngine
+    P.log("case error paths")
+    wl = _tiny("f32")
+    ws, wj, prompts, _ = W.make_all(wl)
+    eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed,
+                       max_seqs=wl.n_seqs, max_ctx=wl.prompt_len - 1 + wl.sample.max_new)
+    with pytest.raises(L.TandemError) as e:
+        eng.step()
+    assert e.value.status == L.E_STATE
+    with pytest.raises(L.TandemError) as e:
+        eng.prefill([np.arange(40, dtype=np.int32)], 1)          # prompt longer than max_ctx allows
+    assert e.value.status == L.E_CAPACITY
+    with pytest.raises(L.TandemError) as e:
+        eng.prefill([np.array([1, 2, 9999], dtype=np.int32)], 1)  # token id outside the vocabulary
+    assert e.value.status == L.E_ARG
+    with pytest.raises(L.TandemError) as e:
+        eng.prefill(prompts, wl.group + 1)                         # more sequences than max_seqs
+    assert e.value.status == L.E_CAPACITY
+    eng.prefill(prompts, wl.group)
+    eng.step()
+    eng.close()

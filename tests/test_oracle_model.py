@@ -12,7 +12,7 @@ import torch.nn.functional as F
 from scipy.special import expit
 
 import workloads as W
-from oracle.model import OracleModel, rmsnorm, rope, silu, KVCache
+from oracle.model import OracleModel, rmsnorm, rope, silu, KVCache, round_bf16
 from oracle.rollout import build_models
 
 
@@ -197,3 +197,44 @@ def test_bf16_weights_are_exact_in_float64():
     back = W.round_to_bf16_bits(f["layers.0.w_qkv"].astype(np.float32))
     np.testing.assert_array_equal(back, bits)
     assert abs(f["layers.0.w_qkv"].std() - 0.02) < 0.002
+
+
+def _bf16_exact(x: float) -> float:
+    """Nearest bf16 by exhaustive search over the two neighbours, with exact Fractions."""
+    from fractions import Fraction
+    import struct
+    f = Fraction(x)
+    b = struct.unpack("<I", struct.pack("<f", np.float32(x)))[0] & 0xFFFF0000
+    cands = set()
+    for d in (-0x20000, -0x10000, 0, 0x10000, 0x20000):
+        u = (b + d) & 0xFFFFFFFF
+        v = struct.unpack("<f", struct.pack("<I", u))[0]
+        if np.isfinite(v):
+            cands.add((v, u))
+    best = min(cands, key=lambda c: (abs(Fraction(c[0]) - f), (c[1] >> 16) & 1))
+    return best[0]
+
+
+def test_round_bf16_is_correctly_rounded():
+    rng = np.random.default_rng(5)
+    xs = list(rng.standard_normal(400) * 10.0 ** rng.integers(-6, 6, 400))
+    # exact ties and near-ties between bf16 neighbours, which double rounding gets wrong
+    base = np.float32(1.0 + 2 ** -7)
+    xs += [1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8), 1.0 + 2 ** -8 + 2 ** -40,
+           1.0 + 2 ** -8 - 2 ** -40, float(base) + 2 ** -9 + 2 ** -30, 1.0 + 2 ** -8 + 2 ** -24 + 2 ** -40]
+    got = round_bf16(np.array(xs))
+    for x, g in zip(xs, got):
+        assert g == _bf16_exact(x), x
+    np.testing.assert_array_equal(round_bf16(np.array([0.0, -0.0, 1.0, -2.5])), [0.0, -0.0, 1.0, -2.5])
+
+
+def test_bf16_model_stores_its_cache_in_bf16():
+    wl = W.workload("small")
+    shape = W.scaled(wl.senior, n_layers=1, vocab=64, d_model=128, ffn_dim=128, n_q_heads=2, n_kv_heads=1)
+    f = W.weights_as_float(shape, W.make_weights(shape, 3))
+    m = OracleModel(shape, f)
+    c = m.new_cache(8)
+    m.prefill(c, [1, 2, 3])
+    np.testing.assert_array_equal(round_bf16(c.k[:, :, :3]), c.k[:, :, :3])
+    np.testing.assert_array_equal(round_bf16(c.v[:, :, :3]), c.v[:, :, :3])
+    assert np.any(c.k[:, :, :3] != 0)
