@@ -84,7 +84,9 @@ typedef struct {
  *              w_gate_up [2 ffn][d] (gate rows, then up rows), w_down [d][ffn]
  *   final_norm [d_model]
  *   lm_head    [vocab][d_model]
- * The layers array is copied at tandem_init; the weights are borrowed. */
+ * Every weight pointer must be 16-byte aligned; d_model and ffn_dim must be
+ * multiples of 8.  The layers array is copied at tandem_init; the weights are
+ * borrowed. */
 typedef struct {
   tandem_model_cfg cfg;
   const void* embed;

@@ -9,6 +9,7 @@ namespace tandem {
 typedef uint16_t bf16_t;   // bf16 bit pattern
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
@@ -34,6 +35,63 @@ template <> struct Elem<bf16_t> {
 
 template <typename T> __device__ __forceinline__ float ld(const T* p) { return Elem<T>::load(p); }
 template <typename T> __device__ __forceinline__ void st(T* p, float v) { Elem<T>::store(p, v); }
+
+// ------------------------------------------------------------ split format
+// Activations of bf16 models are stored "split": each group of 8 values is
+// 16 bf16 words, the 8 high parts hi = bf16(x) followed by the 8 low parts
+// lo = bf16(x - hi).  hi + lo carries x to about 2^-16 relative, in the
+// 4 bytes per value of fp32, and both halves are ready-made MFMA operands.
+__device__ __forceinline__ void split_store(bf16_t* row, int k, float x) {
+  const bf16_t h = f2bf(x);
+  bf16_t* p = row + (k >> 3) * 16 + (k & 7);
+  p[0] = h;
+  p[8] = f2bf(x - bf2f(h));
+}
+__device__ __forceinline__ float split_load(const bf16_t* row, int k) {
+  const bf16_t* p = row + (k >> 3) * 16 + (k & 7);
+  return bf2f(p[0]) + bf2f(p[8]);
+}
+
+// Activation row store in either format (split for bf16 models, plain fp32 otherwise).
+template <bool SPLIT>
+__device__ __forceinline__ void act_store(void* base, size_t row, int K, int k, float x) {
+  if (SPLIT) split_store(reinterpret_cast<bf16_t*>(base) + row * 2 * (size_t)K, k, x);
+  else reinterpret_cast<float*>(base)[row * (size_t)K + k] = x;
+}
+
+// s_waitcnt that waits only for vector memory operations: vmcnt <= n.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+__device__ __forceinline__ void wait_lgkm0() {
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+// 16 bytes per lane from global memory straight into LDS at lds_base + 16 * lane.
+__device__ __forceinline__ void load_lds16(const void* gsrc, void* lds_base) {
+  __builtin_amdgcn_global_load_lds((glb_void_t*)gsrc, (lds_void_t*)lds_base, 16, 0, 0);
+}
+
+// LDS read the compiler does not see as a memory access: it then cannot
+// conflate it with pending LDS-DMA writes (which would make it drain every
+// outstanding load).  The caller must wait with lds_wait() before using the
+// result and must order ring reuse with its own barriers.
+__device__ __forceinline__ u32x4_t lds_read16(uint32_t lds_addr) {
+  u32x4_t r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(lds_addr));
+  return r;
+}
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Ties a value to the preceding lds_wait() so no use is scheduled before it.
+__device__ __forceinline__ void lds_fence_value(u32x4_t& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ uint32_t lds_addr_of(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -87,6 +145,19 @@ __device__ __forceinline__ float uniform_open(uint32_t x) {
 // Standard Gumbel noise -log(-log u).
 __device__ __forceinline__ float gumbel(uint32_t x) {
   return -logf(-logf(uniform_open(x)));
+}
+
+// The same through the hardware log2 (v_log_f32, about 1 ulp): -ln(-ln u)
+// with ln y = log2(y) * ln 2.  u >= 2^-24 keeps both arguments normal.
+__device__ __forceinline__ float gumbel_fast(uint32_t x) {
+  const float ln2 = 0.6931471805599453f;
+  const float a = -__builtin_amdgcn_logf(uniform_open(x)) * ln2;    // -ln u > 0
+  return -__builtin_amdgcn_logf(a) * ln2;
+}
+
+// e^x through the hardware exp2 (v_exp_f32); x <= 0 here.
+__device__ __forceinline__ float fast_exp(float x) {
+  return __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
 }
 
 }  // namespace tandem

@@ -1,28 +1,32 @@
-// Projection GEMMs of the decoder: C = A . W^T with W row-major [out][in],
-// A the fp32 activations (normed hidden states, attention output, SwiGLU
-// output).
+// Projection GEMMs of the decoder: C = A . W^T with W row-major [out][in].
 //
-// bf16 path (gfx950 MFMA, v_mfma_f32_16x16x32_bf16): a weight-streaming
-// kernel.  Each wave owns NB blocks of 16 weight rows and streams them from
-// HBM straight into registers, D chunks of 64 k-values ahead.  The activation
-// tile (BM rows x 64 k) is staged once per workgroup through LDS, split into
-// a bf16 high part and a bf16 low part (x = hi + lo to about 2^-16), and
-// every weight fragment meets both: two MFMAs, fp32 accumulation.  The
-// activations therefore keep fp32-level precision while the weights stream
-// at bf16 width; decode projections are bound by the weight stream, so the
-// second MFMA is nearly free.  LDS rows are padded by 16 bytes so the
-// MFMA-layout reads are free of bank conflicts.  K may be split over grid.z;
-// the partial tiles are summed by the consuming kernel in a fixed order,
-// which keeps results bitwise reproducible.
+// bf16 path (gfx950 MFMA v_mfma_f32_32x32x16_bf16), a streaming kernel for
+// skinny (decode) and tall (prefill) A alike:
+//   * A holds the activations in split format (per 8 values: 8 bf16 high
+//     parts, then 8 bf16 low parts), so every weight fragment meets hi and lo
+//     in two MFMAs: fp32-level activations, bf16 weights, fp32 accumulation.
+//   * One workgroup computes a BM x 128 output tile (BM in {32, 64, 128})
+//     over its slice of K, 64 k-values per chunk; its 4 waves tile the 32 x 32
+//     MFMA blocks 2 x 2 (1 x 4 when BM = 32).  The 32 x 32 x 16 shape keeps
+//     the matrix cores near their peak with only a few accumulators per wave.
+//   * Weight rows and activation rows of each chunk stream into an NS-stage
+//     LDS ring with global_load_lds_dwordx4 (no register staging); 16-byte
+//     pieces are XOR-swizzled by row so the MFMA-layout reads spread over all
+//     banks.  All loads are issued unconditionally (clamped to the last
+//     chunk), the reads are explicit ds_read_b128, and the only waits are
+//     compile-time vmcnt/lgkmcnt values plus a raw s_barrier: the compiler
+//     never sees a memory result it could over-wait for, so NS - 1 chunks
+//     stay in flight the whole time.
+//   * K may be split over grid.z; the consuming kernel sums the partial
+//     tiles in a fixed order, keeping results bitwise reproducible.
 //
-// MFMA operand layout used (16x16x32): lane l supplies row/column l % 16 and
-// eight k-values of group l / 16; the result lane l holds column l % 16 of
-// rows 4 * (l / 16) .. + 3.  Any permutation of k that is the same for both
-// operands gives the same dot product, so lane group g takes the contiguous
-// k range [16 g, 16 g + 16) of each 64-wide chunk: one 32-byte run per lane.
+// MFMA operand layout (32x32x16): lane l supplies row/column l % 32 and eight
+// k-values of group l / 32; result element i of lane l is column l % 32 of
+// row 8 (i / 4) + 4 (l / 32) + i % 4.  Any permutation of k that is the same
+// for both operands gives the same dot product, so lane group g takes the
+// k range [32 g, 32 g + 32) of each chunk, 8 values per k-step.
 //
-// fp32 path: a plain LDS-tiled VALU kernel (fp32 models and K that is not a
-// multiple of 64).
+// fp32 path: a plain LDS-tiled VALU kernel (fp32 models, K not a multiple of 64).
 #include "common.h"
 #include "kernels.h"
 
@@ -31,145 +35,182 @@ namespace tandem {
 namespace {
 
 constexpr int BK = kGemmBK;        // k-values per chunk
-constexpr int LDA = BK + 8;        // padded LDS row (elements)
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
 
-template <int MT, int NB, int EPI, int D>
+template <int BMT, int BNT, int NST> struct GemmShape {
+  static constexpr int BM = BMT;
+  static constexpr int BN = BNT;                      // weight rows per tile (128 or 256)
+  static constexpr int MB = BM / 32;                  // 32-row blocks
+  static constexpr int WM = MB >= 2 ? 2 : 1;          // waves along M
+  static constexpr int WN = 4 / WM;                   // waves along N
+  static constexpr int MBW = MB / WM;                 // 32-row blocks per wave
+  static constexpr int NBW = BN / 32 / WN;            // 32-column blocks per wave
+  static constexpr int NS = NST;                      // ring stages
+  static constexpr int ASTAGE = BM * BK * 4;          // bytes of one activation stage (hi + lo)
+  static constexpr int WSTAGE = BN * BK * 2;          // bytes of one weight stage
+  static constexpr int STAGE = ASTAGE + WSTAGE;
+  static constexpr int NA = BM / 16;                  // activation DMA instructions per wave per chunk
+  static constexpr int NWD = BN / 32;                 // weight DMA instructions per wave per chunk
+  static constexpr int WAIT = (NS - 2) * (NA + NWD);  // vmcnt that leaves NS - 2 chunks in flight
+  static constexpr int OUT_COLS = BN / 2;             // SwiGLU output columns per tile
+  static_assert(NS * STAGE <= 160 * 1024, "LDS ring exceeds 160 KB");
+};
+
+template <int BMT, int BNT, int NST, int EPI>
 __global__ __launch_bounds__(256) void gemm_mfma_kernel(
-    const float* __restrict__ A, const bf16_t* __restrict__ W, int M, int N, int K, int cps,
+    const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, int M, int N, int K, int cps,
     float* __restrict__ out, int ldo, long split_stride) {
-  constexpr int BM = 16 * MT;
-  constexpr int PIECES = BM * (BK / 4);               // float4 pieces of one A chunk
-  constexpr int AITER = (PIECES + 255) / 256;
-  __shared__ __attribute__((aligned(16))) bf16_t Ah[BM][LDA];
-  __shared__ __attribute__((aligned(16))) bf16_t Al[BM][LDA];
+  using G = GemmShape<BMT, BNT, NST>;
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[G::NS * G::STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int g = lane >> 4, c16 = lane & 15;
-  const int m0 = blockIdx.y * BM;
+  const int g = lane >> 5, c32 = lane & 31;
+  const int wm = wave / G::WN, wn = wave % G::WN;
+  const int m0 = blockIdx.y * G::BM;
   const int nch = K / BK;
   const int kc0 = blockIdx.z * cps;
   const int nloc = min(cps, nch - kc0);
   if (nloc <= 0) return;
 
-  // weight rows streamed by this lane
-  const bf16_t* wrow[NB];
-  int ncol[NB];
-  if (EPI == EPI_SWIGLU) {
-    const int j = blockIdx.x * 64 + wave * 16 + c16;
-    ncol[0] = j;
-    ncol[1] = j;
-    const int jc = min(j, N - 1);
-    wrow[0] = W + (size_t)jc * K;
-    wrow[1] = W + (size_t)(N + jc) * K;
-  } else {
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int n = blockIdx.x * (64 * NB) + (wave * NB + nb) * 16 + c16;
-      ncol[nb] = n;
-      wrow[nb] = W + (size_t)min(n, N - 1) * K;
+  // Global weight row of tile row t (0..BN-1).  SwiGLU tiles pair gate and up
+  // rows inside every 32-row block: rows 32p .. 32p+15 are gate rows
+  // j0 + 16p + c, rows 32p+16 .. 32p+31 the matching up rows; other tiles
+  // hold BN consecutive rows.
+  auto wrow_of = [&](int t) -> int {
+    if (EPI == EPI_SWIGLU) {
+      const int j = min(blockIdx.x * G::OUT_COLS + 16 * (t >> 5) + (t & 15), N - 1);
+      return ((t >> 4) & 1) ? N + j : j;
     }
+    return min(blockIdx.x * G::BN + t, N - 1);
+  };
+
+  // DMA sources.  Weight stage: instruction i of wave w covers tile rows
+  // (BN/4) w + 8i .. +8 (128 B each); lane -> row (lane >> 3), physical piece
+  // lane & 7 holding logical piece (lane & 7) ^ ((row >> 1) & 7).
+  const bf16_t* wsrc[G::NWD];
+#pragma unroll
+  for (int i = 0; i < G::NWD; ++i) {
+    const int t = (G::BN / 4) * wave + 8 * i + (lane >> 3);
+    const int lp = (lane & 7) ^ ((t >> 1) & 7);
+    wsrc[i] = W + (size_t)wrow_of(t) * K + lp * 8;
+  }
+  // Activation stage: instruction i of wave w covers tile rows 16i + 4w .. +4
+  // (256 B each: 8 hi pieces and 8 lo pieces); physical piece lane & 15 holds
+  // logical piece (lane & 15) ^ (row & 15).
+  const bf16_t* asrc[G::NA];
+#pragma unroll
+  for (int i = 0; i < G::NA; ++i) {
+    const int r = 16 * i + 4 * wave + (lane >> 4);
+    const int lc = (lane & 15) ^ (r & 15);
+    asrc[i] = A + (size_t)min(m0 + r, M - 1) * 2 * (size_t)K + lc * 8;
+  }
+  unsigned char* const ring0 = ring;
+  auto issue = [&](int it) {
+    const int c = kc0 + min(it, nloc - 1);
+    unsigned char* st = ring0 + (it % G::NS) * G::STAGE;
+#pragma unroll
+    for (int i = 0; i < G::NA; ++i) load_lds16(asrc[i] + (size_t)c * 2 * BK, st + (16 * i + 4 * wave) * 256);
+#pragma unroll
+    for (int i = 0; i < G::NWD; ++i)
+      load_lds16(wsrc[i] + (size_t)c * BK, st + G::ASTAGE + ((G::BN / 4) * wave + 8 * i) * 128);
+  };
+
+  f32x16_t acc[G::MBW][G::NBW];
+#pragma unroll
+  for (int mb = 0; mb < G::MBW; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < G::NBW; ++nb) acc[mb][nb] = f32x16_t{};
+
+  const uint32_t ring_addr = lds_addr_of(ring);
+  struct Frags {
+    u32x4_t a[G::MBW][2];
+    u32x4_t w[G::NBW];
+  };
+  // fragments of k-step j: k-group q = 4g + j of rows / columns c32 of each block
+  auto read_frags = [&](uint32_t st, int j, Frags& f) {
+    const int q = 4 * g + j;
+#pragma unroll
+    for (int mb = 0; mb < G::MBW; ++mb) {
+      const int r = (wm * G::MBW + mb) * 32 + c32;
+      const uint32_t rowa = st + (uint32_t)(r * 256);
+      f.a[mb][0] = lds_read16(rowa + (uint32_t)(((2 * q) ^ (r & 15)) * 16));
+      f.a[mb][1] = lds_read16(rowa + (uint32_t)(((2 * q + 1) ^ (r & 15)) * 16));
+    }
+#pragma unroll
+    for (int nb = 0; nb < G::NBW; ++nb) {
+      const int t = (wn * G::NBW + nb) * 32 + c32;
+      f.w[nb] = lds_read16(st + G::ASTAGE + (uint32_t)(t * 128 + ((q ^ ((t >> 1) & 7)) * 16)));
+    }
+  };
+  auto fence = [&](Frags& f) {
+#pragma unroll
+    for (int mb = 0; mb < G::MBW; ++mb) {
+      lds_fence_value(f.a[mb][0]);
+      lds_fence_value(f.a[mb][1]);
+    }
+#pragma unroll
+    for (int nb = 0; nb < G::NBW; ++nb) lds_fence_value(f.w[nb]);
+  };
+  // hi parts for every accumulator, then lo parts
+  auto mfma_step = [&](const Frags& f) {
+#pragma unroll
+    for (int part = 0; part < 2; ++part)
+#pragma unroll
+      for (int mb = 0; mb < G::MBW; ++mb) {
+        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, f.a[mb][part]);
+#pragma unroll
+        for (int nb = 0; nb < G::NBW; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, f.w[nb]),
+                                                                acc[mb][nb], 0, 0, 0);
+      }
+  };
+
+#pragma unroll
+  for (int s = 0; s < G::NS - 1; ++s) issue(s);
+  for (int it = 0; it < nloc; ++it) {
+    wait_vmcnt<G::WAIT>();          // this wave's loads of chunk it have landed
+    lds_wait();                     // and its reads of chunk it - 1 are done
+    __builtin_amdgcn_s_barrier();   // ... in every wave: chunk it is complete, stage it - 1 is free
+    issue(it + G::NS - 1);
+    const uint32_t st = ring_addr + (uint32_t)((it % G::NS) * G::STAGE);
+    Frags f0, f1;
+    read_frags(st, 0, f0);
+    lds_wait();
+    fence(f0);
+    read_frags(st, 1, f1);          // next k-step in flight during this one
+    mfma_step(f0);
+    lds_wait();
+    fence(f1);
+    read_frags(st, 2, f0);
+    mfma_step(f1);
+    lds_wait();
+    fence(f0);
+    read_frags(st, 3, f1);
+    mfma_step(f0);
+    lds_wait();
+    fence(f1);
+    mfma_step(f1);
   }
 
-  u32x4_t wbuf[D][NB][2];
-  float4 areg[AITER];
-
-  auto load_w = [&](int it, u32x4_t (&dst)[NB][2]) {
-    const size_t off = (size_t)(kc0 + it) * BK + 16 * g;
+  // epilogue: element i of lane l is row 8 (i / 4) + 4 g + i % 4, column c32
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const u32x4_t* p = reinterpret_cast<const u32x4_t*>(wrow[nb] + off);
-      dst[nb][0] = __builtin_nontemporal_load(p);
-      dst[nb][1] = __builtin_nontemporal_load(p + 1);
-    }
-  };
-  auto load_a = [&](int it) {
+  for (int mb = 0; mb < G::MBW; ++mb) {
 #pragma unroll
-    for (int i = 0; i < AITER; ++i) {
-      const int piece = tid + 256 * i;
-      const int r = piece >> 4, cc = (piece & 15) * 4;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (piece < PIECES && m0 + r < M)
-        v = *reinterpret_cast<const float4*>(A + (size_t)(m0 + r) * K + (size_t)(kc0 + it) * BK + cc);
-      areg[i] = v;
-    }
-  };
-  auto store_a = [&]() {
+    for (int nb = 0; nb < G::NBW; ++nb) {
 #pragma unroll
-    for (int i = 0; i < AITER; ++i) {
-      const int piece = tid + 256 * i;
-      if (piece < PIECES) {
-        const int r = piece >> 4, cc = (piece & 15) * 4;
-        const float x[4] = {areg[i].x, areg[i].y, areg[i].z, areg[i].w};
-        bf16_t hi[4], lo[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          hi[e] = f2bf(x[e]);
-          lo[e] = f2bf(x[e] - bf2f(hi[e]));
-        }
-        *reinterpret_cast<uint2*>(&Ah[r][cc]) =
-            make_uint2((uint32_t)hi[0] | ((uint32_t)hi[1] << 16), (uint32_t)hi[2] | ((uint32_t)hi[3] << 16));
-        *reinterpret_cast<uint2*>(&Al[r][cc]) =
-            make_uint2((uint32_t)lo[0] | ((uint32_t)lo[1] << 16), (uint32_t)lo[2] | ((uint32_t)lo[3] << 16));
-      }
-    }
-  };
-
-  f32x4_t acc[MT][NB];
-#pragma unroll
-  for (int mb = 0; mb < MT; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  load_a(0);
-#pragma unroll
-  for (int d = 0; d < D - 1; ++d)
-    if (d < nloc) load_w(d, wbuf[d]);
-
-  for (int kk = 0; kk < nloc; kk += D) {
-#pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const int it = kk + d;
-      if (it < nloc) {
-        if (it + D - 1 < nloc) load_w(it + D - 1, wbuf[(d + D - 1) % D]);
-        __syncthreads();              // every wave is done reading the previous chunk
-        store_a();
-        __syncthreads();
-        if (it + 1 < nloc) load_a(it + 1);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-#pragma unroll
-          for (int mb = 0; mb < MT; ++mb) {
-            const bf16x8_t ah = *reinterpret_cast<const bf16x8_t*>(&Ah[mb * 16 + c16][16 * g + 8 * j]);
-            const bf16x8_t al = *reinterpret_cast<const bf16x8_t*>(&Al[mb * 16 + c16][16 * g + 8 * j]);
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-              const bf16x8_t b = __builtin_bit_cast(bf16x8_t, wbuf[d][nb][j]);
-              acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b, acc[mb][nb], 0, 0, 0);
-              acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b, acc[mb][nb], 0, 0, 0);
-            }
-          }
-        }
-      }
-    }
-  }
-
-  // epilogue
-#pragma unroll
-  for (int mb = 0; mb < MT; ++mb) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + mb * 16 + 4 * g + i;
-      if (m >= M) continue;
-      if (EPI == EPI_SWIGLU) {
-        const int j = ncol[0];
-        if (j < N) out[(size_t)m * ldo + j] = silu(acc[mb][0][i]) * acc[mb][1][i];
-      } else {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const int n = ncol[nb];
-          if (n < N) out[blockIdx.z * split_stride + (size_t)m * ldo + n] = acc[mb][nb][i];
+      for (int i = 0; i < 16; ++i) {
+        const int m = m0 + (wm * G::MBW + mb) * 32 + 8 * (i >> 2) + 4 * g + (i & 3);
+        const float v = acc[mb][nb][i];
+        if (EPI == EPI_SWIGLU) {
+          // columns 0..15 of the block are gate values, 16..31 the matching up values
+          const float up = __shfl_xor(v, 16, 64);
+          const int j = blockIdx.x * G::OUT_COLS + 16 * (wn * G::NBW + nb) + (c32 & 15);
+          if (m < M && c32 < 16 && j < N)
+            split_store(reinterpret_cast<bf16_t*>(out) + (size_t)m * 2 * ldo, j, silu(v) * up);
+        } else {
+          const int n = blockIdx.x * G::BN + (wn * G::NBW + nb) * 32 + c32;
+          if (m < M && n < N) out[blockIdx.z * split_stride + (size_t)m * ldo + n] = v;
         }
       }
     }
@@ -177,9 +218,9 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(
 }
 
 // ---------------------------------------------------------------- VALU path
-template <typename WT, int EPI>
+template <typename WT, bool SPLIT, int EPI>
 __global__ __launch_bounds__(256) void gemm_valu_kernel(
-    const float* __restrict__ A, const WT* __restrict__ W, int M, int N, int K, int kper,
+    const void* __restrict__ Av, const WT* __restrict__ W, int M, int N, int K, int kper,
     float* __restrict__ out, int ldo, long split_stride) {
   // 32 x 32 output tile, 16 x 16 threads with 2 x 2 outputs each
   constexpr int T = 32;
@@ -194,7 +235,12 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(
     for (int e = threadIdx.x; e < T * T; e += 256) {
       const int r = e / T, c = e % T;
       const int m = m0 + r, k = k0 + c;
-      As[r][c] = (m < M && k < ke) ? A[(size_t)m * K + k] : 0.f;
+      float a = 0.f;
+      if (m < M && k < ke) {
+        if (SPLIT) a = split_load(reinterpret_cast<const bf16_t*>(Av) + (size_t)m * 2 * K, k);
+        else a = reinterpret_cast<const float*>(Av)[(size_t)m * K + k];
+      }
+      As[r][c] = a;
 #pragma unroll
       for (int w = 0; w < NW; ++w) {
         const int n = n0 + r;
@@ -222,41 +268,45 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(
       const int m = m0 + ty * 2 + i, n = n0 + tx * 2 + jj;
       if (m >= M || n >= N) continue;
       if (EPI == EPI_SWIGLU)
-        out[(size_t)m * ldo + n] = silu(acc[0][i][jj]) * acc[NW - 1][i][jj];
+        act_store<SPLIT>(out, m, ldo, n, silu(acc[0][i][jj]) * acc[NW - 1][i][jj]);
       else
         out[blockIdx.z * split_stride + (size_t)m * ldo + n] = acc[0][i][jj];
     }
 }
 
-template <int MT, int NB, int EPI>
+template <int BMT, int BNT, int NST, int EPI>
 hipError_t run_mfma(const GemmArgs& a, int S, int cps, hipStream_t st) {
-  constexpr int D = 4;
-  const int cols = (EPI == EPI_SWIGLU) ? 64 : 64 * NB;
-  dim3 grid((a.N + cols - 1) / cols, (a.M + 16 * MT - 1) / (16 * MT), S);
-  hipLaunchKernelGGL((gemm_mfma_kernel<MT, NB, EPI, D>), grid, dim3(256), 0, st, a.A, (const bf16_t*)a.W,
-                     a.M, a.N, a.K, cps, a.out, a.ldo, a.split_stride);
+  using G = GemmShape<BMT, BNT, NST>;
+  const int cols = (EPI == EPI_SWIGLU) ? G::OUT_COLS : G::BN;
+  dim3 grid((a.N + cols - 1) / cols, (a.M + BMT - 1) / BMT, S);
+  hipLaunchKernelGGL((gemm_mfma_kernel<BMT, BNT, NST, EPI>), grid, dim3(256), 0, st, (const bf16_t*)a.A,
+                     (const bf16_t*)a.W, a.M, a.N, a.K, cps, a.out, a.ldo, a.split_stride);
   return hipGetLastError();
 }
 
+#ifndef TANDEM_GEMM_BN
+#define TANDEM_GEMM_BN 128
+#endif
+#ifndef TANDEM_GEMM_NS128
+#define TANDEM_GEMM_NS128 3
+#endif
 template <int EPI>
 hipError_t dispatch_mfma(const GemmArgs& a, int S, int cps, hipStream_t st) {
-  const int mt_need = (min(a.M, 128) + 15) / 16;
-  constexpr int NB = 2;
-  if (mt_need <= 1) return run_mfma<1, NB, EPI>(a, S, cps, st);
-  if (mt_need <= 2) return run_mfma<2, NB, EPI>(a, S, cps, st);
-  if (mt_need <= 4) return run_mfma<4, NB, EPI>(a, S, cps, st);
-  return run_mfma<8, NB, EPI>(a, S, cps, st);
+  constexpr int BNT = TANDEM_GEMM_BN;
+  if (a.M <= 32) return run_mfma<32, BNT, (BNT == 128 ? 4 : 3), EPI>(a, S, cps, st);
+  if (a.M <= 64) return run_mfma<64, BNT, (BNT == 128 ? 4 : 2), EPI>(a, S, cps, st);
+  return run_mfma<128, BNT, (BNT == 128 ? TANDEM_GEMM_NS128 : 2), EPI>(a, S, cps, st);
 }
 
-template <typename WT>
+template <typename WT, bool SPLIT>
 hipError_t run_valu(const GemmArgs& a, int S, int kper, hipStream_t st) {
   dim3 grid((a.N + 31) / 32, (a.M + 31) / 32, S);
   if (a.epi == EPI_SWIGLU)
-    hipLaunchKernelGGL((gemm_valu_kernel<WT, EPI_SWIGLU>), grid, dim3(256), 0, st, a.A, (const WT*)a.W,
-                       a.M, a.N, a.K, kper, a.out, a.ldo, a.split_stride);
+    hipLaunchKernelGGL((gemm_valu_kernel<WT, SPLIT, EPI_SWIGLU>), grid, dim3(256), 0, st, a.A,
+                       (const WT*)a.W, a.M, a.N, a.K, kper, a.out, a.ldo, a.split_stride);
   else
-    hipLaunchKernelGGL((gemm_valu_kernel<WT, EPI_PARTIAL>), grid, dim3(256), 0, st, a.A, (const WT*)a.W,
-                       a.M, a.N, a.K, kper, a.out, a.ldo, a.split_stride);
+    hipLaunchKernelGGL((gemm_valu_kernel<WT, SPLIT, EPI_PARTIAL>), grid, dim3(256), 0, st, a.A,
+                       (const WT*)a.W, a.M, a.N, a.K, kper, a.out, a.ldo, a.split_stride);
   return hipGetLastError();
 }
 
@@ -286,8 +336,8 @@ hipError_t launch_gemm(const GemmArgs& a, int* splits_used, hipStream_t st) {
   const int kper = ((nk + S - 1) / S) * 32;
   S = (a.K + kper - 1) / kper;
   if (splits_used) *splits_used = S;
-  if (a.dt == DT_BF16) return run_valu<bf16_t>(a, S, kper, st);
-  return run_valu<float>(a, S, kper, st);
+  if (a.dt == DT_BF16) return run_valu<bf16_t, true>(a, S, kper, st);
+  return run_valu<float, false>(a, S, kper, st);
 }
 
 }  // namespace tandem

@@ -9,65 +9,90 @@ namespace tandem {
 namespace {
 
 constexpr int kNT = 256;
-constexpr int kMaxPer = 32;        // d_model <= 8192
+constexpr int kSplitMaxDev = 8;    // split-K slices a consumer sums (>= the host's cap)
 
 // ------------------------------------------------------------------ norms
-template <typename WT>
+// One workgroup per row; each thread owns float4 groups of the row.  All
+// split-K partial loads of a group are issued before any is summed (fixed
+// order s = 0..S-1), so a row costs one memory round trip, not S.
+constexpr int kMaxV4 = 8;          // d_model <= 8192
+
+template <bool SPLIT>
+__device__ __forceinline__ void norm_store(void* x, int r, int d, int i4, float4 v, float rs, const float* gain) {
+  const float4 gg = *reinterpret_cast<const float4*>(gain + 4 * i4);
+  const float y[4] = {v.x * rs * gg.x, v.y * rs * gg.y, v.z * rs * gg.z, v.w * rs * gg.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) act_store<SPLIT>(x, r, d, 4 * i4 + e, y[e]);
+}
+
+template <typename WT, bool SPLIT>
 __global__ __launch_bounds__(kNT) void embed_norm_kernel(const int32_t* __restrict__ tok,
                                                          const WT* __restrict__ E, int d,
                                                          const float* __restrict__ gain, float eps,
-                                                         float* __restrict__ h, float* __restrict__ x) {
+                                                         float* __restrict__ h, void* __restrict__ x) {
   __shared__ float red[kNT / 64];
   const int r = blockIdx.x, tid = threadIdx.x;
   const WT* e = E + (size_t)tok[r] * d;
-  float v[kMaxPer];
+  const int n4 = d / 4;
+  float4 v[kMaxV4];
   float ss = 0.f;
 #pragma unroll
-  for (int k = 0; k < kMaxPer; ++k) {
-    const int i = tid + k * kNT;
-    v[k] = i < d ? ld(e + i) : 0.f;
-    ss += v[k] * v[k];
+  for (int k = 0; k < kMaxV4; ++k) {
+    const int i4 = tid + k * kNT;
+    v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i4 < n4) {
+      v[k] = make_float4(ld(e + 4 * i4), ld(e + 4 * i4 + 1), ld(e + 4 * i4 + 2), ld(e + 4 * i4 + 3));
+      ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
+    }
   }
   const float tot = block_sum<kNT>(ss, red);
   const float rs = 1.f / sqrtf(tot / (float)d + eps);
 #pragma unroll
-  for (int k = 0; k < kMaxPer; ++k) {
-    const int i = tid + k * kNT;
-    if (i < d) {
-      h[(size_t)r * d + i] = v[k];
-      x[(size_t)r * d + i] = v[k] * rs * gain[i];
+  for (int k = 0; k < kMaxV4; ++k) {
+    const int i4 = tid + k * kNT;
+    if (i4 < n4) {
+      reinterpret_cast<float4*>(h + (size_t)r * d)[i4] = v[k];
+      norm_store<SPLIT>(x, r, d, i4, v[k], rs, gain);
     }
   }
 }
 
+template <bool SPLIT>
 __global__ __launch_bounds__(kNT) void resid_norm_kernel(const float* __restrict__ ws, int S,
                                                          long ws_stride, float* __restrict__ h,
                                                          const float* __restrict__ gain, float eps,
-                                                         float* __restrict__ x, int d) {
+                                                         void* __restrict__ x, int d) {
   __shared__ float red[kNT / 64];
   const int r = blockIdx.x, tid = threadIdx.x;
-  float v[kMaxPer];
+  const int n4 = d / 4;
+  float4* hrow = reinterpret_cast<float4*>(h + (size_t)r * d);
+  float4 v[kMaxV4];
   float ss = 0.f;
 #pragma unroll
-  for (int k = 0; k < kMaxPer; ++k) {
-    const int i = tid + k * kNT;
-    float a = 0.f;
-    if (i < d) {
-      const size_t off = (size_t)r * d + i;
-      a = h[off];
-      for (int s = 0; s < S; ++s) a += ws[s * ws_stride + off];
+  for (int k = 0; k < kMaxV4; ++k) {
+    const int i4 = tid + k * kNT;
+    v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i4 < n4) {
+      float4 p[kSplitMaxDev];
+#pragma unroll
+      for (int s = 0; s < kSplitMaxDev; ++s)
+        if (s < S) p[s] = reinterpret_cast<const float4*>(ws + s * ws_stride + (size_t)r * d)[i4];
+      float4 a = hrow[i4];
+#pragma unroll
+      for (int s = 0; s < kSplitMaxDev; ++s)
+        if (s < S) { a.x += p[s].x; a.y += p[s].y; a.z += p[s].z; a.w += p[s].w; }
+      v[k] = a;
+      ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
     }
-    v[k] = a;
-    ss += a * a;
   }
   const float tot = block_sum<kNT>(ss, red);
   const float rs = 1.f / sqrtf(tot / (float)d + eps);
 #pragma unroll
-  for (int k = 0; k < kMaxPer; ++k) {
-    const int i = tid + k * kNT;
-    if (i < d) {
-      h[(size_t)r * d + i] = v[k];
-      x[(size_t)r * d + i] = v[k] * rs * gain[i];
+  for (int k = 0; k < kMaxV4; ++k) {
+    const int i4 = tid + k * kNT;
+    if (i4 < n4) {
+      hrow[i4] = v[k];
+      norm_store<SPLIT>(x, r, d, i4, v[k], rs, gain);
     }
   }
 }
@@ -89,10 +114,16 @@ __global__ __launch_bounds__(kNT) void qkv_post_kernel(
   if (row_done && row_done[r]) return;
   const int dim = (nq + 2 * nkv) * hd;
   const size_t rbase = (size_t)r * dim;
-  for (int i = tid; i < dim; i += kNT) {
-    float a = 0.f;
-    for (int s = 0; s < S; ++s) a += ws[s * ws_stride + rbase + i];
-    buf[i] = a;
+  for (int i4 = tid; i4 < dim / 4; i4 += kNT) {
+    float4 p[kSplitMaxDev];
+#pragma unroll
+    for (int s = 0; s < kSplitMaxDev; ++s)
+      if (s < S) p[s] = reinterpret_cast<const float4*>(ws + s * ws_stride + rbase)[i4];
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int s = 0; s < kSplitMaxDev; ++s)
+      if (s < S) { a.x += p[s].x; a.y += p[s].y; a.z += p[s].z; a.w += p[s].w; }
+    reinterpret_cast<float4*>(buf)[i4] = a;
   }
   __syncthreads();
   const int slot = row_slot[r], pos = row_pos[r];
@@ -193,10 +224,10 @@ __global__ __launch_bounds__(kNT) void sample_partials_kernel(SampleArgs a) {
       const int v = base + e;
       if (v < v1) {
         const float sv = (zs[v] + (v == a.eos_id ? a.eos_bias_sen : 0.f)) / a.temp;
-        if (sv > ms) { ls = ls * expf(ms - sv) + 1.f; ms = sv; }
-        else ls += expf(sv - ms);
+        if (sv > ms) { ls = ls * fast_exp(ms - sv) + 1.f; ms = sv; }
+        else ls += fast_exp(sv - ms);
         const float so = own_sen ? sv : (zj[v] + (v == a.eos_id ? a.eos_bias_jun : 0.f)) / a.temp;
-        const float val = so + gumbel(w[e]);
+        const float val = so + gumbel_fast(w[e]);
         top = merge_top2(top, Top2{val, v, -INFINITY});
       }
     }
@@ -341,26 +372,31 @@ __global__ void gather_i32_kernel(const int32_t* src, const int32_t* idx, int n,
 }  // namespace
 
 hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, const float* gain,
-                             float eps, float* h, float* x, int R, hipStream_t st) {
+                             float eps, float* h, void* x, int R, hipStream_t st) {
   if (R <= 0) return hipSuccess;
   if (dt == DT_BF16)
-    hipLaunchKernelGGL((embed_norm_kernel<bf16_t>), dim3(R), dim3(kNT), 0, st, tok, (const bf16_t*)E, d,
+    hipLaunchKernelGGL((embed_norm_kernel<bf16_t, true>), dim3(R), dim3(kNT), 0, st, tok, (const bf16_t*)E, d,
                        gain, eps, h, x);
   else
-    hipLaunchKernelGGL((embed_norm_kernel<float>), dim3(R), dim3(kNT), 0, st, tok, (const float*)E, d,
+    hipLaunchKernelGGL((embed_norm_kernel<float, false>), dim3(R), dim3(kNT), 0, st, tok, (const float*)E, d,
                        gain, eps, h, x);
   return hipGetLastError();
 }
 
-hipError_t launch_resid_norm(const float* ws, int S, long ws_stride, float* h, const float* gain,
-                             float eps, float* x, int R, int d, hipStream_t st) {
+hipError_t launch_resid_norm(int dt, const float* ws, int S, long ws_stride, float* h, const float* gain,
+                             float eps, void* x, int R, int d, hipStream_t st) {
   if (R <= 0) return hipSuccess;
-  hipLaunchKernelGGL(resid_norm_kernel, dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
+  if (S > kSplitMaxDev) return hipErrorInvalidValue;
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL((resid_norm_kernel<true>), dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
+  else
+    hipLaunchKernelGGL((resid_norm_kernel<false>), dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
   return hipGetLastError();
 }
 
 hipError_t launch_qkv_post(const QkvPostArgs& a, hipStream_t st) {
   if (a.R <= 0) return hipSuccess;
+  if (a.S > kSplitMaxDev) return hipErrorInvalidValue;
   const size_t shm = sizeof(float) * (size_t)(a.nq + 2 * a.nkv) * a.hd;
   if (a.dt == DT_BF16)
     hipLaunchKernelGGL((qkv_post_kernel<bf16_t>), dim3(a.R), dim3(kNT), shm, st, a.ws, a.S, a.ws_stride,

@@ -18,11 +18,11 @@ enum Epi { EPI_PARTIAL = 0, EPI_STORE = 1, EPI_SWIGLU = 2 };
 // actually used (may be lower when K is short).
 struct GemmArgs {
   int dt;                 // weight dtype
-  const float* A;         // activations [M][K]
+  const void* A;          // activations [M][K] (split for bf16 weights, else fp32)
   const void* W;          // weights [rows][K]
   int M, N, K;
   int epi;
-  float* out;
+  float* out;             // EPI_SWIGLU: activation rows of width ldo (split for bf16)
   int ldo;
   long split_stride;
   int splits;
@@ -32,13 +32,16 @@ hipError_t launch_gemm(const GemmArgs& a, int* splits_used, hipStream_t st);
 // The K dimension granule of the MFMA path; other K use the VALU path.
 constexpr int kGemmBK = 64;
 
-// h[r] = E[tok[r]], x[r] = rmsnorm(h[r]) * gain (both fp32).
+// Activations x feeding a GEMM are in split format for bf16 models (see
+// common.h) and plain fp32 for fp32 models; both take 4 bytes per value.
+
+// h[r] = E[tok[r]], x[r] = rmsnorm(h[r]) * gain.
 hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, const float* gain,
-                             float eps, float* h, float* x, int R, hipStream_t st);
+                             float eps, float* h, void* x, int R, hipStream_t st);
 
 // h[r] += sum_s ws[s][r] (fixed order), then x[r] = rmsnorm(h[r]) * gain.
-hipError_t launch_resid_norm(const float* ws, int S, long ws_stride, float* h,
-                             const float* gain, float eps, float* x, int R, int d, hipStream_t st);
+hipError_t launch_resid_norm(int dt, const float* ws, int S, long ws_stride, float* h,
+                             const float* gain, float eps, void* x, int R, int d, hipStream_t st);
 
 struct CacheGeom {
   void* k;                // layer base of the K cache  [slot][kvh][ctx_stride][hd]
@@ -63,13 +66,14 @@ struct QkvPostArgs {
 hipError_t launch_qkv_post(const QkvPostArgs& a, hipStream_t st);
 
 // Decode/prefill attention of every row's query heads over positions
-// 0..row_pos[r] of its slot; out[r][h * hd + d] (fp32).
+// 0..row_pos[r] of its slot; out[r][h * hd + d] (an activation row of width
+// nq * hd, split for bf16 models).
 struct AttnArgs {
   int dt;
   const float* q; int R, nq, nkv, hd;
   CacheGeom cache;
   const int32_t* row_slot; const int32_t* row_pos; const int32_t* row_done;
-  float* out;
+  void* out;
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
 

@@ -73,8 +73,8 @@ struct Model {
   long layer_stride;          // elements
   long slot_stride;           // elements
   float* h;
-  float* xa;
-  float* xf;
+  void* xa;                   // activation rows (split format for bf16 models)
+  void* xf;
   float* q;
   float* ws;
   float* logits;
@@ -105,6 +105,10 @@ tandem_status check_cfg(const tandem_model_cfg* c, const char* who, std::string*
   }
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128) {
     snprintf(b, sizeof b, "%s: head_dim %d unsupported (32, 64 or 128)", who, c->head_dim);
+    return fail(err, TANDEM_E_UNSUPPORTED, b);
+  }
+  if (c->d_model % 8 || c->ffn_dim % 8) {
+    snprintf(b, sizeof b, "%s: d_model and ffn_dim must be multiples of 8", who);
     return fail(err, TANDEM_E_UNSUPPORTED, b);
   }
   if (c->d_model > 8192 || (long)(c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim > 16384) {
@@ -249,7 +253,8 @@ int choose_splits(int M, int N, int K, size_t ws_floats) {
   const int m_tiles = (M + 127) / 128, n_tiles = (N + 127) / 128;
   const int base = m_tiles * n_tiles;
   int S = (kTargetGroups + base - 1) / base;
-  // keep the partial-sum traffic (S * M * N * 4 bytes) below half the weight bytes (N * K * 2)
+  // keep the partial-sum traffic (S * M * N * 4 bytes, written and read back)
+  // below half the weight bytes (N * K * 2)
   const int traffic_cap = K / (4 * (M > 0 ? M : 1));
   if (S > traffic_cap) S = traffic_cap;
   if (S > kSplitMax) S = kSplitMax;
@@ -305,11 +310,11 @@ tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok,
     g.out = m.ws; g.ldo = d; g.split_stride = (long)R * d;
     g.splits = choose_splits(R, d, att, m.p.ws_floats);
     TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
-    TIMED(TANDEM_K_OTHER, launch_resid_norm(m.ws, S, (long)R * d, m.h, L.ffn_norm, c.rms_eps, m.xa, R, d, st));
+    TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, L.ffn_norm, c.rms_eps, m.xa, R, d, st));
 
     g = GemmArgs{};
     g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = R; g.N = c.ffn_dim; g.K = d; g.epi = EPI_SWIGLU;
-    g.out = m.xf; g.ldo = c.ffn_dim; g.splits = 1;
+    g.out = (float*)m.xf; g.ldo = c.ffn_dim; g.splits = 1;
     TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
 
     g = GemmArgs{};
@@ -318,7 +323,7 @@ tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok,
     g.splits = choose_splits(R, d, c.ffn_dim, m.p.ws_floats);
     TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
     const float* next_gain = (l + 1 < c.n_layers) ? m.layers[l + 1].attn_norm : m.final_norm;
-    TIMED(TANDEM_K_OTHER, launch_resid_norm(m.ws, S, (long)R * d, m.h, next_gain, c.rms_eps, m.xa, R, d, st));
+    TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, next_gain, c.rms_eps, m.xa, R, d, st));
   }
   if (lm_head) {
     GemmArgs g{};
@@ -430,10 +435,15 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     const tandem_model* m = md[i];
     if (!m->embed || !m->layers || !m->final_norm || !m->lm_head)
       return fail(nullptr, TANDEM_E_ARG, "tandem_init: a model weight pointer is NULL");
+    auto misaligned = [](const void* p) { return ((uintptr_t)p & 15u) != 0; };
+    if (misaligned(m->embed) || misaligned(m->final_norm) || misaligned(m->lm_head))
+      return fail(nullptr, TANDEM_E_ARG, "tandem_init: weights must be 16-byte aligned");
     for (int l = 0; l < m->cfg.n_layers; ++l) {
       const void* const* p = m->layers + 8 * l;
       if (!p[0] || !p[1] || !p[4] || !p[5] || !p[6] || !p[7] || (m->cfg.qk_norm && (!p[2] || !p[3])))
         return fail(nullptr, TANDEM_E_ARG, "tandem_init: a layer weight pointer is NULL");
+      for (int k = 0; k < 8; ++k)
+        if (p[k] && misaligned(p[k])) return fail(nullptr, TANDEM_E_ARG, "tandem_init: weights must be 16-byte aligned");
     }
   }
   if (sw->mode < TANDEM_REDRAW || sw->mode > TANDEM_ALTERNATE)
@@ -490,8 +500,8 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     m.vc = kv + kv_off + m.p.kv_half;
     kv_off += 2 * m.p.kv_half;
     m.h = (float*)(sc + m.p.off_h);
-    m.xa = (float*)(sc + m.p.off_xa);
-    m.xf = (float*)(sc + m.p.off_xf);
+    m.xa = sc + m.p.off_xa;
+    m.xf = sc + m.p.off_xf;
     m.q = (float*)(sc + m.p.off_q);
     m.ws = (float*)(sc + m.p.off_ws);
     m.logits = (float*)(sc + m.p.off_logits);
