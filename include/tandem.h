@@ -60,7 +60,8 @@ enum { TANDEM_JUNIOR = 0, TANDEM_SENIOR = 1, TANDEM_DRAW = 2 };
  *   ALTERNATE owner always flips (the deterministic reasoning-step schedule). */
 enum { TANDEM_REDRAW = 0, TANDEM_SWITCH = 1, TANDEM_ALTERNATE = 2 };
 
-/* element type of the weights and of the KV cache (activations are always fp32) */
+/* element type of the weights and of the KV cache.  The residual stream is
+ * fp32; inputs of the bf16 projections are carried as bf16 hi + lo pairs. */
 enum { TANDEM_BF16 = 0, TANDEM_F32 = 1 };
 
 /* Shape of one pre-norm decoder: RMSNorm, grouped-query attention with

@@ -113,7 +113,7 @@ def _small_pair(vocab=32000):
 
 
 def workload(name: str) -> Workload:
-    """The five synthetic workloads (scope-table shapes, readings Q1-Q15)."""
+    """The synthetic workloads by name (model shapes, batch, schedule; readings Q1-Q15)."""
     if name == "tiny":
         sen = ModelShape(2, 128, 4, 2, 32, 512, 512, dtype="f32")
         jun = ModelShape(1, 64, 2, 1, 32, 256, 512, dtype="f32")
