@@ -11,6 +11,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
@@ -76,11 +77,48 @@ typedef __attribute__((address_space(1))) void glb_void_t;
 __device__ __forceinline__ void load_lds16(const void* gsrc, void* lds_base) {
   __builtin_amdgcn_global_load_lds((glb_void_t*)gsrc, (lds_void_t*)lds_base, 16, 0, 0);
 }
+// Same, for data read once (non-temporal: not kept in the caches).
+__device__ __forceinline__ void load_lds16_nt(const void* gsrc, void* lds_base) {
+  __builtin_amdgcn_global_load_lds((glb_void_t*)gsrc, (lds_void_t*)lds_base, 16, 0, 2);
+}
 
 // LDS read the compiler does not see as a memory access: it then cannot
 // conflate it with pending LDS-DMA writes (which would make it drain every
 // outstanding load).  The caller must wait with lds_wait() before using the
 // result and must order ring reuse with its own barriers.
+// Tiled K/V cache.  A (slot, kv head) plane holds ctx_stride positions in
+// chunks of 16; inside a chunk the elements sit in the order the decode
+// attention MFMAs consume them, so every 64-lane load of a chunk is one
+// contiguous 1 KB piece (for 16-bit elements).
+//   K: piece dc (dims 32dc .. 32dc+31), lane g*16 + c16 holds position c16,
+//      dims 32dc + 8g .. +7.
+//   V: piece j (dims 32j .. 32j+31), lane g*16 + c16 holds positions
+//      4g .. 4g+3 of dim 32j + c16, then of dim 32j + 16 + c16.
+// Both are element indices inside the plane; hd is a multiple of 32.
+__device__ __forceinline__ int kv_k_index(int p, int d, int hd) {
+  return (p >> 4) * 16 * hd + ((((d >> 5) * 64) + ((d >> 3) & 3) * 16 + (p & 15)) << 3) + (d & 7);
+}
+__device__ __forceinline__ int kv_v_index(int p, int d, int hd) {
+  const int j = p & 15;
+  return (p >> 4) * 16 * hd + ((((d >> 5) * 64) + (j >> 2) * 16 + (d & 15)) << 3) + (((d >> 4) & 1) << 2) + (j & 3);
+}
+
+// Raw buffer access: a uniform base and a byte size (reads at or past the
+// size return zeros), per-lane 32-bit byte offsets, a uniform byte offset.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+// Streaming read (non-temporal: data read once, not kept in the caches).
+__device__ __forceinline__ u32x4_t buf_load16_nt(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 2);
+}
+__device__ __forceinline__ u32x2_t buf_load8(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+}
+
 __device__ __forceinline__ u32x4_t lds_read16(uint32_t lds_addr) {
   u32x4_t r;
   asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(lds_addr));

@@ -3,19 +3,19 @@
 // positions 0..its own position of the prompt's cache).
 //
 // bf16 path (HD in {64, 128}): one workgroup per (kv head, row); its four
-// waves take interleaved 32-position chunks and keep their own online
-// softmax, merged through LDS at the end.  Both products run on MFMA
-// 16x16x32 bf16:
-//   S^T = K . Q^T   A = 16 cached keys x 32 dims, B = 32 dims x 16 query
-//                   heads of the group (heads >= G are zero);
-//   O  += P . V     A = 16 heads x 32 positions (the softmax weights, which
-//                   each lane already holds for exactly the positions its
-//                   k-group needs), B = 32 positions x 16 dims read from the
-//                   transposed V cache (4 consecutive positions per load).
+// waves take interleaved 16-position chunks of the tiled cache and keep
+// their own online softmax, merged through LDS at the end.  The products
+// run on MFMA:
+//   S^T = K . Q^T   16x16x32: A = 16 cached keys x 32 dims, B = 32 dims x 16
+//                   query heads of the group (heads >= G are zero);
+//   O  += P . V     16x16x16: A = 16 heads x 16 positions, which is exactly
+//                   the S^T accumulator layout (lane (g, c) holds positions
+//                   4g .. 4g+3 of head c), B = 16 positions x 16 dims.
 // The fp32 query and the fp32 softmax weights enter as bf16 high + low parts
-// (two MFMAs each), so only the cache itself is bf16.  K/V stream straight
-// from HBM into registers in MFMA layout; one load of a kv head's keys serves
-// all G query heads of its group.
+// (two MFMAs each), so only the cache itself is bf16.  The cache is tiled in
+// operand order: every load is one contiguous 1 KB piece per wave, issued
+// as a non-temporal buffer load one chunk ahead of the arithmetic.  One load
+// of a kv head's keys serves all G query heads of its group.
 //
 // fp32 path: a plain VALU kernel, one workgroup per (query head, row).
 #include "common.h"
@@ -24,6 +24,8 @@
 namespace tandem {
 
 namespace {
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void split8(const float* x, bf16x8_t& hi, bf16x8_t& lo) {
   uint32_t h[4], l[4];
@@ -38,109 +40,118 @@ __device__ __forceinline__ void split8(const float* x, bf16x8_t& hi, bf16x8_t& l
   lo = __builtin_bit_cast(bf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
 }
 
-template <int HD>
-struct KVChunk {
-  uint4 k[2][HD / 32];            // keys: positions p0 + 16 pb + c16, dims of lane group g
-  uint2 v[HD / 16][2];            // values: dim db*16 + c16, positions p0 + 4g .. +3 and p0 + 16 + 4g .. +3
-};
-
-template <int HD>
-__device__ __forceinline__ void load_chunk(KVChunk<HD>& c, const bf16_t* kbase, const bf16_t* vbase, int p0,
-                                           int ctx, int ctx_stride, int g, int c16) {
+// 4 fp32 -> bf16 high parts and bf16 low parts (x ~ hi + lo), as MFMA operands
+__device__ __forceinline__ void split4(const float* x, s16x4_t& hi, s16x4_t& lo) {
+  uint32_t h[2], l[2];
 #pragma unroll
-  for (int pb = 0; pb < 2; ++pb) {
-    const int p = min(p0 + 16 * pb + c16, ctx - 1);
-    const uint4* kp = reinterpret_cast<const uint4*>(kbase + (size_t)p * HD + g * (HD / 4));
-#pragma unroll
-    for (int dc = 0; dc < HD / 32; ++dc) c.k[pb][dc] = kp[dc];
+  for (int e = 0; e < 2; ++e) {
+    const bf16_t h0 = f2bf(x[2 * e]), h1 = f2bf(x[2 * e + 1]);
+    const bf16_t l0 = f2bf(x[2 * e] - bf2f(h0)), l1 = f2bf(x[2 * e + 1] - bf2f(h1));
+    h[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    l[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
   }
-#pragma unroll
-  for (int db = 0; db < HD / 16; ++db) {
-    const bf16_t* vp = vbase + (size_t)(db * 16 + c16) * ctx_stride + p0 + 4 * g;
-    c.v[db][0] = *reinterpret_cast<const uint2*>(vp);
-    c.v[db][1] = *reinterpret_cast<const uint2*>(vp + 16);
-  }
+  hi = __builtin_bit_cast(s16x4_t, make_uint2(h[0], h[1]));
+  lo = __builtin_bit_cast(s16x4_t, make_uint2(l[0], l[1]));
 }
 
-template <int HD, int GQA>
-struct AttnState {
-  float m_run, l_run;
-  f32x4_t o[HD / 16];
+// One 16-position chunk of a kv head's keys and values in MFMA operand
+// layout (the cache's tiled order): k[dc] = K[pos c16][32dc + 8g .. +7];
+// v[j] = V[pos 4g .. +3][32j + c16] then V[pos 4g .. +3][32j + 16 + c16].
+template <int HD>
+struct KV16 {
+  u32x4_t k[HD / 32];
+  u32x4_t v[HD / 32];
 };
 
-template <int HD, int GQA>
-__device__ __forceinline__ void attend_chunk(AttnState<HD, GQA>& st, const KVChunk<HD>& c, const bf16x8_t* qh,
-                                             const bf16x8_t* ql, int p0, int ctx, float scale, int g) {
+template <int HD>
+__device__ __forceinline__ void load_chunk(KV16<HD>& c, __amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int chunk,
+                                           int lane) {
+  const int base = chunk * 32 * HD + lane * 16;   // bytes: 16 positions x HD x 2
+#pragma unroll
+  for (int j = 0; j < HD / 32; ++j) c.k[j] = buf_load16_nt(kr, base + j * 1024, 0);
+#pragma unroll
+  for (int j = 0; j < HD / 32; ++j) c.v[j] = buf_load16_nt(vr, base + j * 1024, 0);
+}
+
+// Orders the loads issued so far before everything that reads chunk c: the
+// empty asm "modifies" every register of c and clobbers memory, so earlier
+// loads cannot sink below it, the arithmetic on c cannot rise above it, and
+// the only wait the compiler places here is for c's own loads.
+template <int HD>
+__device__ __forceinline__ void pin_chunk(KV16<HD>& c) {
+#pragma unroll
+  for (int j = 0; j < HD / 32; ++j) asm volatile("" : "+v"(c.k[j]) : : "memory");
+#pragma unroll
+  for (int j = 0; j < HD / 32; ++j) asm volatile("" : "+v"(c.v[j]) : : "memory");
+}
+
+template <int HD>
+struct AttnState {
+  float m_run, l_run;             // running max (log2 units) and this lane's share of the sum
+  f32x4_t o[HD / 16];             // O[head 4g + i][dim 16 db + c16]
+};
+
+template <int HD>
+__device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, const bf16x8_t* qh, const bf16x8_t* ql,
+                                             int p0, int ctx, float scale, int g) {
   constexpr int DC = HD / 32, DB = HD / 16;
-  // S^T: lane holds positions p0 + 16 pb + 4g + i for head c16
-  float s[2][4];
-  // two independent accumulators per position block (hi and lo query parts)
-  // so consecutive MFMAs never wait on each other
-  f32x4_t acc[2][2];
+  f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int pb = 0; pb < 2; ++pb) acc[pb][0] = acc[pb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int dc = 0; dc < DC; ++dc) {
+    const bf16x8_t kk = __builtin_bit_cast(bf16x8_t, c.k[dc]);
+    acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qh[dc], acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, ql[dc], acc1, 0, 0, 0);
+  }
+  // lane (g, c16): scores of positions p0 + 4g + i for head c16
+  const int pg = p0 + 4 * g;
+  float s[4];
 #pragma unroll
-  for (int dc = 0; dc < DC; ++dc)
-#pragma unroll
-    for (int pb = 0; pb < 2; ++pb) {
-      const bf16x8_t kk = __builtin_bit_cast(bf16x8_t, c.k[pb][dc]);
-      acc[pb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qh[dc], acc[pb][0], 0, 0, 0);
-      acc[pb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, ql[dc], acc[pb][1], 0, 0, 0);
-    }
-#pragma unroll
-  for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int pp = p0 + 16 * pb + 4 * g + i;
-      s[pb][i] = pp < ctx ? (acc[pb][0][i] + acc[pb][1][i]) * scale : -INFINITY;
-    }
-  float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
-                   fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+  for (int i = 0; i < 4; ++i) s[i] = pg + i < ctx ? (acc0[i] + acc1[i]) * scale : -INFINITY;
+  float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
   mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
   const float m_new = fmaxf(st.m_run, mx);
   const float alpha = exp2f(st.m_run - m_new);
-  float pr[8];
-  float psum = 0.f;
+  float pr[4];
 #pragma unroll
-  for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float p = exp2f(s[pb][i] - m_new);
-      pr[4 * pb + i] = p;
-      psum += p;
-    }
-  st.l_run = st.l_run * alpha + psum;
+  for (int i = 0; i < 4; ++i) pr[i] = exp2f(s[i] - m_new);
+  st.l_run = st.l_run * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
   st.m_run = m_new;
-  bf16x8_t ph, pl;
-  split8(pr, ph, pl);
-  // rescale the accumulator rows (heads 4g + i) by their heads' alpha
-  float ai[4];
+  s16x4_t ph, pl;
+  split4(pr, ph, pl);
+  // rescale the accumulator rows (heads 4g + i) only when some head's max moved
+  if (__ballot(alpha != 1.f)) {
+    float ai[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) ai[i] = __shfl(alpha, 4 * g + i, 64);
-  // mask values past the context (stale cache contents must not leak as 0 * inf)
-  const int nvalid0 = ctx - (p0 + 4 * g), nvalid1 = ctx - (p0 + 16 + 4 * g);
-  bf16x8_t vv[DB];
+    for (int i = 0; i < 4; ++i) ai[i] = __shfl(alpha, 4 * g + i, 64);
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    uint2 v0 = c.v[db][0], v1 = c.v[db][1];
-    if (nvalid0 < 4) {
-      v0.x = nvalid0 <= 0 ? 0u : (nvalid0 == 1 ? (v0.x & 0xFFFFu) : v0.x);
-      v0.y = nvalid0 <= 2 ? 0u : (v0.y & 0xFFFFu);
-    }
-    if (nvalid1 < 4) {
-      v1.x = nvalid1 <= 0 ? 0u : (nvalid1 == 1 ? (v1.x & 0xFFFFu) : v1.x);
-      v1.y = nvalid1 <= 2 ? 0u : (v1.y & 0xFFFFu);
-    }
-    vv[db] = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) st.o[db][i] *= ai[i];
+      for (int i = 0; i < 4; ++i) st.o[db][i] *= ai[i];
+  }
+  // positions at or past the context hold stale cache contents: zero them so
+  // that 0 * (stale) cannot produce NaN
+  if (p0 + 16 > ctx) {
+    // keep the first nv of this lane's four positions (16 bits each)
+    const int nv = min(max(ctx - pg, 0), 4);
+    const uint64_t keep = nv == 4 ? ~0ull : (1ull << (16 * nv)) - 1ull;
+    const uint32_t klo = (uint32_t)keep, khi = (uint32_t)(keep >> 32);
+#pragma unroll
+    for (int j = 0; j < DC; ++j) c.v[j] &= u32x4_t{klo, khi, klo, khi};
   }
   // hi parts over all dim blocks, then lo parts (independent consecutive MFMAs)
 #pragma unroll
-  for (int db = 0; db < DB; ++db) st.o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vv[db], st.o[db], 0, 0, 0);
+  for (int db = 0; db < DB; ++db) {
+    const u32x4_t v = c.v[db >> 1];
+    const s16x4_t vv = __builtin_bit_cast(s16x4_t, (db & 1) ? make_uint2(v.z, v.w) : make_uint2(v.x, v.y));
+    st.o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ph, vv, st.o[db], 0, 0, 0);
+  }
 #pragma unroll
-  for (int db = 0; db < DB; ++db) st.o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, vv[db], st.o[db], 0, 0, 0);
+  for (int db = 0; db < DB; ++db) {
+    const u32x4_t v = c.v[db >> 1];
+    const s16x4_t vv = __builtin_bit_cast(s16x4_t, (db & 1) ? make_uint2(v.z, v.w) : make_uint2(v.x, v.y));
+    st.o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pl, vv, st.o[db], 0, 0, 0);
+  }
 }
 
 template <int HD, int GQA>
@@ -151,7 +162,6 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
     bf16_t* __restrict__ out, int nq) {
   constexpr int DC = HD / 32;     // k-steps of the S product
   constexpr int DB = HD / 16;     // 16-dim blocks of the O product
-  constexpr int KSEG = HD / 4;    // dims per lane group
   __shared__ float sm_m[4][16];
   __shared__ float sm_l[4][16];
   __shared__ float sm_o[4][GQA][HD];
@@ -167,18 +177,19 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   }
   const int slot = row_slot[r];
   const int ctx = row_pos[r] + 1;
-  const bf16_t* kbase = kc + (size_t)slot * slot_stride + (size_t)kh * ctx_stride * HD;
-  const bf16_t* vbase = vc + (size_t)slot * slot_stride + (size_t)kh * HD * ctx_stride;
+  const size_t plane = (size_t)slot * slot_stride + (size_t)kh * ctx_stride * HD;
+  const __amdgpu_buffer_rsrc_t kr = buf_rsrc(kc + plane, (uint32_t)ctx_stride * HD * 2);
+  const __amdgpu_buffer_rsrc_t vr = buf_rsrc(vc + plane, (uint32_t)ctx_stride * HD * 2);
 
-  // Q^T operand: column = query head c16 of this group, k = dims of group g
+  // Q^T operand: column = query head c16 of this group, k = dims 32dc + 8g .. +7
   bf16x8_t qh[DC], ql[DC];
   {
     const bool valid = c16 < GQA;
-    const float* qp = q + ((size_t)r * nq + kh * GQA + (valid ? c16 : 0)) * HD + g * KSEG;
+    const float* qp = q + ((size_t)r * nq + kh * GQA + (valid ? c16 : 0)) * HD + 8 * g;
 #pragma unroll
     for (int dc = 0; dc < DC; ++dc) {
-      const float4 a = *reinterpret_cast<const float4*>(qp + 8 * dc);
-      const float4 b = *reinterpret_cast<const float4*>(qp + 8 * dc + 4);
+      const float4 a = *reinterpret_cast<const float4*>(qp + 32 * dc);
+      const float4 b = *reinterpret_cast<const float4*>(qp + 32 * dc + 4);
       float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
 #pragma unroll
       for (int e = 0; e < 8; ++e) x[e] = valid ? x[e] : 0.f;
@@ -187,26 +198,34 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   }
   const float scale = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
 
-  AttnState<HD, GQA> st;
+  AttnState<HD> st;
   st.m_run = -INFINITY;
   st.l_run = 0.f;
 #pragma unroll
   for (int db = 0; db < DB; ++db) st.o[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // two register buffers: the next chunk of this wave is in flight while the
-  // current one is consumed; past the end the current chunk is reloaded (an
-  // L2 hit) so every iteration issues the same loads
-  const int nchunk = (ctx + 31) >> 5;
-  KVChunk<HD> ca, cb;
-  if (wave < nchunk) load_chunk<HD>(ca, kbase, vbase, 32 * wave, ctx, ctx_stride, g, c16);
-  for (int ch = wave; ch < nchunk; ch += 8) {
-    const int nb = ch + 4 < nchunk ? ch + 4 : ch;
-    load_chunk<HD>(cb, kbase, vbase, 32 * nb, ctx, ctx_stride, g, c16);
-    attend_chunk<HD, GQA>(st, ca, qh, ql, 32 * ch, ctx, scale, g);
-    if (ch + 4 >= nchunk) break;
-    const int na = ch + 8 < nchunk ? ch + 8 : ch + 4;
-    load_chunk<HD>(ca, kbase, vbase, 32 * na, ctx, ctx_stride, g, c16);
-    attend_chunk<HD, GQA>(st, cb, qh, ql, 32 * (ch + 4), ctx, scale, g);
+  // Two register buffers: the next chunk of this wave is in flight while the
+  // current one is consumed.  Wave w owns chunks w, w + 4, w + 8, ...; the
+  // loop walks them in pairs and always issues the same loads (indices past
+  // the wave's last chunk are clamped to it: a cache hit), so the only
+  // condition inside is whether the pair's second chunk exists.  pin_chunk
+  // keeps the next chunk's loads ahead of the current chunk's arithmetic
+  // (left alone, the compiler sinks the loads to their first use and the
+  // prefetch disappears).
+  const int nchunk = (ctx + 15) >> 4;
+  const int nmine = nchunk > wave ? (nchunk - wave + 3) >> 2 : 0;
+  auto chunk_at = [&](int i) { return wave + 4 * min(i, nmine - 1); };
+  if (nmine > 0) {
+    KV16<HD> ca, cb;
+    load_chunk<HD>(ca, kr, vr, chunk_at(0), lane);
+    for (int i = 0; i < nmine; i += 2) {
+      load_chunk<HD>(cb, kr, vr, chunk_at(i + 1), lane);
+      pin_chunk<HD>(ca);
+      attend_chunk<HD>(st, ca, qh, ql, 16 * chunk_at(i), ctx, scale, g);
+      load_chunk<HD>(ca, kr, vr, chunk_at(i + 2), lane);
+      pin_chunk<HD>(cb);
+      if (i + 1 < nmine) attend_chunk<HD>(st, cb, qh, ql, 16 * chunk_at(i + 1), ctx, scale, g);
+    }
   }
 
   float l_run = st.l_run;
@@ -259,7 +278,7 @@ __global__ __launch_bounds__(128) void attn_valu_kernel(
   const int slot = row_slot[r];
   const int ctx = row_pos[r] + 1;
   const KT* kbase = kc + (size_t)slot * slot_stride + (size_t)kh * ctx_stride * hd;
-  const KT* vbase = vc + (size_t)slot * slot_stride + (size_t)kh * hd * ctx_stride;
+  const KT* vbase = vc + (size_t)slot * slot_stride + (size_t)kh * ctx_stride * hd;
   if (tid < hd) sq[tid] = q[((size_t)r * nq + h) * hd + tid];
   __syncthreads();
   const float scale = 1.f / sqrtf((float)hd);
@@ -269,7 +288,7 @@ __global__ __launch_bounds__(128) void attn_valu_kernel(
     float s = -INFINITY;
     if (p < ctx) {
       float acc = 0.f;
-      for (int d = 0; d < hd; ++d) acc += sq[d] * ld(kbase + (size_t)p * hd + d);
+      for (int d = 0; d < hd; ++d) acc += sq[d] * ld(kbase + kv_k_index(p, d, hd));
       s = acc * scale;
     }
     float mx = wave_max(s);
@@ -290,7 +309,7 @@ __global__ __launch_bounds__(128) void attn_valu_kernel(
     if (tid < hd) {
       const int n = min(128, ctx - p0);
       float acc = 0.f;
-      for (int t = 0; t < n; ++t) acc += sp[t] * ld(vbase + (size_t)tid * ctx_stride + p0 + t);
+      for (int t = 0; t < n; ++t) acc += sp[t] * ld(vbase + kv_v_index(p0 + t, tid, hd));
       o = o * alpha + acc;
     }
     m_run = m_new;

@@ -113,7 +113,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(
     for (int i = 0; i < G::NA; ++i) load_lds16(asrc[i] + (size_t)c * 2 * BK, st + (16 * i + 4 * wave) * 256);
 #pragma unroll
     for (int i = 0; i < G::NWD; ++i)
-      load_lds16(wsrc[i] + (size_t)c * BK, st + G::ASTAGE + ((G::BN / 4) * wave + 8 * i) * 128);
+      load_lds16_nt(wsrc[i] + (size_t)c * BK, st + G::ASTAGE + ((G::BN / 4) * wave + 8 * i) * 128);
   };
 
   f32x16_t acc[G::MBW][G::NBW];

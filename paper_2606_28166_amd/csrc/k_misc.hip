@@ -100,8 +100,8 @@ __global__ __launch_bounds__(kNT) void resid_norm_kernel(const float* __restrict
 // ------------------------------------------------------------ qkv post
 // One workgroup per row.  Sums the split-K partials, applies the optional
 // per-head q/k RMSNorm and NeoX rotary embedding (lane i rotates the pair
-// (i, i + hd/2)), writes q, and appends k (row-major [pos][hd]) and v
-// (transposed [hd][pos]) at the row's (slot, pos).
+// (i, i + hd/2)), writes q, and appends k and v at the row's (slot, pos) of
+// the tiled cache.
 template <typename KT>
 __global__ __launch_bounds__(kNT) void qkv_post_kernel(
     const float* __restrict__ ws, int S, long ws_stride, int nq, int nkv, int hd,
@@ -155,16 +155,16 @@ __global__ __launch_bounds__(kNT) void qkv_post_kernel(
         qo[lane] = y1;
         qo[lane + half] = y2;
       } else {
-        KT* ko = kc + (size_t)slot * slot_stride + ((size_t)(head - nq) * ctx_stride + pos) * hd;
-        st(ko + lane, y1);
-        st(ko + lane + half, y2);
+        KT* ko = kc + (size_t)slot * slot_stride + (size_t)(head - nq) * ctx_stride * hd;
+        st(ko + kv_k_index(pos, lane, hd), y1);
+        st(ko + kv_k_index(pos, lane + half, hd), y2);
       }
     }
   }
   for (int e = tid; e < nkv * hd; e += kNT) {
     const int kh = e / hd, d = e % hd;
-    KT* vo = vc + (size_t)slot * slot_stride + ((size_t)kh * hd + d) * ctx_stride + pos;
-    st(vo, buf[(nq + nkv) * hd + e]);
+    KT* vo = vc + (size_t)slot * slot_stride + (size_t)kh * ctx_stride * hd;
+    st(vo + kv_v_index(pos, d, hd), buf[(nq + nkv) * hd + e]);
   }
 }
 
@@ -326,15 +326,15 @@ __global__ __launch_bounds__(kNT) void kv_replicate_kernel(T* kc, T* vc, int nkv
   const int layer = lk / nkv, kh = lk % nkv;
   const int dst = dst0 + blockIdx.y;
   const size_t kh_off = (size_t)kh * ctx_stride * hd;
+  // positions 0 .. n_pos-1 occupy the whole 16-position chunks that hold
+  // them: a contiguous prefix of each tiled plane
+  const long n = (long)((n_pos + 15) >> 4) * 16 * hd;
   const T* ks = kc + layer * layer_stride + (size_t)src * slot_stride + kh_off;
   T* kd = kc + layer * layer_stride + (size_t)dst * slot_stride + kh_off;
-  for (long e = threadIdx.x; e < (long)n_pos * hd; e += kNT) kd[e] = ks[e];
+  for (long e = threadIdx.x; e < n; e += kNT) kd[e] = ks[e];
   const T* vs = vc + layer * layer_stride + (size_t)src * slot_stride + kh_off;
   T* vd = vc + layer * layer_stride + (size_t)dst * slot_stride + kh_off;
-  for (long e = threadIdx.x; e < (long)n_pos * hd; e += kNT) {
-    const long d = e / n_pos, p = e % n_pos;
-    vd[d * ctx_stride + p] = vs[d * ctx_stride + p];
-  }
+  for (long e = threadIdx.x; e < n; e += kNT) vd[e] = vs[e];
 }
 
 __global__ void init_state_kernel(InitStateArgs a) {

@@ -44,8 +44,8 @@ hipError_t launch_resid_norm(int dt, const float* ws, int S, long ws_stride, flo
                              const float* gain, float eps, void* x, int R, int d, hipStream_t st);
 
 struct CacheGeom {
-  void* k;                // layer base of the K cache  [slot][kvh][ctx_stride][hd]
-  void* v;                // layer base of the V cache  [slot][kvh][hd][ctx_stride] (transposed)
+  void* k;                // layer base of the K cache  [slot][kvh][tiled plane of ctx_stride x hd]
+  void* v;                // layer base of the V cache  [slot][kvh][tiled plane of ctx_stride x hd]
   int ctx_stride;
   long slot_stride;       // elements between slots (= n_kv * ctx_stride * hd)
 };
