@@ -185,6 +185,10 @@ struct tandem_handle {
   unsigned long long thr;
   uint32_t key0, key1;
   hipStream_t stream;
+  // The two models' forwards are independent until sampling: the junior's
+  // runs on a second stream forked from and joined back into `stream`.
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   int32_t *owner, *c, *t, *pos, *pending, *done;
   int32_t* seq_slot;
   int32_t *row_slot, *row_pos, *row_tok, *row_src;
@@ -206,8 +210,8 @@ struct tandem_handle {
 
 namespace {
 
-// Record a begin event for a kernel class (no-op unless timing is enabled).
-hipError_t tim_begin(tandem_handle* h, int klass, size_t* idx) {
+// Record a begin event for a kernel class on stream st (no-op unless timing is enabled).
+hipError_t tim_begin(tandem_handle* h, int klass, size_t* idx, hipStream_t st) {
   *idx = SIZE_MAX;
   if (!(h->timing & (1 << klass))) return hipSuccess;
   while (h->ev_pool.size() < h->ev_used + 2) {
@@ -219,22 +223,22 @@ hipError_t tim_begin(tandem_handle* h, int klass, size_t* idx) {
   *idx = h->ev_used;
   h->ev_used += 2;
   h->ev_marks[klass].push_back({klass, *idx});
-  return hipEventRecord(h->ev_pool[*idx], h->stream);
+  return hipEventRecord(h->ev_pool[*idx], st);
 }
-hipError_t tim_end(tandem_handle* h, size_t idx) {
+hipError_t tim_end(tandem_handle* h, size_t idx, hipStream_t st) {
   if (idx == SIZE_MAX) return hipSuccess;
-  return hipEventRecord(h->ev_pool[idx + 1], h->stream);
+  return hipEventRecord(h->ev_pool[idx + 1], st);
 }
 
 }  // namespace
 
-// Launch one kernel class between timing events.
+// Launch one kernel class between timing events on the launch stream `st`.
 #define TIMED(klass, expr)                                                                 \
   do {                                                                                     \
     size_t ti_ = 0;                                                                        \
-    HIPCHK(tim_begin(h, (klass), &ti_));                                                   \
+    HIPCHK(tim_begin(h, (klass), &ti_, st));                                               \
     HIPCHK(expr);                                                                          \
-    HIPCHK(tim_end(h, ti_));                                                               \
+    HIPCHK(tim_end(h, ti_, st));                                                           \
   } while (0)
 
 #define HIPCHK(expr)                                                                       \
@@ -268,12 +272,11 @@ int choose_splits(int M, int N, int K, size_t ws_floats) {
 // position from the row arrays; done rows (row_done != NULL) skip the cache
 // append and produce zero attention.  With lm_head the logits land in m.logits.
 tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok, const int32_t* row_slot,
-                      const int32_t* row_pos, const int32_t* row_done, bool lm_head) {
+                      const int32_t* row_pos, const int32_t* row_done, bool lm_head, hipStream_t st) {
   const tandem_model_cfg& c = m.cfg;
   const int dt = c.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32;
   const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads;
   const int qkv = m.p.qkv_dim, att = m.p.att_dim;
-  hipStream_t st = h->stream;
   TIMED(TANDEM_K_OTHER, launch_embed_norm(dt, row_tok, m.embed, d, m.layers[0].attn_norm, c.rms_eps, m.h, m.xa, R, st));
   for (int l = 0; l < c.n_layers; ++l) {
     const Layer& L = m.layers[l];
@@ -335,14 +338,30 @@ tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok,
   return TANDEM_OK;
 }
 
+// Both models' forwards over the same rows: the junior on the side stream,
+// the senior on the main stream, joined before anything that reads either.
+tandem_status forward_pair(tandem_handle* h, int R, const int32_t* row_tok, const int32_t* row_slot,
+                           const int32_t* row_pos, const int32_t* row_done, bool lm_head) {
+  hipStream_t st = h->stream;
+  HIPCHK(hipEventRecord(h->ev_fork, st));
+  HIPCHK(hipStreamWaitEvent(h->side, h->ev_fork, 0));
+  tandem_status s = forward(h, h->m[1], R, row_tok, row_slot, row_pos, row_done, lm_head, h->side);
+  if (s != TANDEM_OK) return s;
+  s = forward(h, h->m[0], R, row_tok, row_slot, row_pos, row_done, lm_head, st);
+  if (s != TANDEM_OK) return s;
+  HIPCHK(hipEventRecord(h->ev_join, h->side));
+  HIPCHK(hipStreamWaitEvent(st, h->ev_join, 0));
+  return TANDEM_OK;
+}
+
 tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg, int32_t* n_active) {
   if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
   if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
   if (!h->prefilled) return fail(&h->err, TANDEM_E_STATE, "tandem_step before tandem_prefill");
   const int R = h->n_seq;
   hipStream_t st = h->stream;
-  for (int i = 0; i < 2; ++i) {
-    tandem_status s = forward(h, h->m[i], R, h->pending, h->seq_slot, h->pos, h->done, true);
+  {
+    tandem_status s = forward_pair(h, R, h->pending, h->seq_slot, h->pos, h->done, true);
     if (s != TANDEM_OK) return s;
   }
   const int V = h->m[0].cfg.vocab;
@@ -525,11 +544,20 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   auto bail = [&](hipError_t e, const char* what) {
     std::string msg = std::string("HIP error in tandem_init (") + what + "): " + hipGetErrorString(e);
     if (h->h_count) (void)hipHostFree(h->h_count);
+    if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
+    if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+    if (h->side) (void)hipStreamDestroy(h->side);
     delete h;
     return fail(nullptr, TANDEM_E_HIP, msg);
   };
   hipError_t e = hipHostMalloc((void**)&h->h_count, 4, hipHostMallocDefault);
   if (e != hipSuccess) { h->h_count = nullptr; return bail(e, "hipHostMalloc"); }
+  e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
+  if (e != hipSuccess) { h->side = nullptr; return bail(e, "side stream"); }
+  e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
+  if (e != hipSuccess) { h->ev_fork = nullptr; return bail(e, "fork event"); }
+  e = hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming);
+  if (e != hipSuccess) { h->ev_join = nullptr; return bail(e, "join event"); }
   for (int i = 0; i < 2; ++i) {
     e = launch_rope_table(h->m[i].cfg.rope_theta, h->m[i].cfg.head_dim, P.ctx_stride, h->m[i].rope, h->stream);
     if (e != hipSuccess) return bail(e, "rope table");
@@ -610,8 +638,8 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
       HIPCHK(hipMemcpyAsync(h->row_pos, rows.data() + nr, (size_t)nr * 4, hipMemcpyHostToDevice, st));
       HIPCHK(hipMemcpyAsync(h->row_src, rows.data() + 2 * nr, (size_t)nr * 4, hipMemcpyHostToDevice, st));
       TIMED(TANDEM_K_OTHER, launch_gather_i32(prompt_tokens, h->row_src, nr, h->row_tok, st));
-      for (int i = 0; i < 2; ++i) {
-        tandem_status s = forward(h, h->m[i], nr, h->row_tok, h->row_slot, h->row_pos, nullptr, false);
+      {
+        tandem_status s = forward_pair(h, nr, h->row_tok, h->row_slot, h->row_pos, nullptr, false);
         if (s != TANDEM_OK) return s;
       }
       for (int j = j0; j < j1; ++j) {
@@ -692,7 +720,11 @@ tandem_status tandem_timing_read(tandem_handle* h, int32_t kernel_class, double*
 void tandem_destroy(tandem_handle* h) {
   if (!h) return;
   (void)hipStreamSynchronize(h->stream);
+  if (h->side) (void)hipStreamSynchronize(h->side);
   for (hipEvent_t e : h->ev_pool) (void)hipEventDestroy(e);
+  if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
+  if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+  if (h->side) (void)hipStreamDestroy(h->side);
   if (h->h_count) (void)hipHostFree(h->h_count);
   delete h;
 }
