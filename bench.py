@@ -10,7 +10,11 @@ Prints ONE JSON line:
   value            co-generated tokens / s over the whole job (prefill + decode)
   roofline         decode attention (the dominant kernel): algorithmic K/V
                    bytes per launch / its average launch time (HIP events on
-                   the library's stream over the timed region) vs 8 TB/s
+                   the stream each launch runs on, over the timed region, where
+                   the junior's forward overlaps the senior's) vs 8 TB/s
+  roofline_isolated the same kernel timed in an extra untimed rollout whose two
+                   forwards run one after the other (each launch alone on the
+                   GPU); the per-class breakdown comes from that rollout too
   cpu_baseline     the CPU oracle timed on a bounded sample of the same
                    workload on this host's cores
   decode_*         decode-only tokens/s and whole-decode-step HBM fraction
@@ -120,7 +124,8 @@ def main():
     ap.add_argument("--max-new", type=int, default=None, help="shorter rollouts (development only)")
     ap.add_argument("--cpu-steps", type=int, default=4, help="decode steps of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--breakdown", action="store_true", help="also time every kernel class (extra pass)")
+    ap.add_argument("--no-isolated", action="store_true",
+                    help="skip the extra rollout that times every kernel class with the forwards serialized")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -193,14 +198,25 @@ def main():
     pf = prefill_flops(wl, plens)
     pre_ms = float(np.mean(pre))
 
-    breakdown = None
-    if args.breakdown:
+    breakdown, iso = None, None
+    if not args.no_isolated:
+        from paper_2606_28166_amd import _lib as LIB
         eng.prefill(prompts, wl.group)
-        eng.timing(0b1111)
+        eng.timing(0b1111 | LIB.TIMING_SERIAL)
         for _ in range(L):
             eng.step()
-        breakdown = {k: {"ms": round(v[0], 3), "launches": v[1]} for k, v in eng.timing_read().items()}
+        tr = eng.timing_read()
         eng.timing(0)
+        breakdown = {k: {"ms": round(v[0], 3), "launches": v[1]} for k, v in tr.items()}
+        iso_ms, iso_n = tr["attention"]
+        iso_bytes = attention_bytes(wl, plens, L)
+        iso_gbs = iso_bytes / (iso_ms / 1e3) / 1e9
+        iso = {"bound": "hbm", "kernel": "decode attention (both models)", "achieved": round(iso_gbs, 1),
+               "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(iso_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+               "launches": iso_n, "avg_launch_us": round(iso_ms * 1e3 / max(iso_n, 1), 2),
+               "bytes_per_launch": int(iso_bytes / max(iso_n, 1)),
+               "method": "one extra rollout's decode steps, the two forwards serialized, all kernel classes timed"}
+        log(f"[bench] isolated rollout: attention {iso_ms:.1f} ms/{iso_n} launches -> {iso_gbs:.0f} GB/s")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -229,6 +245,7 @@ def main():
                      "frac": round(att_gbs / HBM_PEAK_GBS, 4), "traffic": None,
                      "launches": att_n, "avg_launch_us": round(att_ms * 1e3 / max(att_n, 1), 2),
                      "bytes_per_launch": int(att_bytes / max(att_n, 1))},
+        "roofline_isolated": iso,
         "cpu_baseline": cpu,
         "decode_tokens_per_s": round(n * L * args.steps / dec_s, 2),
         "decode_ms_per_token_step": round(sum(dec) / (L * args.steps), 4),

@@ -191,7 +191,9 @@ tandem_status tandem_get_state(tandem_handle* h, int32_t* owner, int32_t* c, int
 
 /* Instrumentation (the benchmark's roofline and the per-kernel breakdown).
  * class_mask bit k enables class k: the library then records a hipEvent pair
- * around every launch of that class on its stream; tandem_timing_read
+ * around every launch of that class on the stream it runs on (the junior's
+ * forward runs on a second stream joined back into the caller's, so its
+ * launches may overlap the senior's); tandem_timing_read
  * synchronises and returns the summed device milliseconds and the number of
  * launches of one class since the last tandem_timing_enable.  Every call to
  * tandem_timing_enable resets the sums (mask 0 switches timing off).  Each
@@ -201,6 +203,11 @@ enum { TANDEM_K_ATTENTION = 0,    /* decode / prompt attention            */
        TANDEM_K_SAMPLE = 2,       /* sampling, log-prob, handoff rule     */
        TANDEM_K_OTHER = 3,        /* norms, QKV post-processing, copies   */
        TANDEM_K_CLASSES = 4 };
+/* Flag for class_mask: while timing with this bit set, the senior's and the
+ * junior's forwards run one after the other instead of overlapping on two
+ * streams, so each timed launch has the GPU to itself.  Results are
+ * unchanged; only the schedule differs. */
+enum { TANDEM_TIMING_SERIAL = 1 << 8 };
 tandem_status tandem_timing_enable(tandem_handle* h, int32_t class_mask);
 tandem_status tandem_timing_read(tandem_handle* h, int32_t kernel_class, double* total_ms, int64_t* launches);
 

@@ -58,6 +58,7 @@ EXPORTS = ("tandem_workspace_size", "tandem_init", "tandem_prefill", "tandem_ste
            "tandem_step_forced", "tandem_get_state", "tandem_timing_enable", "tandem_timing_read",
            "tandem_last_error", "tandem_status_string", "tandem_destroy")
 K_ATTENTION, K_GEMM, K_SAMPLE, K_OTHER = 0, 1, 2, 3
+TIMING_SERIAL = 1 << 8          # timing flag: run the two forwards one after the other
 
 
 def _load():

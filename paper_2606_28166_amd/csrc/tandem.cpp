@@ -343,6 +343,13 @@ tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok,
 tandem_status forward_pair(tandem_handle* h, int R, const int32_t* row_tok, const int32_t* row_slot,
                            const int32_t* row_pos, const int32_t* row_done, bool lm_head) {
   hipStream_t st = h->stream;
+  if (h->timing & TANDEM_TIMING_SERIAL) {
+    for (int i = 0; i < 2; ++i) {
+      tandem_status s = forward(h, h->m[i], R, row_tok, row_slot, row_pos, row_done, lm_head, st);
+      if (s != TANDEM_OK) return s;
+    }
+    return TANDEM_OK;
+  }
   HIPCHK(hipEventRecord(h->ev_fork, st));
   HIPCHK(hipStreamWaitEvent(h->side, h->ev_fork, 0));
   tandem_status s = forward(h, h->m[1], R, row_tok, row_slot, row_pos, row_done, lm_head, h->side);
@@ -694,7 +701,7 @@ tandem_status tandem_timing_enable(tandem_handle* h, int32_t class_mask) {
   if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
   if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
   HIPCHK(hipStreamSynchronize(h->stream));
-  h->timing = class_mask & ((1 << TANDEM_K_CLASSES) - 1);
+  h->timing = class_mask & (((1 << TANDEM_K_CLASSES) - 1) | TANDEM_TIMING_SERIAL);
   h->ev_used = 0;
   for (auto& v : h->ev_marks) v.clear();
   return TANDEM_OK;
