@@ -6,9 +6,11 @@
 //     parts, then 8 bf16 low parts), so every weight fragment meets hi and lo
 //     in two MFMAs: fp32-level activations, bf16 weights, fp32 accumulation.
 //   * One workgroup computes a BM x 128 output tile (BM in {32, 64, 128})
-//     over its slice of K, 64 k-values per chunk; its 4 waves tile the 32 x 32
-//     MFMA blocks 2 x 2 (1 x 4 when BM = 32).  The 32 x 32 x 16 shape keeps
-//     the matrix cores near their peak with only a few accumulators per wave.
+//     over its slice of K, 64 k-values per chunk.  With BM = 128 its 8 waves
+//     (two per SIMD, so one issues MFMAs while the other waits on LDS) tile
+//     the 32 x 32 MFMA blocks 4 x 2; smaller tiles use 4 waves (2 x 2, or
+//     1 x 4 when BM = 32).  The 32 x 32 x 16 shape keeps the matrix cores
+//     near their peak with only a few accumulators per wave.
 //   * Weight rows and activation rows of each chunk stream into an NS-stage
 //     LDS ring with global_load_lds_dwordx4 (no register staging); 16-byte
 //     pieces are XOR-swizzled by row so the MFMA-layout reads spread over all
@@ -38,30 +40,32 @@ constexpr int BK = kGemmBK;        // k-values per chunk
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
 
-template <int BMT, int BNT, int NST> struct GemmShape {
+template <int BMT, int BNT, int NST, int NWT = 4> struct GemmShape {
+  static constexpr int NW = NWT;                      // waves per workgroup (4 or 8)
   static constexpr int BM = BMT;
   static constexpr int BN = BNT;                      // weight rows per tile (128 or 256)
   static constexpr int MB = BM / 32;                  // 32-row blocks
-  static constexpr int WM = MB >= 2 ? 2 : 1;          // waves along M
-  static constexpr int WN = 4 / WM;                   // waves along N
+  static constexpr int WM = NW == 8 ? (MB >= 4 ? 4 : MB) : (MB >= 2 ? 2 : 1);   // waves along M
+  static constexpr int WN = NW / WM;                  // waves along N
   static constexpr int MBW = MB / WM;                 // 32-row blocks per wave
   static constexpr int NBW = BN / 32 / WN;            // 32-column blocks per wave
   static constexpr int NS = NST;                      // ring stages
   static constexpr int ASTAGE = BM * BK * 4;          // bytes of one activation stage (hi + lo)
   static constexpr int WSTAGE = BN * BK * 2;          // bytes of one weight stage
   static constexpr int STAGE = ASTAGE + WSTAGE;
-  static constexpr int NA = BM / 16;                  // activation DMA instructions per wave per chunk
-  static constexpr int NWD = BN / 32;                 // weight DMA instructions per wave per chunk
+  static constexpr int NA = BM / (4 * NW);            // activation DMA instructions per wave per chunk
+  static constexpr int NWD = BN / (8 * NW);           // weight DMA instructions per wave per chunk
   static constexpr int WAIT = (NS - 2) * (NA + NWD);  // vmcnt that leaves NS - 2 chunks in flight
   static constexpr int OUT_COLS = BN / 2;             // SwiGLU output columns per tile
   static_assert(NS * STAGE <= 160 * 1024, "LDS ring exceeds 160 KB");
+  static_assert(NA >= 1 && NWD >= 1 && MBW >= 1 && NBW >= 1, "tile too small for the waves");
 };
 
-template <int BMT, int BNT, int NST, int EPI>
-__global__ __launch_bounds__(256) void gemm_mfma_kernel(
+template <int BMT, int BNT, int NST, int EPI, int NWT>
+__global__ __launch_bounds__(64 * NWT) void gemm_mfma_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, int M, int N, int K, int cps,
     float* __restrict__ out, int ldo, long split_stride) {
-  using G = GemmShape<BMT, BNT, NST>;
+  using G = GemmShape<BMT, BNT, NST, NWT>;
   __shared__ __attribute__((aligned(1024))) unsigned char ring[G::NS * G::STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -86,22 +90,22 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(
   };
 
   // DMA sources.  Weight stage: instruction i of wave w covers tile rows
-  // (BN/4) w + 8i .. +8 (128 B each); lane -> row (lane >> 3), physical piece
-  // lane & 7 holding logical piece (lane & 7) ^ ((row >> 1) & 7).
+  // (BN/NW) w + 8i .. +8 (128 B each); lane -> row (lane >> 3), physical
+  // piece lane & 7 holding logical piece (lane & 7) ^ ((row >> 1) & 7).
   const bf16_t* wsrc[G::NWD];
 #pragma unroll
   for (int i = 0; i < G::NWD; ++i) {
-    const int t = (G::BN / 4) * wave + 8 * i + (lane >> 3);
+    const int t = (G::BN / G::NW) * wave + 8 * i + (lane >> 3);
     const int lp = (lane & 7) ^ ((t >> 1) & 7);
     wsrc[i] = W + (size_t)wrow_of(t) * K + lp * 8;
   }
-  // Activation stage: instruction i of wave w covers tile rows 16i + 4w .. +4
+  // Activation stage: instruction i of wave w covers tile rows 4 (NW i + w) .. +4
   // (256 B each: 8 hi pieces and 8 lo pieces); physical piece lane & 15 holds
   // logical piece (lane & 15) ^ (row & 15).
   const bf16_t* asrc[G::NA];
 #pragma unroll
   for (int i = 0; i < G::NA; ++i) {
-    const int r = 16 * i + 4 * wave + (lane >> 4);
+    const int r = 4 * (G::NW * i + wave) + (lane >> 4);
     const int lc = (lane & 15) ^ (r & 15);
     asrc[i] = A + (size_t)min(m0 + r, M - 1) * 2 * (size_t)K + lc * 8;
   }
@@ -110,10 +114,10 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(
     const int c = kc0 + min(it, nloc - 1);
     unsigned char* st = ring0 + (it % G::NS) * G::STAGE;
 #pragma unroll
-    for (int i = 0; i < G::NA; ++i) load_lds16(asrc[i] + (size_t)c * 2 * BK, st + (16 * i + 4 * wave) * 256);
+    for (int i = 0; i < G::NA; ++i) load_lds16(asrc[i] + (size_t)c * 2 * BK, st + 4 * (G::NW * i + wave) * 256);
 #pragma unroll
     for (int i = 0; i < G::NWD; ++i)
-      load_lds16_nt(wsrc[i] + (size_t)c * BK, st + G::ASTAGE + ((G::BN / 4) * wave + 8 * i) * 128);
+      load_lds16_nt(wsrc[i] + (size_t)c * BK, st + G::ASTAGE + ((G::BN / G::NW) * wave + 8 * i) * 128);
   };
 
   f32x16_t acc[G::MBW][G::NBW];
@@ -276,26 +280,20 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(
 
 template <int BMT, int BNT, int NST, int EPI>
 hipError_t run_mfma(const GemmArgs& a, int S, int cps, hipStream_t st) {
-  using G = GemmShape<BMT, BNT, NST>;
+  constexpr int NW = (BMT == 128) ? 8 : 4;    // 128-row tiles: two waves per SIMD
+  using G = GemmShape<BMT, BNT, NST, NW>;
   const int cols = (EPI == EPI_SWIGLU) ? G::OUT_COLS : G::BN;
   dim3 grid((a.N + cols - 1) / cols, (a.M + BMT - 1) / BMT, S);
-  hipLaunchKernelGGL((gemm_mfma_kernel<BMT, BNT, NST, EPI>), grid, dim3(256), 0, st, (const bf16_t*)a.A,
+  hipLaunchKernelGGL((gemm_mfma_kernel<BMT, BNT, NST, EPI, NW>), grid, dim3(64 * NW), 0, st, (const bf16_t*)a.A,
                      (const bf16_t*)a.W, a.M, a.N, a.K, cps, a.out, a.ldo, a.split_stride);
   return hipGetLastError();
 }
 
-#ifndef TANDEM_GEMM_BN
-#define TANDEM_GEMM_BN 128
-#endif
-#ifndef TANDEM_GEMM_NS128
-#define TANDEM_GEMM_NS128 3
-#endif
 template <int EPI>
 hipError_t dispatch_mfma(const GemmArgs& a, int S, int cps, hipStream_t st) {
-  constexpr int BNT = TANDEM_GEMM_BN;
-  if (a.M <= 32) return run_mfma<32, BNT, (BNT == 128 ? 4 : 3), EPI>(a, S, cps, st);
-  if (a.M <= 64) return run_mfma<64, BNT, (BNT == 128 ? 4 : 2), EPI>(a, S, cps, st);
-  return run_mfma<128, BNT, (BNT == 128 ? TANDEM_GEMM_NS128 : 2), EPI>(a, S, cps, st);
+  if (a.M <= 32) return run_mfma<32, 128, 4, EPI>(a, S, cps, st);
+  if (a.M <= 64) return run_mfma<64, 128, 4, EPI>(a, S, cps, st);
+  return run_mfma<128, 128, 3, EPI>(a, S, cps, st);
 }
 
 template <typename WT, bool SPLIT>

@@ -9,7 +9,7 @@ namespace tandem {
 namespace {
 
 constexpr int kNT = 256;
-constexpr int kSplitMaxDev = 8;    // split-K slices a consumer sums (>= the host's cap)
+constexpr int kSplitMaxDev = 16;   // split-K slices a consumer sums (>= the host's cap)
 
 // ------------------------------------------------------------------ norms
 // One workgroup per row; each thread owns float4 groups of the row.  All
@@ -97,11 +97,50 @@ __global__ __launch_bounds__(kNT) void resid_norm_kernel(const float* __restrict
   }
 }
 
+// ------------------------------------------------------------ SwiGLU finish
+// One thread per 8 consecutive outputs of a row (one split-format piece).
+__global__ __launch_bounds__(kNT) void swiglu_finish_kernel(const float* __restrict__ ws, int S, long ws_stride,
+                                                            int M, int ffn, bf16_t* __restrict__ out) {
+  const long e = (long)blockIdx.x * kNT + threadIdx.x;
+  const int np = ffn / 8;
+  if (e >= (long)M * np) return;
+  const int m = (int)(e / np), p = (int)(e % np);
+  float g[8], u[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) g[i] = u[i] = 0.f;
+  const float* row = ws + (size_t)m * 2 * ffn + 8 * p;
+#pragma unroll
+  for (int s = 0; s < kSplitMaxDev; ++s)
+    if (s < S) {
+      const float4* gp = reinterpret_cast<const float4*>(row + s * ws_stride);
+      const float4* up = reinterpret_cast<const float4*>(row + s * ws_stride + ffn);
+      const float4 g0 = gp[0], g1 = gp[1], u0 = up[0], u1 = up[1];
+      g[0] += g0.x; g[1] += g0.y; g[2] += g0.z; g[3] += g0.w;
+      g[4] += g1.x; g[5] += g1.y; g[6] += g1.z; g[7] += g1.w;
+      u[0] += u0.x; u[1] += u0.y; u[2] += u0.z; u[3] += u0.w;
+      u[4] += u1.x; u[5] += u1.y; u[6] += u1.z; u[7] += u1.w;
+    }
+  uint32_t hw[4], lw[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float y0 = g[2 * i] / (1.f + expf(-g[2 * i])) * u[2 * i];
+    const float y1 = g[2 * i + 1] / (1.f + expf(-g[2 * i + 1])) * u[2 * i + 1];
+    const bf16_t h0 = f2bf(y0), h1 = f2bf(y1);
+    hw[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    lw[i] = (uint32_t)f2bf(y0 - bf2f(h0)) | ((uint32_t)f2bf(y1 - bf2f(h1)) << 16);
+  }
+  uint4* o = reinterpret_cast<uint4*>(out + (size_t)m * 2 * ffn + 16 * p);
+  o[0] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+  o[1] = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+}
+
+
 // ------------------------------------------------------------ qkv post
-// One workgroup per row.  Sums the split-K partials, applies the optional
-// per-head q/k RMSNorm and NeoX rotary embedding (lane i rotates the pair
-// (i, i + hd/2)), writes q, and appends k and v at the row's (slot, pos) of
-// the tiled cache.
+// One wave per head of one row (q heads, then k heads, then v heads; four
+// heads per workgroup).  Sums the head's split-K partials, applies the
+// optional per-head q/k RMSNorm and the NeoX rotary embedding (lane i
+// rotates the pair (i, i + hd/2)), writes q, and appends k and v at the
+// row's (slot, pos) of the tiled cache.
 template <typename KT>
 __global__ __launch_bounds__(kNT) void qkv_post_kernel(
     const float* __restrict__ ws, int S, long ws_stride, int nq, int nkv, int hd,
@@ -109,62 +148,62 @@ __global__ __launch_bounds__(kNT) void qkv_post_kernel(
     const float2* __restrict__ rope, const int32_t* __restrict__ row_slot,
     const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
     float* __restrict__ q_out, KT* __restrict__ kc, KT* __restrict__ vc, int ctx_stride, long slot_stride) {
-  extern __shared__ float buf[];
-  const int r = blockIdx.x, tid = threadIdx.x;
+  const int r = blockIdx.x, lane = threadIdx.x & 63;
+  const int nh = nq + 2 * nkv;
+  const int head = blockIdx.y * (kNT / 64) + (threadIdx.x >> 6);
+  if (head >= nh) return;
   if (row_done && row_done[r]) return;
-  const int dim = (nq + 2 * nkv) * hd;
-  const size_t rbase = (size_t)r * dim;
-  for (int i4 = tid; i4 < dim / 4; i4 += kNT) {
-    float4 p[kSplitMaxDev];
-#pragma unroll
-    for (int s = 0; s < kSplitMaxDev; ++s)
-      if (s < S) p[s] = reinterpret_cast<const float4*>(ws + s * ws_stride + rbase)[i4];
-    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-    for (int s = 0; s < kSplitMaxDev; ++s)
-      if (s < S) { a.x += p[s].x; a.y += p[s].y; a.z += p[s].z; a.w += p[s].w; }
-    reinterpret_cast<float4*>(buf)[i4] = a;
-  }
-  __syncthreads();
-  const int slot = row_slot[r], pos = row_pos[r];
   const int half = hd / 2;
-  const int lane = tid & 63, wave = tid >> 6;
-  for (int head = wave; head < nq + nkv; head += kNT / 64) {
-    const bool isq = head < nq;
-    const float* src = buf + head * hd;
-    float x1 = 0.f, x2 = 0.f;
-    if (lane < half) {
-      x1 = src[lane];
-      x2 = src[lane + half];
-    }
-    const float* gn = isq ? q_norm : k_norm;
-    if (gn) {
-      const float ss = wave_sum(x1 * x1 + x2 * x2);
-      const float rs = 1.f / sqrtf(ss / (float)hd + eps);
-      if (lane < half) {
-        x1 *= rs * gn[lane];
-        x2 *= rs * gn[lane + half];
+  const bool act = lane < half;
+  const size_t base = ((size_t)r * nh + head) * hd;
+  float x1 = 0.f, x2 = 0.f;
+  if (act) {
+    float a1[kSplitMaxDev], a2[kSplitMaxDev];
+#pragma unroll
+    for (int s = 0; s < kSplitMaxDev; ++s)
+      if (s < S) {
+        a1[s] = ws[s * ws_stride + base + lane];
+        a2[s] = ws[s * ws_stride + base + lane + half];
       }
-    }
-    if (lane < half) {
-      const float2 cs = rope[(size_t)pos * half + lane];
-      const float y1 = x1 * cs.x - x2 * cs.y;
-      const float y2 = x2 * cs.x + x1 * cs.y;
-      if (isq) {
-        float* qo = q_out + ((size_t)r * nq + head) * hd;
-        qo[lane] = y1;
-        qo[lane + half] = y2;
-      } else {
-        KT* ko = kc + (size_t)slot * slot_stride + (size_t)(head - nq) * ctx_stride * hd;
-        st(ko + kv_k_index(pos, lane, hd), y1);
-        st(ko + kv_k_index(pos, lane + half, hd), y2);
+#pragma unroll
+    for (int s = 0; s < kSplitMaxDev; ++s)
+      if (s < S) {
+        x1 += a1[s];
+        x2 += a2[s];
       }
+  }
+  const int slot = row_slot[r], pos = row_pos[r];
+  if (head >= nq + nkv) {                      // v head: stored as is
+    KT* vo = vc + (size_t)slot * slot_stride + (size_t)(head - nq - nkv) * ctx_stride * hd;
+    if (act) {
+      st(vo + kv_v_index(pos, lane, hd), x1);
+      st(vo + kv_v_index(pos, lane + half, hd), x2);
+    }
+    return;
+  }
+  const bool isq = head < nq;
+  const float* gn = isq ? q_norm : k_norm;
+  if (gn) {
+    const float ss = wave_sum(x1 * x1 + x2 * x2);
+    const float rs = 1.f / sqrtf(ss / (float)hd + eps);
+    if (act) {
+      x1 *= rs * gn[lane];
+      x2 *= rs * gn[lane + half];
     }
   }
-  for (int e = tid; e < nkv * hd; e += kNT) {
-    const int kh = e / hd, d = e % hd;
-    KT* vo = vc + (size_t)slot * slot_stride + (size_t)kh * ctx_stride * hd;
-    st(vo + kv_v_index(pos, d, hd), buf[(nq + nkv) * hd + e]);
+  if (act) {
+    const float2 cs = rope[(size_t)pos * half + lane];
+    const float y1 = x1 * cs.x - x2 * cs.y;
+    const float y2 = x2 * cs.x + x1 * cs.y;
+    if (isq) {
+      float* qo = q_out + ((size_t)r * nq + head) * hd;
+      qo[lane] = y1;
+      qo[lane + half] = y2;
+    } else {
+      KT* ko = kc + (size_t)slot * slot_stride + (size_t)(head - nq) * ctx_stride * hd;
+      st(ko + kv_k_index(pos, lane, hd), y1);
+      st(ko + kv_k_index(pos, lane + half, hd), y2);
+    }
   }
 }
 
@@ -383,6 +422,15 @@ hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, c
   return hipGetLastError();
 }
 
+hipError_t launch_swiglu_finish(const float* ws, int S, long ws_stride, int M, int ffn, void* out, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (S > kSplitMaxDev || ffn % 8) return hipErrorInvalidValue;
+  const long n = (long)M * (ffn / 8);
+  hipLaunchKernelGGL(swiglu_finish_kernel, dim3((unsigned)((n + kNT - 1) / kNT)), dim3(kNT), 0, st, ws, S, ws_stride,
+                     M, ffn, (bf16_t*)out);
+  return hipGetLastError();
+}
+
 hipError_t launch_resid_norm(int dt, const float* ws, int S, long ws_stride, float* h, const float* gain,
                              float eps, void* x, int R, int d, hipStream_t st) {
   if (R <= 0) return hipSuccess;
@@ -396,15 +444,15 @@ hipError_t launch_resid_norm(int dt, const float* ws, int S, long ws_stride, flo
 
 hipError_t launch_qkv_post(const QkvPostArgs& a, hipStream_t st) {
   if (a.R <= 0) return hipSuccess;
-  if (a.S > kSplitMaxDev) return hipErrorInvalidValue;
-  const size_t shm = sizeof(float) * (size_t)(a.nq + 2 * a.nkv) * a.hd;
+  if (a.S > kSplitMaxDev || a.hd > 128) return hipErrorInvalidValue;
+  const dim3 grid(a.R, (a.nq + 2 * a.nkv + kNT / 64 - 1) / (kNT / 64));
   if (a.dt == DT_BF16)
-    hipLaunchKernelGGL((qkv_post_kernel<bf16_t>), dim3(a.R), dim3(kNT), shm, st, a.ws, a.S, a.ws_stride,
+    hipLaunchKernelGGL((qkv_post_kernel<bf16_t>), grid, dim3(kNT), 0, st, a.ws, a.S, a.ws_stride,
                        a.nq, a.nkv, a.hd, a.q_norm, a.k_norm, a.eps, a.rope, a.row_slot, a.row_pos,
                        a.row_done, a.q_out, (bf16_t*)a.cache.k, (bf16_t*)a.cache.v,
                        a.cache.ctx_stride, a.cache.slot_stride);
   else
-    hipLaunchKernelGGL((qkv_post_kernel<float>), dim3(a.R), dim3(kNT), shm, st, a.ws, a.S, a.ws_stride,
+    hipLaunchKernelGGL((qkv_post_kernel<float>), grid, dim3(kNT), 0, st, a.ws, a.S, a.ws_stride,
                        a.nq, a.nkv, a.hd, a.q_norm, a.k_norm, a.eps, a.rope, a.row_slot, a.row_pos,
                        a.row_done, a.q_out, (float*)a.cache.k, (float*)a.cache.v,
                        a.cache.ctx_stride, a.cache.slot_stride);

@@ -40,6 +40,11 @@ hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, c
                              float eps, float* h, void* x, int R, hipStream_t st);
 
 // h[r] += sum_s ws[s][r] (fixed order), then x[r] = rmsnorm(h[r]) * gain.
+// SwiGLU of split-K gate/up partials: ws[s][m][0 .. ffn) are gate sums,
+// ws[s][m][ffn .. 2 ffn) the matching up sums; out[m] = silu(gate) * up in
+// split format (row stride 2 * ffn bf16).  ffn % 8 == 0.
+hipError_t launch_swiglu_finish(const float* ws, int S, long ws_stride, int M, int ffn, void* out, hipStream_t st);
+
 hipError_t launch_resid_norm(int dt, const float* ws, int S, long ws_stride, float* h,
                              const float* gain, float eps, void* x, int R, int d, hipStream_t st);
 

@@ -26,8 +26,7 @@ namespace {
 
 thread_local std::string g_err = "no error";
 
-constexpr int kSplitMax = 8;          // split-K slices of a decode projection
-constexpr int kTargetGroups = 512;    // workgroups a projection launch aims for
+constexpr int kSplitMax = 16;         // split-K slices of a decode projection
 constexpr int kVocabChunk = 4096;     // vocabulary entries per sampling workgroup
 constexpr size_t kAlign = 256;
 
@@ -130,6 +129,13 @@ tandem_status check_cap(const tandem_capacity* cap, std::string* err) {
   return TANDEM_OK;
 }
 
+// Narrow FFNs give the fused gate/up + SwiGLU GEMM too few output tiles to
+// fill the device: those run as a split-K GEMM over the 2 ffn gate and up
+// rows plus a SwiGLU pass over the summed partials.
+bool split_gate_up(const tandem_model_cfg* c) {
+  return c->weight_dtype == TANDEM_BF16 && c->d_model % 64 == 0 && c->ffn_dim < 8192;
+}
+
 Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const tandem_capacity* cap) {
   Plan P{};
   P.ctx_stride = (int)align_up((size_t)cap->max_ctx, 64);
@@ -143,7 +149,8 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
     m.qkv_dim = (c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim;
     m.att_dim = c->n_q_heads * c->head_dim;
     m.rmax = cap->max_seqs > cap->max_prefill_tokens ? cap->max_seqs : cap->max_prefill_tokens;
-    const size_t nmax = (size_t)(m.qkv_dim > c->d_model ? m.qkv_dim : c->d_model);
+    size_t nmax = (size_t)(m.qkv_dim > c->d_model ? m.qkv_dim : c->d_model);
+    if (split_gate_up(c) && (size_t)2 * c->ffn_dim > nmax) nmax = (size_t)2 * c->ffn_dim;
     const size_t rows_ws = (size_t)kSplitMax * cap->max_seqs > (size_t)cap->max_prefill_tokens
                                ? (size_t)kSplitMax * cap->max_seqs
                                : (size_t)cap->max_prefill_tokens;
@@ -189,6 +196,7 @@ struct tandem_handle {
   // runs on a second stream forked from and joined back into `stream`.
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  int n_cu = 256;             // compute units of the device (split-K sizing)
   int32_t *owner, *c, *t, *pos, *pending, *done;
   int32_t* seq_slot;
   int32_t *row_slot, *row_pos, *row_tok, *row_src;
@@ -253,15 +261,16 @@ hipError_t tim_end(tandem_handle* h, size_t idx, hipStream_t st) {
 
 namespace {
 
-int choose_splits(int M, int N, int K, size_t ws_floats) {
+// Split-K slices of one projection: as many as keep (tiles x slices) within
+// one workgroup per compute unit (more slices than that leave a straggling
+// second round), at most kSplitMax, one 64-wide k chunk each at least, and
+// what the partial-sum workspace holds.
+int choose_splits(int M, int N, int K, size_t ws_floats, int n_cu) {
   const int m_tiles = (M + 127) / 128, n_tiles = (N + 127) / 128;
   const int base = m_tiles * n_tiles;
-  int S = (kTargetGroups + base - 1) / base;
-  // keep the partial-sum traffic (S * M * N * 4 bytes, written and read back)
-  // below half the weight bytes (N * K * 2)
-  const int traffic_cap = K / (4 * (M > 0 ? M : 1));
-  if (S > traffic_cap) S = traffic_cap;
+  int S = n_cu / base;
   if (S > kSplitMax) S = kSplitMax;
+  if (S > K / 64) S = K / 64;
   const size_t cap_ws = ws_floats / ((size_t)M * N);
   if ((size_t)S > cap_ws) S = (int)cap_ws;
   if (S < 1) S = 1;
@@ -290,7 +299,7 @@ tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok,
     g.dt = dt;
     g.A = m.xa; g.W = L.w_qkv; g.M = R; g.N = qkv; g.K = d; g.epi = EPI_PARTIAL;
     g.out = m.ws; g.ldo = qkv; g.split_stride = (long)R * qkv;
-    g.splits = choose_splits(R, qkv, d, m.p.ws_floats);
+    g.splits = choose_splits(R, qkv, d, m.p.ws_floats, h->n_cu);
     int S = 1;
     TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
 
@@ -311,19 +320,27 @@ tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok,
     g = GemmArgs{};
     g.dt = dt; g.A = m.xa; g.W = L.w_o; g.M = R; g.N = d; g.K = att; g.epi = EPI_PARTIAL;
     g.out = m.ws; g.ldo = d; g.split_stride = (long)R * d;
-    g.splits = choose_splits(R, d, att, m.p.ws_floats);
+    g.splits = choose_splits(R, d, att, m.p.ws_floats, h->n_cu);
     TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
     TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, L.ffn_norm, c.rms_eps, m.xa, R, d, st));
 
     g = GemmArgs{};
-    g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = R; g.N = c.ffn_dim; g.K = d; g.epi = EPI_SWIGLU;
-    g.out = (float*)m.xf; g.ldo = c.ffn_dim; g.splits = 1;
-    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+    if (split_gate_up(&c)) {
+      g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = R; g.N = 2 * c.ffn_dim; g.K = d; g.epi = EPI_PARTIAL;
+      g.out = m.ws; g.ldo = 2 * c.ffn_dim; g.split_stride = (long)R * 2 * c.ffn_dim;
+      g.splits = choose_splits(R, 2 * c.ffn_dim, d, m.p.ws_floats, h->n_cu);
+      TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+      TIMED(TANDEM_K_OTHER, launch_swiglu_finish(m.ws, S, (long)R * 2 * c.ffn_dim, R, c.ffn_dim, m.xf, st));
+    } else {
+      g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = R; g.N = c.ffn_dim; g.K = d; g.epi = EPI_SWIGLU;
+      g.out = (float*)m.xf; g.ldo = c.ffn_dim; g.splits = 1;
+      TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+    }
 
     g = GemmArgs{};
     g.dt = dt; g.A = m.xf; g.W = L.w_down; g.M = R; g.N = d; g.K = c.ffn_dim; g.epi = EPI_PARTIAL;
     g.out = m.ws; g.ldo = d; g.split_stride = (long)R * d;
-    g.splits = choose_splits(R, d, c.ffn_dim, m.p.ws_floats);
+    g.splits = choose_splits(R, d, c.ffn_dim, m.p.ws_floats, h->n_cu);
     TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
     const float* next_gain = (l + 1 < c.n_layers) ? m.layers[l + 1].attn_norm : m.final_norm;
     TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, next_gain, c.rms_eps, m.xa, R, d, st));
@@ -559,6 +576,14 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   };
   hipError_t e = hipHostMalloc((void**)&h->h_count, 4, hipHostMallocDefault);
   if (e != hipSuccess) { h->h_count = nullptr; return bail(e, "hipHostMalloc"); }
+  {
+    int dev = 0, ncu = 0;
+    e = hipGetDevice(&dev);
+    if (e != hipSuccess) return bail(e, "hipGetDevice");
+    e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return bail(e, "compute unit count");
+    if (ncu > 0) h->n_cu = ncu;
+  }
   e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
   if (e != hipSuccess) { h->side = nullptr; return bail(e, "side stream"); }
   e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
