@@ -9,12 +9,15 @@ prefill of both models on every prompt, then max_new tandem decode steps
 Prints ONE JSON line:
   value            co-generated tokens / s over the whole job (prefill + decode)
   roofline         decode attention (the dominant kernel): algorithmic K/V
-                   bytes per launch / its average launch time (HIP events on
-                   the stream each launch runs on, over the timed region, where
-                   the junior's forward overlaps the senior's) vs 8 TB/s
-  roofline_isolated the same kernel timed in an extra untimed rollout whose two
-                   forwards run one after the other (each launch alone on the
-                   GPU); the per-class breakdown comes from that rollout too
+                   bytes per launch / its average launch time, from HIP event
+                   pairs around every launch (on the stream it runs on) in an
+                   extra rollout whose two forwards run one after the other, so
+                   each launch has the GPU to itself; the per-class breakdown
+                   comes from the same rollout
+  roofline_concurrent the same in the two-stream schedule of the timed region
+                   (the junior's forward overlapping the senior's)
+  (the timed region replays the captured step graph; graph-captured event
+   records carry no launch times, so both roofline rollouts launch from the host)
   cpu_baseline     the CPU oracle timed on a bounded sample of the same
                    workload on this host's cores
   decode_*         decode-only tokens/s and whole-decode-step HBM fraction
@@ -153,36 +156,36 @@ def main():
     L = wl.sample.max_new
     n = wl.n_seqs
 
-    def rollout_once(timed_attention=False):
+    from paper_2606_28166_amd import _lib as LIB
+
+    def rollout_once(timing=0):
+        """Prefill + L decode steps; timing = the library's class mask (0: step-graph replays)."""
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
         ev[0].record(stream)
         eng.prefill(prompts, wl.group)
         ev[1].record(stream)
-        if timed_attention:
-            eng.timing(1 << 0)
+        eng.timing(timing)
         for _ in range(L):
             eng.step()
         ev[2].record(stream)
         torch.cuda.synchronize()
-        att = eng.timing_read()["attention"] if timed_attention else None
-        if timed_attention:
-            eng.timing(0)
-        return ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), att
+        tr = eng.timing_read() if timing & 0b1111 else None
+        eng.timing(0)
+        return ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), tr
 
     for i in range(args.warmup):
         p_ms, d_ms, _ = rollout_once()
         log(f"[bench] warmup {i}: prefill {p_ms:.1f} ms, decode {d_ms:.1f} ms")
 
+    # ---- timed region: whole rollouts, decode steps replayed from the step graph
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    pre, dec, att_ms, att_n = [], [], 0.0, 0
+    pre, dec = [], []
     for i in range(args.steps):
-        p_ms, d_ms, att = rollout_once(timed_attention=True)
+        p_ms, d_ms, _ = rollout_once()
         pre.append(p_ms)
         dec.append(d_ms)
-        att_ms += att[0]
-        att_n += att[1]
-        log(f"[bench] step {i}: prefill {p_ms:.1f} ms, decode {d_ms:.1f} ms, attention {att[0]:.1f} ms/{att[1]} launches")
+        log(f"[bench] step {i}: prefill {p_ms:.1f} ms, decode {d_ms:.1f} ms")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
 
@@ -193,30 +196,36 @@ def main():
     value = toks / wall
     dec_s = sum(dec) / 1e3
     dec_bytes = sum(decode_step_bytes(wl, plens, t) for t in range(1, L + 1)) * args.steps
-    att_bytes = attention_bytes(wl, plens, L) * args.steps
-    att_gbs = att_bytes / (att_ms / 1e3) / 1e9
     pf = prefill_flops(wl, plens)
     pre_ms = float(np.mean(pre))
 
-    breakdown, iso = None, None
+    # ---- the dominant kernel's roofline.  Event records captured into a HIP
+    # graph carry no launch times, so the attention launches are timed in extra
+    # rollouts whose steps are launched from the host, with a HIP event pair
+    # around every launch on the stream it runs on: one with the two forwards
+    # serialized (each launch alone on the GPU: the kernel's own roofline, and
+    # the per-class breakdown), one in the production two-stream schedule.
+    def roofline_of(att, method):
+        ms, nl = att
+        nbytes = attention_bytes(wl, plens, L)
+        gbs = nbytes / (ms / 1e3) / 1e9
+        return {"bound": "hbm", "kernel": "decode attention (both models)", "achieved": round(gbs, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "launches": nl, "avg_launch_us": round(ms * 1e3 / max(nl, 1), 2),
+                "bytes_per_launch": int(nbytes / max(nl, 1)), "method": method}
+
+    roof, roof_conc, breakdown = None, None, None
     if not args.no_isolated:
-        from paper_2606_28166_amd import _lib as LIB
-        eng.prefill(prompts, wl.group)
-        eng.timing(0b1111 | LIB.TIMING_SERIAL)
-        for _ in range(L):
-            eng.step()
-        tr = eng.timing_read()
-        eng.timing(0)
+        _, d_ser, tr = rollout_once(0b1111 | LIB.TIMING_SERIAL)
         breakdown = {k: {"ms": round(v[0], 3), "launches": v[1]} for k, v in tr.items()}
-        iso_ms, iso_n = tr["attention"]
-        iso_bytes = attention_bytes(wl, plens, L)
-        iso_gbs = iso_bytes / (iso_ms / 1e3) / 1e9
-        iso = {"bound": "hbm", "kernel": "decode attention (both models)", "achieved": round(iso_gbs, 1),
-               "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(iso_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-               "launches": iso_n, "avg_launch_us": round(iso_ms * 1e3 / max(iso_n, 1), 2),
-               "bytes_per_launch": int(iso_bytes / max(iso_n, 1)),
-               "method": "one extra rollout's decode steps, the two forwards serialized, all kernel classes timed"}
-        log(f"[bench] isolated rollout: attention {iso_ms:.1f} ms/{iso_n} launches -> {iso_gbs:.0f} GB/s")
+        roof = roofline_of(tr["attention"], "one rollout's decode steps, the two forwards serialized and launched "
+                                            "from the host, a HIP event pair around every launch")
+        log(f"[bench] serialized rollout: decode {d_ser:.1f} ms, attention {tr['attention'][0]:.1f} ms / "
+            f"{tr['attention'][1]} launches -> {roof['achieved']:.0f} GB/s")
+        _, d_con, tr = rollout_once(1 << LIB.K_ATTENTION)
+        roof_conc = roofline_of(tr["attention"], "one rollout's decode steps in the two-stream schedule, launched "
+                                                 "from the host, a HIP event pair around every attention launch")
+        log(f"[bench] concurrent instrumented rollout: decode {d_con:.1f} ms, attention -> {roof_conc['achieved']:.0f} GB/s")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -240,12 +249,8 @@ def main():
         "config": {"workload": DESCRIPTIONS[wl.name], "name": wl.name, "rows": n, "prompt_len": plens[0],
                    "max_new": L, "senior_layers": wl.senior.n_layers, "junior_layers": wl.junior.n_layers,
                    "vocab": wl.senior.vocab},
-        "roofline": {"bound": "hbm", "kernel": "decode attention (both models)",
-                     "achieved": round(att_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(att_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                     "launches": att_n, "avg_launch_us": round(att_ms * 1e3 / max(att_n, 1), 2),
-                     "bytes_per_launch": int(att_bytes / max(att_n, 1))},
-        "roofline_isolated": iso,
+        "roofline": roof,
+        "roofline_concurrent": roof_conc,
         "cpu_baseline": cpu,
         "decode_tokens_per_s": round(n * L * args.steps / dec_s, 2),
         "decode_ms_per_token_step": round(sum(dec) / (L * args.steps), 4),

@@ -173,7 +173,12 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens,
  * token through both models (appending to both caches), sample y_t from the
  * owner, write (y_t, m_t, senior log-prob) to the output arenas, stop at EOS
  * or at t = max_new_tokens, apply the handoff rule.  If n_active is not NULL
- * the call synchronises and stores the number of unfinished sequences. */
+ * the call synchronises and stores the number of unfinished sequences.
+ * The step's kernels are captured once per batch into a HIP graph (on the
+ * first tandem_step after tandem_prefill, or after a timing-mode change)
+ * and every step replays it: the per-step state lives in device memory, so
+ * the same graph serves every step.  Capture allocates host-side graph
+ * objects and events owned by the handle. */
 tandem_status tandem_step(tandem_handle* h, int32_t* n_active);
 
 /* As tandem_step, but the appended token of sequence s is forced[s] (device
@@ -197,17 +202,22 @@ tandem_status tandem_get_state(tandem_handle* h, int32_t* owner, int32_t* c, int
  * synchronises and returns the summed device milliseconds and the number of
  * launches of one class since the last tandem_timing_enable.  Every call to
  * tandem_timing_enable resets the sums (mask 0 switches timing off).  Each
- * event pair adds a few microseconds of stream time. */
+ * event pair adds a few microseconds of stream time.  While any class is
+ * timed, tandem_step launches its kernels from the host instead of replaying
+ * the step graph (event records inside a graph carry no launch times). */
 enum { TANDEM_K_ATTENTION = 0,    /* decode / prompt attention            */
        TANDEM_K_GEMM = 1,         /* projection and LM-head GEMMs         */
        TANDEM_K_SAMPLE = 2,       /* sampling, log-prob, handoff rule     */
        TANDEM_K_OTHER = 3,        /* norms, QKV post-processing, copies   */
        TANDEM_K_CLASSES = 4 };
-/* Flag for class_mask: while timing with this bit set, the senior's and the
- * junior's forwards run one after the other instead of overlapping on two
- * streams, so each timed launch has the GPU to itself.  Results are
- * unchanged; only the schedule differs. */
-enum { TANDEM_TIMING_SERIAL = 1 << 8 };
+/* Flags for class_mask (they also apply with no class bit set):
+ *   TANDEM_TIMING_SERIAL  the senior's and the junior's forwards run one after
+ *                         the other instead of overlapping on two streams, so
+ *                         each timed launch has the GPU to itself;
+ *   TANDEM_TIMING_EAGER   tandem_step launches every kernel from the host
+ *                         instead of replaying its captured HIP graph.
+ * Results are unchanged; only the schedule differs. */
+enum { TANDEM_TIMING_SERIAL = 1 << 8, TANDEM_TIMING_EAGER = 1 << 9 };
 tandem_status tandem_timing_enable(tandem_handle* h, int32_t class_mask);
 tandem_status tandem_timing_read(tandem_handle* h, int32_t kernel_class, double* total_ms, int64_t* launches);
 

@@ -59,6 +59,7 @@ EXPORTS = ("tandem_workspace_size", "tandem_init", "tandem_prefill", "tandem_ste
            "tandem_last_error", "tandem_status_string", "tandem_destroy")
 K_ATTENTION, K_GEMM, K_SAMPLE, K_OTHER = 0, 1, 2, 3
 TIMING_SERIAL = 1 << 8          # timing flag: run the two forwards one after the other
+TIMING_EAGER = 1 << 9           # timing flag: launch every kernel from the host (no step graph)
 
 
 def _load():

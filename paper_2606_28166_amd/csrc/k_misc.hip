@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kNT) void resid_norm_kernel(const float* __restrict
 // ------------------------------------------------------------ SwiGLU finish
 // One thread per 8 consecutive outputs of a row (one split-format piece).
 __global__ __launch_bounds__(kNT) void swiglu_finish_kernel(const float* __restrict__ ws, int S, long ws_stride,
-                                                            int M, int ffn, bf16_t* __restrict__ out) {
+                                                            int M, int ffn, int interleaved, bf16_t* __restrict__ out) {
   const long e = (long)blockIdx.x * kNT + threadIdx.x;
   const int np = ffn / 8;
   if (e >= (long)M * np) return;
@@ -108,12 +108,15 @@ __global__ __launch_bounds__(kNT) void swiglu_finish_kernel(const float* __restr
   float g[8], u[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) g[i] = u[i] = 0.f;
-  const float* row = ws + (size_t)m * 2 * ffn + 8 * p;
+  // gate and up columns of outputs 8 p .. 8 p + 7
+  const int gcol = interleaved ? 32 * (p >> 1) + 8 * (p & 1) : 8 * p;
+  const int ucol = interleaved ? gcol + 16 : 8 * p + ffn;
+  const float* row = ws + (size_t)m * 2 * ffn;
 #pragma unroll
   for (int s = 0; s < kSplitMaxDev; ++s)
     if (s < S) {
-      const float4* gp = reinterpret_cast<const float4*>(row + s * ws_stride);
-      const float4* up = reinterpret_cast<const float4*>(row + s * ws_stride + ffn);
+      const float4* gp = reinterpret_cast<const float4*>(row + s * ws_stride + gcol);
+      const float4* up = reinterpret_cast<const float4*>(row + s * ws_stride + ucol);
       const float4 g0 = gp[0], g1 = gp[1], u0 = up[0], u1 = up[1];
       g[0] += g0.x; g[1] += g0.y; g[2] += g0.z; g[3] += g0.w;
       g[4] += g1.x; g[5] += g1.y; g[6] += g1.z; g[7] += g1.w;
@@ -422,12 +425,13 @@ hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, c
   return hipGetLastError();
 }
 
-hipError_t launch_swiglu_finish(const float* ws, int S, long ws_stride, int M, int ffn, void* out, hipStream_t st) {
+hipError_t launch_swiglu_finish(const float* ws, int S, long ws_stride, int M, int ffn, bool interleaved, void* out,
+                                hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (S > kSplitMaxDev || ffn % 8) return hipErrorInvalidValue;
+  if (S > kSplitMaxDev || ffn % (interleaved ? 16 : 8)) return hipErrorInvalidValue;
   const long n = (long)M * (ffn / 8);
   hipLaunchKernelGGL(swiglu_finish_kernel, dim3((unsigned)((n + kNT - 1) / kNT)), dim3(kNT), 0, st, ws, S, ws_stride,
-                     M, ffn, (bf16_t*)out);
+                     M, ffn, interleaved ? 1 : 0, (bf16_t*)out);
   return hipGetLastError();
 }
 

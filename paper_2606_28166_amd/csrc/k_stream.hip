@@ -1,0 +1,357 @@
+// Decode projections: C = A . W^T for at most 128 activation rows, streaming
+// the weights from HBM straight into registers.
+//
+// At decode a projection is a wide, skinny product: every weight is used by
+// only the M <= 128 activation rows, so the kernel is a weight stream and its
+// speed is the bytes it keeps in flight.  Two things make that stream fast on
+// gfx950:
+//   * The weights are packed once (pack_weights_kernel, at init) into MFMA
+//     fragment order: a 32-row x 16-k block is one contiguous 1 KB fragment
+//     whose 64 lanes each hold the 8 k-values one lane of
+//     v_mfma_f32_32x32x16_bf16 consumes.  Every weight load is then one
+//     coalesced 1 KB piece per wave, issued as a non-temporal buffer load
+//     straight into VGPRs, NS - 1 chunks ahead of the arithmetic (512 KB of
+//     register file per compute unit holds far more bytes in flight than the
+//     160 KB of LDS).
+//   * The activations (split format: bf16 high and low parts, so the product
+//     keeps fp32-level inputs) are the operand every wave shares; they stream
+//     through an NS-stage LDS ring by direct global->LDS loads, XOR-swizzled
+//     so the fragment reads are free of bank conflicts.
+// A workgroup is 4 waves, one per SIMD.  Wave w owns NBW 32-row weight blocks
+// and all MB 32-row activation blocks, so each A fragment read from LDS feeds
+// 2 * NBW MFMAs.  The work is a list of items (a group of 128 * NBW weight
+// rows x one K slice); the grid is at most one workgroup per compute unit
+// and each workgroup walks its items as one continuous chunk stream, so the
+// prefetch runs on across item boundaries.  K slices > 1 write split-K
+// partial tiles that the consuming kernel sums in a fixed order.
+//
+// MFMA operand layout (32x32x16): lane l supplies row / column l % 32 and
+// the 8 k-values 8 (l / 32) .. +7 of the 16-value k-step; result element i
+// of lane l is row 8 (i / 4) + 4 (l / 32) + i % 4, column l % 32.
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace tandem {
+
+namespace {
+
+constexpr int SBK = 64;            // k-values per chunk (4 k-steps of 16)
+constexpr int SNW = 4;             // waves per workgroup
+
+// pair_rows F > 0 (a [2F][K] gate/up matrix): packed block b holds gate rows
+// 16 b .. 16 b + 15 in its first 16 rows and the matching up rows F + 16 b ..
+// in its last 16, so one MFMA output tile holds both halves of 16 SwiGLU
+// outputs.
+__global__ __launch_bounds__(256) void pack_weights_kernel(const bf16_t* __restrict__ W, int N, int K, int pair_rows,
+                                                           bf16_t* __restrict__ out, long n_pieces) {
+  const int ksn = K / 16;
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_pieces; i += (long)gridDim.x * blockDim.x) {
+    const long f = i >> 6;                        // fragment = (32-row block, 16-k step)
+    const int lane = (int)(i & 63);
+    const long nb = f / ksn;
+    const int ks = (int)(f % ksn);
+    const int c = lane & 31;
+    const long row = pair_rows > 0 ? (c < 16 ? nb * 16 + c : pair_rows + nb * 16 + (c - 16)) : nb * 32 + c;
+    const int k = 16 * ks + 8 * (lane >> 5);
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (row < N) v = *reinterpret_cast<const uint4*>(W + row * (long)K + k);
+    reinterpret_cast<uint4*>(out)[i] = v;
+  }
+}
+
+// Two prefetch distances: weights (from HBM) are loaded NS - 1 chunks ahead
+// into a ring of NS register sets; activations (L2-resident) one chunk ahead
+// into a 2-stage LDS ring.  Iteration c issues A(c + 1) then W(c + NS - 1);
+// loads retire in order, so waiting for A(c) (vmcnt <= the NWL weight loads
+// issued after it) also covers W(c), issued earlier.
+template <int MB, int NBW, int NS>
+struct StreamShape {
+  static constexpr int BM = 32 * MB;                 // activation rows of the tile
+  static constexpr int ASTAGE = BM * SBK * 4;        // bytes of one activation stage (hi + lo)
+  static constexpr int NA = BM / (4 * SNW);          // activation DMA instructions per wave per chunk
+  static constexpr int NWL = 4 * NBW;                // weight loads per wave per chunk
+  static constexpr int DW = NS - 1;                  // weight chunks in flight ahead of the arithmetic
+  static constexpr int WAIT = NWL;                   // vmcnt once A(c) (and so W(c)) has landed
+  static constexpr int COLS = SNW * NBW * 32;        // weight rows per item
+  static_assert(NS >= 2 && NS % 2 == 0, "ring of register sets (even: the LDS stage is c % 2)");
+  static_assert(2 * ASTAGE <= 160 * 1024, "LDS ring");
+  static_assert(NA >= 1, "at least one activation DMA per wave");
+};
+
+// Position in a workgroup's chunk stream: item (weight group x K slice) and
+// chunk inside the item's K slice.  Uniform across the workgroup.
+struct Cursor {
+  int item, grp, s, c, nloc;
+};
+
+__device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); }
+
+template <int MB, int NBW, int NS, int EPI>
+__global__ __launch_bounds__(256) void gemm_stream_kernel(
+    const bf16_t* __restrict__ A, const bf16_t* __restrict__ Wp, int M, int N, int K, int n_groups, int S, int cps,
+    float* __restrict__ out, int ldo, long split_stride) {
+  using G = StreamShape<MB, NBW, NS>;
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[2 * G::ASTAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 5, c32 = lane & 31;
+  const int nch = K / SBK;
+  const int n_items = n_groups * S;
+  const int nblk = (N + 31) >> 5;
+  const int grid = gridDim.x;
+  if ((int)blockIdx.x >= n_items) return;
+
+  auto set_item = [&](Cursor& u, int item) {
+    u.item = item;
+    u.s = item / n_groups;
+    u.grp = item - u.s * n_groups;
+    u.c = 0;
+    u.nloc = min(cps, nch - u.s * cps);
+  };
+  // the load cursor stays on the last chunk once the stream is exhausted
+  // (re-issuing it is a cache hit and keeps the wait counts uniform)
+  auto advance = [&](Cursor& u) {
+    if (u.c + 1 < u.nloc) { ++u.c; return; }
+    if (u.item + grid < n_items) set_item(u, u.item + grid);
+  };
+
+  // Activation DMA: instruction i of wave w covers tile rows r0 + 16 i .. +4
+  // (r0 = 4 w + lane / 16; 256 B per row: 8 hi pieces and 8 lo pieces);
+  // physical piece lane & 15 holds logical piece (lane & 15) ^ (row & 15).
+  const int r0 = 4 * wave + (lane >> 4);
+  const int lc = (lane & 15) ^ (r0 & 15);
+  const __amdgpu_buffer_rsrc_t wr = buf_rsrc(Wp, (uint32_t)((size_t)nblk * (K / 16) * 1024));
+  const int kfr = K / 16;                                  // fragments per 32-row block
+
+  u32x4_t wb[NS][NBW][4];
+  auto issue_a = [&](const Cursor& u, int stage) {
+    const int kc = u.s * cps + u.c;
+    unsigned char* st = ring + stage * G::ASTAGE;
+#pragma unroll
+    for (int i = 0; i < G::NA; ++i) {
+      const bf16_t* src = A + (size_t)min(r0 + 16 * i, M - 1) * 2 * (size_t)K + (size_t)kc * 2 * SBK + lc * 8;
+      load_lds16(src, st + 4 * (SNW * i + wave) * 256);
+    }
+  };
+  auto issue_w = [&](const Cursor& u, u32x4_t (&w)[NBW][4]) {
+    const int kc = u.s * cps + u.c;
+#pragma unroll
+    for (int b = 0; b < NBW; ++b) {
+      const int nb = min(u.grp * (SNW * NBW) + wave * NBW + b, nblk - 1);
+      const int base = (nb * kfr + 4 * kc) * 1024 + lane * 16;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[b][j] = buf_load16_nt(wr, base + j * 1024, 0);
+    }
+  };
+  // keeps the loads issued so far above the arithmetic of this chunk and
+  // makes the compiler wait for this chunk's weights here, not earlier
+  auto pin = [&](u32x4_t (&w)[NBW][4]) {
+#pragma unroll
+    for (int b = 0; b < NBW; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(w[b][j]) : : "memory");
+  };
+
+  f32x16_t acc[MB][NBW];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int b = 0; b < NBW; ++b) acc[mb][b] = f32x16_t{};
+
+  const uint32_t ring_addr = lds_addr_of(ring);
+  // A fragments of k-step j (k-values 16 j + 8 g .. +7 of the chunk = group 2 j + g)
+  auto read_a = [&](uint32_t st, int j, u32x4_t (&f)[MB][2]) {
+    const int q = 2 * j + g;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int r = mb * 32 + c32;
+      const uint32_t row = st + (uint32_t)(r * 256);
+      f[mb][0] = lds_read16(row + (uint32_t)(((2 * q) ^ (r & 15)) * 16));
+      f[mb][1] = lds_read16(row + (uint32_t)(((2 * q + 1) ^ (r & 15)) * 16));
+    }
+  };
+  auto fence_a = [&](u32x4_t (&f)[MB][2]) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      lds_fence_value(f[mb][0]);
+      lds_fence_value(f[mb][1]);
+    }
+  };
+  // one chunk = 4 k-steps; the A fragments of k-step j + 1 are read while the
+  // MFMAs of k-step j run (high parts of every block, then low parts, so
+  // consecutive MFMAs never share an accumulator when MB * NBW > 1)
+  auto compute = [&](int stage, u32x4_t (&w)[NBW][4]) {
+    const uint32_t st = ring_addr + (uint32_t)(stage * G::ASTAGE);
+    u32x4_t fa[MB][2], fb[MB][2];
+    read_a(st, 0, fa);
+    pin(w);
+    lds_wait();
+    fence_a(fa);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      u32x4_t (&cur)[MB][2] = (j & 1) ? fb : fa;
+      u32x4_t (&nxt)[MB][2] = (j & 1) ? fa : fb;
+      if (j < 3) read_a(st, j + 1, nxt);
+#pragma unroll
+      for (int part = 0; part < 2; ++part)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, cur[mb][part]);
+#pragma unroll
+          for (int b = 0; b < NBW; ++b)
+            acc[mb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, w[b][j]),
+                                                                 acc[mb][b], 0, 0, 0);
+        }
+      if (j < 3) {
+        lds_wait();
+        fence_a(nxt);
+      }
+    }
+  };
+  auto epilogue = [&](const Cursor& u) {
+    if (EPI == EPI_SWIGLU) {
+      // columns c < 16 of a block are gate sums, c + 16 the matching up sums
+      // (pair-interleaved packing); output column 16 nb + c, split format
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int b = 0; b < NBW; ++b) {
+          const int nb = u.grp * (SNW * NBW) + wave * NBW + b;
+          const int j = nb * 16 + (c32 & 15);
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const float v = acc[mb][b][i];
+            const float up = __shfl_xor(v, 16, 64);
+            const int m = mb * 32 + 8 * (i >> 2) + 4 * g + (i & 3);
+            if (m < M && c32 < 16 && j < ldo)
+              split_store(reinterpret_cast<bf16_t*>(out) + (size_t)m * 2 * ldo, j, silu_f(v) * up);
+            acc[mb][b][i] = 0.f;
+          }
+        }
+      return;
+    }
+    float* o = out + (size_t)u.s * split_stride;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int b = 0; b < NBW; ++b) {
+        const int n = (u.grp * (SNW * NBW) + wave * NBW + b) * 32 + c32;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int m = mb * 32 + 8 * (i >> 2) + 4 * g + (i & 3);
+          if (m < M && n < N) o[(size_t)m * ldo + n] = acc[mb][b][i];
+          acc[mb][b][i] = 0.f;
+        }
+      }
+  };
+
+  // Every item's chunk count is a multiple of NS (the host guarantees
+  // K % (64 NS) == 0 and cps % NS == 0), so chunk c of an item sits in
+  // register set c % NS and LDS stage c % 2: compile-time indices below.
+  Cursor la, lw, cp;                    // activation / weight load cursors, compute cursor
+  set_item(la, blockIdx.x);
+  lw = la;
+  issue_a(la, 0);
+  advance(la);
+#pragma unroll
+  for (int d = 0; d < G::DW; ++d) {
+    issue_w(lw, wb[d]);
+    advance(lw);
+  }
+  for (int item = blockIdx.x; item < n_items; item += grid) {
+    set_item(cp, item);
+    for (int c0 = 0; c0 < cp.nloc; c0 += NS) {
+#pragma unroll
+      for (int u = 0; u < NS; ++u) {
+        wait_vmcnt<G::WAIT>();          // A(c) and W(c) of this wave have landed
+        lds_wait();                     // and its LDS reads of the previous chunk are done
+        __builtin_amdgcn_s_barrier();   // ... in every wave: A(c) is complete, the other stage is free
+        issue_a(la, (u + 1) & 1);
+        advance(la);
+        issue_w(lw, wb[(u + G::DW) % NS]);
+        advance(lw);
+        compute(u & 1, wb[u]);
+      }
+    }
+    epilogue(cp);
+  }
+}
+
+template <int MB, int NBW, int EPI>
+hipError_t run_stream(const GemmStreamArgs& a, int grid, hipStream_t st) {
+  constexpr int NS = kStreamStages;
+  hipLaunchKernelGGL((gemm_stream_kernel<MB, NBW, NS, EPI>), dim3(grid), dim3(64 * SNW), 0, st,
+                     (const bf16_t*)a.A, (const bf16_t*)a.Wp, a.M, a.N, a.K, a.n_groups, a.S, a.cps, a.out, a.ldo,
+                     a.split_stride);
+  return hipGetLastError();
+}
+
+template <int MB>
+hipError_t dispatch_nbw(const GemmStreamArgs& a, int grid, hipStream_t st) {
+  return a.epi == EPI_SWIGLU ? run_stream<MB, 1, EPI_SWIGLU>(a, grid, st) : run_stream<MB, 1, EPI_PARTIAL>(a, grid, st);
+}
+
+}  // namespace
+
+size_t packed_weight_bytes(int N, int K) { return (size_t)((N + 31) / 32) * 32 * (size_t)K * 2; }
+
+bool stream_gemm_ok(int M, int N, int K) {
+  return M >= 1 && M <= kStreamMaxRows && K % (SBK * kStreamStages) == 0 && N >= 1 &&
+         packed_weight_bytes(N, K) < ((size_t)1 << 31);
+}
+
+hipError_t launch_pack_weights(const void* W, int N, int K, int pair_rows, void* out, hipStream_t st) {
+  if (pair_rows > 0 && (N != 2 * pair_rows || pair_rows % 16)) return hipErrorInvalidValue;
+  const long pieces = (long)((N + 31) / 32) * (K / 16) * 64;
+  const long blocks = std::min<long>((pieces + 255) / 256, 65536);
+  hipLaunchKernelGGL(pack_weights_kernel, dim3((unsigned)blocks), dim3(256), 0, st, (const bf16_t*)W, N, K, pair_rows,
+                     (bf16_t*)out, pieces);
+  return hipGetLastError();
+}
+
+StreamPlan plan_stream_gemm(int M, int N, int K, int n_cu, size_t ws_floats, int mode) {
+  // Cost in chunk times of the busiest workgroup: items are dealt round-robin
+  // to at most n_cu workgroups, each item costs its chunks plus about two for
+  // its epilogue and pipeline refill; K slices > 1 also pay for the partial
+  // tiles the consumer reads back (in 32 KB-per-unit chunks spread over the
+  // device) and, for SwiGLU, for the separate pass that applies it.
+  const int nch = K / SBK;
+  const int groups = (N + 127) / 128;
+  const int smax = mode == kPlanStore ? 1 : std::min(kSplitMaxStream, nch / kStreamStages);
+  double best = 1e300;
+  StreamPlan pl{1, 1, nch, groups, std::min(groups, n_cu)};
+  for (int S = 1; S <= std::max(1, smax); ++S) {
+    const int cps = ((nch + S - 1) / S + kStreamStages - 1) / kStreamStages * kStreamStages;
+    const int su = (nch + cps - 1) / cps;
+    if (su != S) continue;
+    if (S > 1 && (size_t)S * M * N > ws_floats) break;
+    const long items = (long)groups * S;
+    double cost = (double)((items + n_cu - 1) / n_cu) * (cps + 2);
+    if (S > 1) {
+      cost += (double)S * M * N * 4 / ((double)n_cu * 32768);
+      if (mode == kPlanSwiglu) cost += 4 + (double)S * M * N * 4 / ((double)n_cu * 16384);
+    }
+    if (cost < best) {
+      best = cost;
+      pl = StreamPlan{1, S, cps, groups, (int)std::min<long>(items, n_cu)};
+    }
+  }
+  return pl;
+}
+
+hipError_t launch_gemm_stream(const GemmStreamArgs& a, hipStream_t st) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (!stream_gemm_ok(a.M, a.N, a.K) || a.S < 1 || a.cps < 1 || a.n_groups < 1 || a.nbw != 1 ||
+      a.cps % kStreamStages != 0 || (long)a.S * a.cps < a.K / SBK || (long)(a.S - 1) * a.cps >= a.K / SBK ||
+      a.grid < 1)
+    return hipErrorInvalidValue;
+  if (a.epi == EPI_SWIGLU && (a.S != 1 || a.N % 32)) return hipErrorInvalidValue;
+  const int grid = std::min(a.grid, a.n_groups * a.S);
+  if (a.M <= 32) return dispatch_nbw<1>(a, grid, st);
+  if (a.M <= 64) return dispatch_nbw<2>(a, grid, st);
+  return dispatch_nbw<4>(a, grid, st);
+}
+
+}  // namespace tandem

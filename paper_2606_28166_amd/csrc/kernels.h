@@ -32,6 +32,44 @@ hipError_t launch_gemm(const GemmArgs& a, int* splits_used, hipStream_t st);
 // The K dimension granule of the MFMA path; other K use the VALU path.
 constexpr int kGemmBK = 64;
 
+// Decode projections over packed weights (k_stream.hip), M <= kStreamMaxRows.
+// Packed layout of a [N][K] bf16 matrix: fragments of 32 rows x 16 k, 1 KB
+// each, ordered [row block][k step]; lane l of fragment (nb, ks) holds
+// W[32 nb + l % 32][16 ks + 8 (l / 32) .. +7] (rows >= N are zero).
+constexpr int kStreamMaxRows = 128;
+constexpr int kStreamStages = 4;   // weight register sets; K % 256 == 0 and chunks per K slice % 4 == 0
+constexpr int kSplitMaxStream = 16;  // K slices at most (the consumers sum up to 16 partials)
+size_t packed_weight_bytes(int N, int K);
+bool stream_gemm_ok(int M, int N, int K);
+// pair_rows F > 0: W is a [2F][K] gate/up matrix, packed pair-interleaved (block b =
+// gate rows 16 b .. +15, then up rows F + 16 b .. +15) for the SwiGLU epilogue.
+hipError_t launch_pack_weights(const void* W, int N, int K, int pair_rows, void* out, hipStream_t st);
+struct StreamPlan {
+  int nbw;                // 32-row weight blocks per wave (1)
+  int S;                  // K slices (split-K partial tiles when > 1)
+  int cps;                // 64-wide k chunks per slice
+  int n_groups;           // weight-row groups of 128 * nbw rows
+  int grid;               // workgroups (<= items)
+};
+// Chooses the blocking for an M x N x K decode projection on n_cu compute
+// units.  kPlanStore: one K slice (plain output); kPlanPartial: split-K
+// partials (S * M * N <= ws_floats); kPlanSwiglu: S = 1 is the fused SwiGLU
+// epilogue, S > 1 partials plus a separate SwiGLU pass.
+enum { kPlanStore = 0, kPlanPartial = 1, kPlanSwiglu = 2 };
+StreamPlan plan_stream_gemm(int M, int N, int K, int n_cu, size_t ws_floats, int mode);
+struct GemmStreamArgs {
+  const void* A;          // split activations [M][2K] (bf16 hi/lo pieces)
+  const void* Wp;         // packed weights (pair-interleaved for EPI_SWIGLU)
+  int M, N, K;
+  int epi;                // EPI_PARTIAL / EPI_STORE: out + s * split_stride + m * ldo + n;
+                          // EPI_SWIGLU (S = 1): split-format rows of ldo = N / 2 outputs
+  float* out;
+  int ldo;
+  long split_stride;
+  int nbw, S, cps, n_groups, grid;
+};
+hipError_t launch_gemm_stream(const GemmStreamArgs& a, hipStream_t st);
+
 // Activations x feeding a GEMM are in split format for bf16 models (see
 // common.h) and plain fp32 for fp32 models; both take 4 bytes per value.
 
@@ -43,7 +81,10 @@ hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, c
 // SwiGLU of split-K gate/up partials: ws[s][m][0 .. ffn) are gate sums,
 // ws[s][m][ffn .. 2 ffn) the matching up sums; out[m] = silu(gate) * up in
 // split format (row stride 2 * ffn bf16).  ffn % 8 == 0.
-hipError_t launch_swiglu_finish(const float* ws, int S, long ws_stride, int M, int ffn, void* out, hipStream_t st);
+// interleaved: the partial columns follow the pair-interleaved packing (gate
+// j at 32 (j / 16) + j % 16, up j 16 columns later).
+hipError_t launch_swiglu_finish(const float* ws, int S, long ws_stride, int M, int ffn, bool interleaved, void* out,
+                                hipStream_t st);
 
 hipError_t launch_resid_norm(int dt, const float* ws, int S, long ws_stride, float* h,
                              const float* gain, float eps, void* x, int R, int d, hipStream_t st);

@@ -41,6 +41,11 @@ struct Layer {
   const float* ffn_norm;
   const void* w_gate_up;
   const void* w_down;
+  // packed copies (NULL: the matrix has none)
+  const void* p_qkv;
+  const void* p_o;
+  const void* p_gate_up;
+  const void* p_down;
 };
 
 struct ModelPlan {            // byte offsets / sizes of one model's buffers
@@ -49,7 +54,29 @@ struct ModelPlan {            // byte offsets / sizes of one model's buffers
   size_t ws_floats;
   size_t kv_half;             // bytes of the K (= V) cache
   size_t off_h, off_xa, off_xf, off_q, off_ws, off_logits, off_rope;
+  size_t off_packed, packed_bytes;   // MFMA-ordered copies of the projection and LM-head weights
 };
+
+// The matrices of a model in packing order: per layer QKV, O, gate/up, down,
+// then the LM head.  (rows N, reduction length K)
+std::vector<std::pair<int, int>> packed_shapes(const tandem_model_cfg* c) {
+  std::vector<std::pair<int, int>> v;
+  const int d = c->d_model, qkv = (c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim, att = c->n_q_heads * c->head_dim;
+  for (int l = 0; l < c->n_layers; ++l) {
+    v.push_back({qkv, d});
+    v.push_back({d, att});
+    v.push_back({2 * c->ffn_dim, d});
+    v.push_back({d, c->ffn_dim});
+  }
+  v.push_back({c->vocab, d});
+  return v;
+}
+
+// A matrix gets a packed copy (and the streaming decode GEMM) when the model
+// is bf16 and its shape fits that kernel.
+bool packs(const tandem_model_cfg* c, int N, int K) {
+  return c->weight_dtype == TANDEM_BF16 && c->ffn_dim % 16 == 0 && stream_gemm_ok(1, N, K);
+}
 
 struct Plan {
   int ctx_stride;
@@ -67,6 +94,7 @@ struct Model {
   std::vector<Layer> layers;
   const float* final_norm;
   const void* lm_head;
+  const void* p_lm;           // packed LM head (NULL: none)
   char* kc;
   char* vc;
   long layer_stride;          // elements
@@ -150,7 +178,8 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
     m.att_dim = c->n_q_heads * c->head_dim;
     m.rmax = cap->max_seqs > cap->max_prefill_tokens ? cap->max_seqs : cap->max_prefill_tokens;
     size_t nmax = (size_t)(m.qkv_dim > c->d_model ? m.qkv_dim : c->d_model);
-    if (split_gate_up(c) && (size_t)2 * c->ffn_dim > nmax) nmax = (size_t)2 * c->ffn_dim;
+    if ((split_gate_up(c) || c->weight_dtype == TANDEM_BF16) && (size_t)2 * c->ffn_dim > nmax)
+      nmax = (size_t)2 * c->ffn_dim;
     const size_t rows_ws = (size_t)kSplitMax * cap->max_seqs > (size_t)cap->max_prefill_tokens
                                ? (size_t)kSplitMax * cap->max_seqs
                                : (size_t)cap->max_prefill_tokens;
@@ -167,6 +196,10 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
     m.off_ws = sc; sc = align_up(sc + m.ws_floats * 4, kAlign);
     m.off_logits = sc; sc = align_up(sc + (size_t)cap->max_seqs * c->vocab * 4, kAlign);
     m.off_rope = sc; sc = align_up(sc + (size_t)P.ctx_stride * (c->head_dim / 2) * 8, kAlign);
+    m.packed_bytes = 0;
+    for (const auto& nk : packed_shapes(c))
+      if (packs(c, nk.first, nk.second)) m.packed_bytes += align_up(packed_weight_bytes(nk.first, nk.second), kAlign);
+    m.off_packed = sc; sc = align_up(sc + m.packed_bytes, kAlign);
   }
   P.kv_bytes = kv;
   const size_t S = (size_t)cap->max_seqs;
@@ -196,6 +229,11 @@ struct tandem_handle {
   // runs on a second stream forked from and joined back into `stream`.
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  // Step graphs are captured on and replayed on a stream of the library's own
+  // (the caller's may be the legacy null stream, which cannot be captured),
+  // ordered after and before the caller's stream by a pair of events.
+  hipStream_t gstream = nullptr;
+  hipEvent_t ev_in = nullptr, ev_out = nullptr;
   int n_cu = 256;             // compute units of the device (split-K sizing)
   int32_t *owner, *c, *t, *pos, *pending, *done;
   int32_t* seq_slot;
@@ -210,15 +248,24 @@ struct tandem_handle {
   std::string err = "no error";
   std::vector<int32_t> hbuf;  // host staging of prefill metadata
   // instrumentation: event pairs per kernel class
-  int timing = 0;             // class mask
-  std::vector<hipEvent_t> ev_pool;
+  int timing = 0;             // class mask and flags
+  std::vector<hipEvent_t> ev_pool;                   // eager launches
   size_t ev_used = 0;
-  std::vector<std::pair<int, size_t>> ev_marks[TANDEM_K_CLASSES];   // (class, index of the begin event)
+  std::vector<std::pair<int, size_t>> ev_marks;      // (class, index of the begin event), not yet summed
+  double acc_ms[TANDEM_K_CLASSES] = {};
+  int64_t acc_n[TANDEM_K_CLASSES] = {};
+  // Decode steps replay a captured HIP graph of the whole step (both
+  // forwards, sampling, handoff rule); rebuilt when the batch or the schedule
+  // flags change.  (Event records captured into a graph do not carry launch
+  // times, so timed steps are launched eagerly.)
+  hipGraphExec_t graph = nullptr;
+  int graph_R = -1, graph_flags = -1;
 };
 
 namespace {
 
-// Record a begin event for a kernel class on stream st (no-op unless timing is enabled).
+// Record a begin event for a kernel class on stream st (no-op unless timing
+// is enabled).
 hipError_t tim_begin(tandem_handle* h, int klass, size_t* idx, hipStream_t st) {
   *idx = SIZE_MAX;
   if (!(h->timing & (1 << klass))) return hipSuccess;
@@ -230,12 +277,36 @@ hipError_t tim_begin(tandem_handle* h, int klass, size_t* idx, hipStream_t st) {
   }
   *idx = h->ev_used;
   h->ev_used += 2;
-  h->ev_marks[klass].push_back({klass, *idx});
+  h->ev_marks.push_back({klass, *idx});
   return hipEventRecord(h->ev_pool[*idx], st);
 }
 hipError_t tim_end(tandem_handle* h, size_t idx, hipStream_t st) {
   if (idx == SIZE_MAX) return hipSuccess;
   return hipEventRecord(h->ev_pool[idx + 1], st);
+}
+
+// Add the recorded launch times to the class sums.
+hipError_t harvest_all(tandem_handle* h) {
+  if (h->ev_marks.empty()) return hipSuccess;
+  hipError_t r = hipStreamSynchronize(h->stream);
+  if (r != hipSuccess) return r;
+  for (const auto& mk : h->ev_marks) {
+    float ms = 0.f;
+    r = hipEventElapsedTime(&ms, h->ev_pool[mk.second], h->ev_pool[mk.second + 1]);
+    if (r != hipSuccess) return r;
+    h->acc_ms[mk.first] += ms;
+    h->acc_n[mk.first] += 1;
+  }
+  h->ev_marks.clear();
+  h->ev_used = 0;
+  return hipSuccess;
+}
+
+void drop_graphs(tandem_handle* h) {
+  if (h->graph) (void)hipGraphExecDestroy(h->graph);
+  h->graph = nullptr;
+  h->graph_R = -1;
+  h->graph_flags = -1;
 }
 
 }  // namespace
@@ -277,6 +348,77 @@ int choose_splits(int M, int N, int K, size_t ws_floats, int n_cu) {
   return S;
 }
 
+// One projection out = A . W^T (M rows): the streaming kernel over the packed
+// copy for decode-sized M, the tiled kernel otherwise.  EPI_PARTIAL writes
+// split-K partial tiles (stride M * N floats) and returns their count in *S;
+// EPI_STORE writes out[m * N + n].
+tandem_status gemm(tandem_handle* h, const Model& m, const void* A, const void* W, const void* Wp, int M, int N,
+                   int K, int epi, float* out, int* S, hipStream_t st) {
+  const int dt = m.cfg.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32;
+  *S = 1;
+  if (Wp && M <= kStreamMaxRows) {
+    const StreamPlan pl = plan_stream_gemm(M, N, K, h->n_cu, m.p.ws_floats, epi == EPI_STORE ? kPlanStore : kPlanPartial);
+    GemmStreamArgs a{};
+    a.A = A; a.Wp = Wp; a.M = M; a.N = N; a.K = K; a.epi = epi; a.out = out; a.ldo = N; a.split_stride = (long)M * N;
+    a.nbw = pl.nbw; a.S = pl.S; a.cps = pl.cps; a.n_groups = pl.n_groups; a.grid = pl.grid;
+    *S = pl.S;
+    TIMED(TANDEM_K_GEMM, launch_gemm_stream(a, st));
+    return TANDEM_OK;
+  }
+  GemmArgs g{};
+  g.dt = dt; g.A = A; g.W = W; g.M = M; g.N = N; g.K = K; g.epi = epi;
+  g.out = out; g.ldo = N; g.split_stride = (long)M * N;
+  g.splits = epi == EPI_PARTIAL ? choose_splits(M, N, K, m.p.ws_floats, h->n_cu) : 1;
+  TIMED(TANDEM_K_GEMM, launch_gemm(g, S, st));
+  return TANDEM_OK;
+}
+
+// Gate/up projection and SwiGLU: x_f = silu(A W_g^T) * (A W_u^T) in split
+// format.  Decode-sized M streams the pair-interleaved packed copy, with the
+// SwiGLU in the GEMM epilogue (one K slice) or in a pass over the split-K
+// partials; larger M uses the tiled kernel.
+tandem_status gate_up(tandem_handle* h, const Model& m, const Layer& L, int M, hipStream_t st) {
+  const tandem_model_cfg& c = m.cfg;
+  const int dt = c.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32;
+  const int d = c.d_model, F = c.ffn_dim;
+  if (L.p_gate_up && M <= kStreamMaxRows) {
+    const StreamPlan pl = plan_stream_gemm(M, 2 * F, d, h->n_cu, m.p.ws_floats, kPlanSwiglu);
+    GemmStreamArgs a{};
+    a.A = m.xa; a.Wp = L.p_gate_up; a.M = M; a.N = 2 * F; a.K = d;
+    a.nbw = pl.nbw; a.S = pl.S; a.cps = pl.cps; a.n_groups = pl.n_groups; a.grid = pl.grid;
+    if (pl.S == 1) {
+      a.epi = EPI_SWIGLU; a.out = (float*)m.xf; a.ldo = F;
+      TIMED(TANDEM_K_GEMM, launch_gemm_stream(a, st));
+    } else {
+      a.epi = EPI_PARTIAL; a.out = m.ws; a.ldo = 2 * F; a.split_stride = (long)M * 2 * F;
+      TIMED(TANDEM_K_GEMM, launch_gemm_stream(a, st));
+      TIMED(TANDEM_K_OTHER, launch_swiglu_finish(m.ws, pl.S, (long)M * 2 * F, M, F, true, m.xf, st));
+    }
+    return TANDEM_OK;
+  }
+  int S = 1;
+  if (split_gate_up(&c)) {
+    GemmArgs g{};
+    g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = M; g.N = 2 * F; g.K = d; g.epi = EPI_PARTIAL;
+    g.out = m.ws; g.ldo = 2 * F; g.split_stride = (long)M * 2 * F;
+    g.splits = choose_splits(M, 2 * F, d, m.p.ws_floats, h->n_cu);
+    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+    TIMED(TANDEM_K_OTHER, launch_swiglu_finish(m.ws, S, (long)M * 2 * F, M, F, false, m.xf, st));
+    return TANDEM_OK;
+  }
+  GemmArgs g{};
+  g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = M; g.N = F; g.K = d; g.epi = EPI_SWIGLU;
+  g.out = (float*)m.xf; g.ldo = F; g.splits = 1;
+  TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+  return TANDEM_OK;
+}
+
+#define CALL(expr)                                                                         \
+  do {                                                                                     \
+    tandem_status s_ = (expr);                                                             \
+    if (s_ != TANDEM_OK) return s_;                                                        \
+  } while (0)
+
 // Forward R rows through one model.  Rows read their token, cache slot and
 // position from the row arrays; done rows (row_done != NULL) skip the cache
 // append and produce zero attention.  With lm_head the logits land in m.logits.
@@ -295,13 +437,8 @@ tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok,
     cg.ctx_stride = h->plan.ctx_stride;
     cg.slot_stride = m.slot_stride;
 
-    GemmArgs g{};
-    g.dt = dt;
-    g.A = m.xa; g.W = L.w_qkv; g.M = R; g.N = qkv; g.K = d; g.epi = EPI_PARTIAL;
-    g.out = m.ws; g.ldo = qkv; g.split_stride = (long)R * qkv;
-    g.splits = choose_splits(R, qkv, d, m.p.ws_floats, h->n_cu);
     int S = 1;
-    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+    CALL(gemm(h, m, m.xa, L.w_qkv, L.p_qkv, R, qkv, d, EPI_PARTIAL, m.ws, &S, st));
 
     QkvPostArgs qp{};
     qp.dt = dt; qp.ws = m.ws; qp.S = S; qp.ws_stride = (long)R * qkv;
@@ -317,40 +454,17 @@ tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok,
     aa.row_slot = row_slot; aa.row_pos = row_pos; aa.row_done = row_done; aa.out = m.xa;
     TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
 
-    g = GemmArgs{};
-    g.dt = dt; g.A = m.xa; g.W = L.w_o; g.M = R; g.N = d; g.K = att; g.epi = EPI_PARTIAL;
-    g.out = m.ws; g.ldo = d; g.split_stride = (long)R * d;
-    g.splits = choose_splits(R, d, att, m.p.ws_floats, h->n_cu);
-    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+    CALL(gemm(h, m, m.xa, L.w_o, L.p_o, R, d, att, EPI_PARTIAL, m.ws, &S, st));
     TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, L.ffn_norm, c.rms_eps, m.xa, R, d, st));
 
-    g = GemmArgs{};
-    if (split_gate_up(&c)) {
-      g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = R; g.N = 2 * c.ffn_dim; g.K = d; g.epi = EPI_PARTIAL;
-      g.out = m.ws; g.ldo = 2 * c.ffn_dim; g.split_stride = (long)R * 2 * c.ffn_dim;
-      g.splits = choose_splits(R, 2 * c.ffn_dim, d, m.p.ws_floats, h->n_cu);
-      TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
-      TIMED(TANDEM_K_OTHER, launch_swiglu_finish(m.ws, S, (long)R * 2 * c.ffn_dim, R, c.ffn_dim, m.xf, st));
-    } else {
-      g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = R; g.N = c.ffn_dim; g.K = d; g.epi = EPI_SWIGLU;
-      g.out = (float*)m.xf; g.ldo = c.ffn_dim; g.splits = 1;
-      TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
-    }
-
-    g = GemmArgs{};
-    g.dt = dt; g.A = m.xf; g.W = L.w_down; g.M = R; g.N = d; g.K = c.ffn_dim; g.epi = EPI_PARTIAL;
-    g.out = m.ws; g.ldo = d; g.split_stride = (long)R * d;
-    g.splits = choose_splits(R, d, c.ffn_dim, m.p.ws_floats, h->n_cu);
-    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+    CALL(gate_up(h, m, L, R, st));
+    CALL(gemm(h, m, m.xf, L.w_down, L.p_down, R, d, c.ffn_dim, EPI_PARTIAL, m.ws, &S, st));
     const float* next_gain = (l + 1 < c.n_layers) ? m.layers[l + 1].attn_norm : m.final_norm;
     TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, next_gain, c.rms_eps, m.xa, R, d, st));
   }
   if (lm_head) {
-    GemmArgs g{};
-    g.dt = dt; g.A = m.xa; g.W = m.lm_head; g.M = R; g.N = c.vocab; g.K = d; g.epi = EPI_STORE;
-    g.out = m.logits; g.ldo = c.vocab; g.splits = 1;
     int S = 1;
-    TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
+    CALL(gemm(h, m, m.xa, m.lm_head, m.p_lm, R, c.vocab, d, EPI_STORE, m.logits, &S, st));
   }
   return TANDEM_OK;
 }
@@ -378,10 +492,8 @@ tandem_status forward_pair(tandem_handle* h, int R, const int32_t* row_tok, cons
   return TANDEM_OK;
 }
 
-tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg, int32_t* n_active) {
-  if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
-  if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
-  if (!h->prefilled) return fail(&h->err, TANDEM_E_STATE, "tandem_step before tandem_prefill");
+// Enqueue one decode step (both forwards, sampling, outputs, handoff rule).
+tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg) {
   const int R = h->n_seq;
   hipStream_t st = h->stream;
   {
@@ -415,6 +527,59 @@ tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_de
   fa.out_len = h->out.length; fa.ld_out = h->smp.max_new_tokens;
   fa.dbg_sampled = dbg ? dbg->sampled : nullptr; fa.dbg_margin = dbg ? dbg->margin : nullptr;
   TIMED(TANDEM_K_SAMPLE, launch_sample_finish(fa, st));
+  return TANDEM_OK;
+}
+
+// Capture the step into h->graph (the streams return to normal operation
+// whatever happens inside).
+tandem_status capture_step(tandem_handle* h) {
+  hipStream_t caller = h->stream;
+  HIPCHK(hipStreamBeginCapture(h->gstream, hipStreamCaptureModeThreadLocal));
+  h->stream = h->gstream;                 // the step's main stream while recording
+  tandem_status s = record_step(h, nullptr, nullptr);
+  h->stream = caller;
+  hipGraph_t graph = nullptr;
+  hipError_t e = hipStreamEndCapture(h->gstream, &graph);
+  if (s != TANDEM_OK) {
+    if (graph) (void)hipGraphDestroy(graph);
+    return s;
+  }
+  HIPCHK(e);
+  e = hipGraphInstantiate(&h->graph, graph, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph);
+  if (e != hipSuccess) h->graph = nullptr;
+  HIPCHK(e);
+  return TANDEM_OK;
+}
+
+tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg, int32_t* n_active) {
+  if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
+  if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
+  if (!h->prefilled) return fail(&h->err, TANDEM_E_STATE, "tandem_step before tandem_prefill");
+  const int R = h->n_seq;
+  hipStream_t st = h->stream;
+  const bool timed = (h->timing & ((1 << TANDEM_K_CLASSES) - 1)) != 0;
+  const bool graph = !forced && !dbg && !timed && !(h->timing & TANDEM_TIMING_EAGER);
+  if (graph) {
+    if (!h->graph || h->graph_R != R || h->graph_flags != h->timing) {
+      drop_graphs(h);
+      tandem_status s = capture_step(h);
+      if (s != TANDEM_OK) {
+        drop_graphs(h);
+        return s;
+      }
+      h->graph_R = R;
+      h->graph_flags = h->timing;
+    }
+    HIPCHK(hipEventRecord(h->ev_in, st));
+    HIPCHK(hipStreamWaitEvent(h->gstream, h->ev_in, 0));
+    HIPCHK(hipGraphLaunch(h->graph, h->gstream));
+    HIPCHK(hipEventRecord(h->ev_out, h->gstream));
+    HIPCHK(hipStreamWaitEvent(st, h->ev_out, 0));
+  } else {
+    tandem_status s = record_step(h, forced, dbg);
+    if (s != TANDEM_OK) return s;
+  }
   if (n_active) {
     HIPCHK(launch_count_active(h->done, R, h->d_count, st));
     HIPCHK(hipMemcpyAsync(h->h_count, h->d_count, 4, hipMemcpyDeviceToHost, st));
@@ -535,7 +700,7 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     for (int l = 0; l < m.cfg.n_layers; ++l) {
       const void* const* p = src->layers + 8 * l;
       m.layers[l] = Layer{(const float*)p[0], p[1], (const float*)p[2], (const float*)p[3],
-                          p[4], (const float*)p[5], p[6], p[7]};
+                          p[4], (const float*)p[5], p[6], p[7], nullptr, nullptr, nullptr, nullptr};
     }
     m.slot_stride = (long)m.cfg.n_kv_heads * P.ctx_stride * m.cfg.head_dim;
     m.layer_stride = (long)cap->max_seqs * m.slot_stride;
@@ -549,6 +714,7 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     m.ws = (float*)(sc + m.p.off_ws);
     m.logits = (float*)(sc + m.p.off_logits);
     m.rope = (float2*)(sc + m.p.off_rope);
+    m.p_lm = nullptr;
   }
   const size_t S = (size_t)cap->max_seqs;
   int32_t* stt = (int32_t*)(sc + P.off_state);
@@ -571,6 +737,9 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
     if (h->ev_join) (void)hipEventDestroy(h->ev_join);
     if (h->side) (void)hipStreamDestroy(h->side);
+    if (h->ev_in) (void)hipEventDestroy(h->ev_in);
+    if (h->ev_out) (void)hipEventDestroy(h->ev_out);
+    if (h->gstream) (void)hipStreamDestroy(h->gstream);
     delete h;
     return fail(nullptr, TANDEM_E_HIP, msg);
   };
@@ -590,9 +759,44 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   if (e != hipSuccess) { h->ev_fork = nullptr; return bail(e, "fork event"); }
   e = hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming);
   if (e != hipSuccess) { h->ev_join = nullptr; return bail(e, "join event"); }
+  e = hipStreamCreateWithFlags(&h->gstream, hipStreamNonBlocking);
+  if (e != hipSuccess) { h->gstream = nullptr; return bail(e, "graph stream"); }
+  e = hipEventCreateWithFlags(&h->ev_in, hipEventDisableTiming);
+  if (e != hipSuccess) { h->ev_in = nullptr; return bail(e, "graph entry event"); }
+  e = hipEventCreateWithFlags(&h->ev_out, hipEventDisableTiming);
+  if (e != hipSuccess) { h->ev_out = nullptr; return bail(e, "graph exit event"); }
   for (int i = 0; i < 2; ++i) {
     e = launch_rope_table(h->m[i].cfg.rope_theta, h->m[i].cfg.head_dim, P.ctx_stride, h->m[i].rope, h->stream);
     if (e != hipSuccess) return bail(e, "rope table");
+  }
+  // MFMA-ordered copies of the projection and LM-head weights (read by the
+  // streaming decode GEMM; the caller's row-major weights stay in use for
+  // prefill-sized products)
+  for (int i = 0; i < 2; ++i) {
+    Model& m = h->m[i];
+    char* dst = sc + m.p.off_packed;
+    const auto shapes = packed_shapes(&m.cfg);
+    size_t k = 0;
+    auto pack = [&](const void* src, int N, int K, int pair_rows, const void** out) -> hipError_t {
+      const auto& nk = shapes[k++];
+      if (nk.first != N || nk.second != K) return hipErrorInvalidValue;
+      *out = nullptr;
+      if (!packs(&m.cfg, N, K)) return hipSuccess;
+      hipError_t r = launch_pack_weights(src, N, K, pair_rows, dst, h->stream);
+      *out = dst;
+      dst += align_up(packed_weight_bytes(N, K), kAlign);
+      return r;
+    };
+    const tandem_model_cfg& c = m.cfg;
+    for (int l = 0; l < c.n_layers && e == hipSuccess; ++l) {
+      Layer& L = m.layers[l];
+      if (e == hipSuccess) e = pack(L.w_qkv, m.p.qkv_dim, c.d_model, 0, &L.p_qkv);
+      if (e == hipSuccess) e = pack(L.w_o, c.d_model, m.p.att_dim, 0, &L.p_o);
+      if (e == hipSuccess) e = pack(L.w_gate_up, 2 * c.ffn_dim, c.d_model, c.ffn_dim, &L.p_gate_up);
+      if (e == hipSuccess) e = pack(L.w_down, c.d_model, c.ffn_dim, 0, &L.p_down);
+    }
+    if (e == hipSuccess) e = pack(m.lm_head, c.vocab, c.d_model, 0, &m.p_lm);
+    if (e != hipSuccess) return bail(e, "weight packing");
   }
   std::vector<int32_t> ident(S);
   for (size_t i = 0; i < S; ++i) ident[i] = (int32_t)i;
@@ -625,6 +829,7 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
   }
   hipStream_t st = h->stream;
   h->prefilled = false;
+  drop_graphs(h);      // a new batch: the step graph is captured again on demand
   const int n_seq = n_prompts * G;
   {
     // token ids index the embedding tables: check them on the host before any kernel reads them
@@ -726,9 +931,13 @@ tandem_status tandem_timing_enable(tandem_handle* h, int32_t class_mask) {
   if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
   if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
   HIPCHK(hipStreamSynchronize(h->stream));
-  h->timing = class_mask & (((1 << TANDEM_K_CLASSES) - 1) | TANDEM_TIMING_SERIAL);
+  h->timing = class_mask & (((1 << TANDEM_K_CLASSES) - 1) | TANDEM_TIMING_SERIAL | TANDEM_TIMING_EAGER);
   h->ev_used = 0;
-  for (auto& v : h->ev_marks) v.clear();
+  h->ev_marks.clear();
+  for (int k = 0; k < TANDEM_K_CLASSES; ++k) {
+    h->acc_ms[k] = 0.0;
+    h->acc_n[k] = 0;
+  }
   return TANDEM_OK;
 }
 
@@ -737,15 +946,9 @@ tandem_status tandem_timing_read(tandem_handle* h, int32_t kernel_class, double*
   if (kernel_class < 0 || kernel_class >= TANDEM_K_CLASSES || !total_ms || !launches)
     return fail(&h->err, TANDEM_E_ARG, "tandem_timing_read: bad kernel class or NULL output");
   if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
-  HIPCHK(hipStreamSynchronize(h->stream));
-  double ms = 0.0;
-  for (const auto& mk : h->ev_marks[kernel_class]) {
-    float e = 0.f;
-    HIPCHK(hipEventElapsedTime(&e, h->ev_pool[mk.second], h->ev_pool[mk.second + 1]));
-    ms += e;
-  }
-  *total_ms = ms;
-  *launches = (int64_t)h->ev_marks[kernel_class].size();
+  HIPCHK(harvest_all(h));
+  *total_ms = h->acc_ms[kernel_class];
+  *launches = h->acc_n[kernel_class];
   return TANDEM_OK;
 }
 
@@ -753,10 +956,15 @@ void tandem_destroy(tandem_handle* h) {
   if (!h) return;
   (void)hipStreamSynchronize(h->stream);
   if (h->side) (void)hipStreamSynchronize(h->side);
+  if (h->gstream) (void)hipStreamSynchronize(h->gstream);
+  drop_graphs(h);
   for (hipEvent_t e : h->ev_pool) (void)hipEventDestroy(e);
   if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   if (h->ev_join) (void)hipEventDestroy(h->ev_join);
   if (h->side) (void)hipStreamDestroy(h->side);
+  if (h->ev_in) (void)hipEventDestroy(h->ev_in);
+  if (h->ev_out) (void)hipEventDestroy(h->ev_out);
+  if (h->gstream) (void)hipStreamDestroy(h->gstream);
   if (h->h_count) (void)hipHostFree(h->h_count);
   delete h;
 }
