@@ -51,7 +51,7 @@ def rollout(sen: OracleModel, jun: OracleModel, prompts: Sequence[np.ndarray], G
             switch, sample, seed: int, boundary: Optional[np.ndarray] = None,
             forced: Optional[np.ndarray] = None, keep_logits_at: Sequence[int] = (),
             seq_subset: Optional[Sequence[int]] = None, max_steps: Optional[int] = None,
-            start_state=None) -> RolloutResult:
+            start_state=None, progress=None) -> RolloutResult:
     """Run the tandem rollout.
 
     switch: workloads.SwitchSettings; sample: workloads.SampleSettings.
@@ -59,6 +59,8 @@ def rollout(sen: OracleModel, jun: OracleModel, prompts: Sequence[np.ndarray], G
     result depends only on the weights, its prompt, the seed and its id).
     max_steps truncates the run (the stop rule still uses sample.max_new).
     forced: int array [n_rows, >= steps] of tokens to append, by row.
+    progress: optional callable(step, n_steps), called after prefill (step 0)
+    and after every decode step (reporting only; the result does not depend on it).
     """
     V = sen.s.vocab
     if jun.s.vocab != V:
@@ -91,6 +93,8 @@ def rollout(sen: OracleModel, jun: OracleModel, prompts: Sequence[np.ndarray], G
         pending[r] = int(x[-1])
     del proto
 
+    if progress is not None:
+        progress(0, steps)
     owner = np.array([first_owner(switch.first_owner, seed, int(s), thr) for s in ids], np.int64)
     c = np.zeros(R, np.int64)
     t = np.ones(R, np.int64)
@@ -141,6 +145,8 @@ def rollout(sen: OracleModel, jun: OracleModel, prompts: Sequence[np.ndarray], G
             pending[r] = y
             pos[r] += 1
             t[r] += 1
+        if progress is not None:
+            progress(step + 1, steps)
 
     return RolloutResult(out_tok, out_smp, out_own, out_lp, out_mg, out_dec, length,
                          owner.astype(np.int32), c.astype(np.int32), t.astype(np.int32),

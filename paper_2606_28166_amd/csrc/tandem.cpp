@@ -440,18 +440,28 @@ tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok,
     int S = 1;
     CALL(gemm(h, m, m.xa, L.w_qkv, L.p_qkv, R, qkv, d, EPI_PARTIAL, m.ws, &S, st));
 
-    QkvPostArgs qp{};
-    qp.dt = dt; qp.ws = m.ws; qp.S = S; qp.ws_stride = (long)R * qkv;
-    qp.R = R; qp.nq = nq; qp.nkv = nkv; qp.hd = hd;
-    qp.q_norm = c.qk_norm ? L.q_norm : nullptr; qp.k_norm = c.qk_norm ? L.k_norm : nullptr;
-    qp.eps = c.rms_eps; qp.rope = m.rope;
-    qp.row_slot = row_slot; qp.row_pos = row_pos; qp.row_done = row_done;
-    qp.q_out = m.q; qp.cache = cg;
-    TIMED(TANDEM_K_OTHER, launch_qkv_post(qp, st));
+    // decode rows (each its own cache slot) on the MFMA attention path get
+    // the QKV post-processing inside the attention kernel
+    const bool fuse = row_done != nullptr && attention_has_mfma(dt, hd, nq / nkv);
+    if (!fuse) {
+      QkvPostArgs qp{};
+      qp.dt = dt; qp.ws = m.ws; qp.S = S; qp.ws_stride = (long)R * qkv;
+      qp.R = R; qp.nq = nq; qp.nkv = nkv; qp.hd = hd;
+      qp.q_norm = c.qk_norm ? L.q_norm : nullptr; qp.k_norm = c.qk_norm ? L.k_norm : nullptr;
+      qp.eps = c.rms_eps; qp.rope = m.rope;
+      qp.row_slot = row_slot; qp.row_pos = row_pos; qp.row_done = row_done;
+      qp.q_out = m.q; qp.cache = cg;
+      TIMED(TANDEM_K_OTHER, launch_qkv_post(qp, st));
+    }
 
     AttnArgs aa{};
     aa.dt = dt; aa.q = m.q; aa.R = R; aa.nq = nq; aa.nkv = nkv; aa.hd = hd; aa.cache = cg;
     aa.row_slot = row_slot; aa.row_pos = row_pos; aa.row_done = row_done; aa.out = m.xa;
+    if (fuse) {
+      aa.fuse.ws = m.ws; aa.fuse.S = S; aa.fuse.ws_stride = (long)R * qkv; aa.fuse.nkv = nkv;
+      aa.fuse.q_norm = c.qk_norm ? L.q_norm : nullptr; aa.fuse.k_norm = c.qk_norm ? L.k_norm : nullptr;
+      aa.fuse.eps = c.rms_eps; aa.fuse.rope = m.rope;
+    }
     TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
 
     CALL(gemm(h, m, m.xa, L.w_o, L.p_o, R, d, att, EPI_PARTIAL, m.ws, &S, st));

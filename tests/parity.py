@@ -63,8 +63,12 @@ def run(wl: W.Workload, steps: Optional[int] = None, logits_at: Sequence[int] = 
     ws, wj, prompts, bnd = weights if weights is not None else W.make_all(wl)
     sen, jun = build_models(wl, ws, wj)
     t0 = time.time()
+    def progress(t, n):
+        if n >= 32 and (t % 16 == 0 or t == n):
+            log(f"  oracle {wl.name}: step {t}/{n} ({time.time() - t0:.0f}s)")
+
     ref = rollout(sen, jun, prompts, wl.group, wl.switch, wl.sample, wl.philox_seed, bnd,
-                  max_steps=steps, keep_logits_at=logits_at, seq_subset=seq_subset)
+                  max_steps=steps, keep_logits_at=logits_at, seq_subset=seq_subset, progress=progress)
     log(f"  oracle {wl.name}: {time.time() - t0:.1f}s")
     rows = ref.seq_ids
     n = wl.n_seqs
