@@ -97,6 +97,26 @@ def prefill_flops(wl: W.Workload, plens) -> float:
     return f
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_attention_traffic_qwen.txt")
+
+
+def measured_traffic_ratio():
+    """HBM bytes (FETCH_SIZE + WRITE_SIZE, calibrated on a plain copy) per
+    algorithmic K/V byte of the decode attention kernel, from the committed
+    rocprofv3 counter summary; None when that summary is missing or was taken
+    on a different version of the kernel source."""
+    import hashlib
+    try:
+        d = json.loads(open(TRAFFIC_FILE).read().split("\n\n", 1)[1])
+        src = os.path.join(ROOT, "paper_2606_28166_amd", "csrc", "k_attn.hip")
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        if d["kernel_source_sha256_16"] != digest:
+            return None
+        return float(d["traffic_over_algorithmic"])
+    except (OSError, IndexError, KeyError, ValueError):
+        return None
+
+
 # ------------------------------------------------------------------ CPU oracle
 def cpu_baseline(wl: W.Workload, ws, wj, prompts, steps: int):
     """The oracle (float64 NumPy) on prompt 0's G rows: its prefill plus `steps` decode steps."""
@@ -205,14 +225,18 @@ def main():
     # around every launch on the stream it runs on: one with the two forwards
     # serialized (each launch alone on the GPU: the kernel's own roofline, and
     # the per-class breakdown), one in the production two-stream schedule.
+    traffic_ratio = measured_traffic_ratio() if wl.name == "qwen" else None
+
     def roofline_of(att, method):
         ms, nl = att
         nbytes = attention_bytes(wl, plens, L)
         gbs = nbytes / (ms / 1e3) / 1e9
+        per = nbytes / max(nl, 1)
         return {"bound": "hbm", "kernel": "decode attention (both models)", "achieved": round(gbs, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                "traffic": None if traffic_ratio is None else int(per * traffic_ratio),
                 "launches": nl, "avg_launch_us": round(ms * 1e3 / max(nl, 1), 2),
-                "bytes_per_launch": int(nbytes / max(nl, 1)), "method": method}
+                "bytes_per_launch": int(per), "method": method}
 
     roof, roof_conc, breakdown = None, None, None
     if not args.no_isolated:

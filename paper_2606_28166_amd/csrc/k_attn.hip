@@ -298,19 +298,18 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
 
   // Two register buffers: the next chunk of this wave is in flight while the
   // current one is consumed.  The loop walks the wave's chunks in pairs and
-  // always issues the same loads (indices past the wave's last chunk are
-  // clamped to it: a cache hit), so the only condition inside is whether the
-  // pair's second chunk exists.  pin_chunk keeps the next chunk's loads
+  // loads only chunks that exist (uniform branches: a re-read of a streamed
+  // chunk would come from HBM again).  pin_chunk keeps the next chunk's loads
   // ahead of the current chunk's arithmetic (left alone, the compiler sinks
   // the loads to their first use and the prefetch disappears).
-  if (nmine > 0) {
-    for (int i = 0; i < nmine; i += 2) {
-      load_chunk<HD>(cb, kr, vr, chunk_at(i + 1), lane);
-      pin_chunk<HD>(ca);
-      attend_chunk<HD>(st, ca, qh, ql, 16 * chunk_at(i), ctx, scale, g);
-      load_chunk<HD>(ca, kr, vr, chunk_at(i + 2), lane);
+  for (int i = 0; i < nmine; i += 2) {
+    if (i + 1 < nmine) load_chunk<HD>(cb, kr, vr, chunk_at(i + 1), lane);
+    pin_chunk<HD>(ca);
+    attend_chunk<HD>(st, ca, qh, ql, 16 * chunk_at(i), ctx, scale, g);
+    if (i + 2 < nmine) load_chunk<HD>(ca, kr, vr, chunk_at(i + 2), lane);
+    if (i + 1 < nmine) {
       pin_chunk<HD>(cb);
-      if (i + 1 < nmine) attend_chunk<HD>(st, cb, qh, ql, 16 * chunk_at(i + 1), ctx, scale, g);
+      attend_chunk<HD>(st, cb, qh, ql, 16 * chunk_at(i + 1), ctx, scale, g);
     }
   }
 
