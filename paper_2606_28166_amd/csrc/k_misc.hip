@@ -1,6 +1,8 @@
 // Row-wise kernels of the tandem step: embedding + RMSNorm, residual +
 // RMSNorm, QKV post-processing with the KV append, sampling, the handoff
 // rule, prompt-KV replication and per-sequence state set-up.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -250,8 +252,9 @@ __device__ __forceinline__ void merge_lse(float& m, float& l, float m2, float l2
 __global__ __launch_bounds__(kNT) void sample_partials_kernel(SampleArgs a) {
   __shared__ float sm[kNT / 64][5];
   const int ch = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
-  if (a.done[r]) return;
-  const int s = r, tt = a.t[s];
+  const int s = a.act[r];
+  if (a.done[s]) return;
+  const int tt = a.t[s];
   const bool own_sen = a.owner[s] != 0;
   const float* zs = a.z_sen + (size_t)r * a.V;
   const float* zj = a.z_jun + (size_t)r * a.V;
@@ -301,7 +304,7 @@ __global__ __launch_bounds__(kNT) void sample_partials_kernel(SampleArgs a) {
 // senior log-prob, write the outputs and apply the handoff rule.
 __global__ __launch_bounds__(64) void sample_finish_kernel(FinishArgs a) {
   const int r = blockIdx.x, lane = threadIdx.x;
-  const int s = r;
+  const int s = a.act[r];
   if (a.done[s]) return;
   float ms = -INFINITY, ls = 0.f;
   Top2 top{-INFINITY, 0x7FFFFFFF, -INFINITY};
@@ -406,6 +409,75 @@ __global__ void count_active_kernel(const int32_t* done, int n, int32_t* out) {
   if (threadIdx.x == 0) *out = (int32_t)c;
 }
 
+// One workgroup of 1024 threads: a count pass, then a write pass in which
+// each 1024-id block places its unfinished ids after the running count of
+// earlier ones (block prefix sum) and its finished ids after all unfinished.
+__global__ __launch_bounds__(1024) void compact_kernel(const int32_t* __restrict__ done, int n,
+                                                       int32_t* __restrict__ act, int32_t* __restrict__ n_out) {
+  __shared__ int wsum[16];
+  __shared__ int base_a, base_d, total_a;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // block-wide exclusive prefix of flag over the 1024 threads; returns the block total
+  auto scan = [&](int flag, int* excl) -> int {
+    int x = flag;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) wsum[w] = x;
+    __syncthreads();
+    int before = 0, tot = 0;
+    for (int i = 0; i < 16; ++i) {
+      if (i < w) before += wsum[i];
+      tot += wsum[i];
+    }
+    __syncthreads();
+    *excl = before + x - flag;
+    return tot;
+  };
+  int cnt = 0;
+  for (int b = 0; b < n; b += 1024) {
+    const int s = b + tid;
+    int ex;
+    cnt += scan(s < n && !done[s] ? 1 : 0, &ex);
+  }
+  if (tid == 0) { total_a = cnt; base_a = 0; base_d = cnt; }
+  __syncthreads();
+  for (int b = 0; b < n; b += 1024) {
+    const int s = b + tid;
+    const int alive = s < n && !done[s] ? 1 : 0;
+    const int fin = s < n && done[s] ? 1 : 0;
+    int ea, ed;
+    const int ta = scan(alive, &ea);
+    const int td = scan(fin, &ed);
+    if (alive) act[base_a + ea] = s;
+    if (fin) act[base_d + ed] = s;
+    __syncthreads();
+    if (tid == 0) { base_a += ta; base_d += td; }
+    __syncthreads();
+  }
+  if (tid == 0) *n_out = total_a;
+}
+
+__global__ void gather_rows_kernel(GatherRowsArgs a) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= a.R) return;
+  const int s = a.act[r];
+  a.row_tok[r] = a.pending[s];
+  a.row_slot[r] = a.seq_slot[s];
+  a.row_pos[r] = a.pos[s];
+  a.row_done[r] = a.done[s];
+}
+
+__global__ void scatter_rows_kernel(const float* __restrict__ src, const int32_t* __restrict__ act, int V,
+                                    float* __restrict__ dst) {
+  const int r = blockIdx.y;
+  const float* sp = src + (size_t)r * V;
+  float* dp = dst + (size_t)act[r] * V;
+  for (int v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) dp[v] = sp[v];
+}
+
 __global__ void gather_i32_kernel(const int32_t* src, const int32_t* idx, int n, int32_t* dst) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) dst[i] = src[idx[i]];
@@ -502,6 +574,24 @@ hipError_t launch_init_state(const InitStateArgs& a, hipStream_t st) {
 
 hipError_t launch_count_active(const int32_t* done, int n, int32_t* out, hipStream_t st) {
   hipLaunchKernelGGL(count_active_kernel, dim3(1), dim3(kNT), 0, st, done, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_compact(const int32_t* done, int n, int32_t* act, int32_t* n_active_out, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, st, done, n, act, n_active_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const GatherRowsArgs& a, hipStream_t st) {
+  if (a.R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3((a.R + 255) / 256), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_rows(const float* src, const int32_t* act, int R, int V, float* dst, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(scatter_rows_kernel, dim3(std::min((V + 255) / 256, 64), R), dim3(256), 0, st, src, act, V, dst);
   return hipGetLastError();
 }
 

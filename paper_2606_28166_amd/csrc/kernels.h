@@ -146,14 +146,16 @@ struct SampleArgs {
   int R, V;
   float temp; int eos_id; float eos_bias_sen, eos_bias_jun;
   uint32_t key0, key1;
-  const int32_t* owner; const int32_t* t; const int32_t* done;   // per sequence (row == seq)
+  const int32_t* owner; const int32_t* t; const int32_t* done;   // per sequence
+  const int32_t* act;     // [R] sequence of each row
   float* partials;        // [R][n_chunks][5]
   int chunk;              // vocab entries per chunk
 };
 hipError_t launch_sample_partials(const SampleArgs& a, int n_chunks, hipStream_t st);
 
 struct FinishArgs {
-  const float* z_sen; int R, V;
+  const float* z_sen; int R, V;           // logits by row
+  const int32_t* act;                     // [R] sequence of each row (state and outputs by sequence)
   float temp; int eos_id; float eos_bias_sen;
   const float* partials; int n_chunks;
   const int32_t* forced;                      // [R] or NULL
@@ -185,6 +187,22 @@ struct InitStateArgs {
 hipError_t launch_init_state(const InitStateArgs& a, hipStream_t st);
 
 hipError_t launch_count_active(const int32_t* done, int n, int32_t* out, hipStream_t st);
+
+// Stable partition of the sequence ids 0 .. n-1: act[0 .. n_active) = the
+// unfinished ones in increasing order, then the finished ones in increasing
+// order; *n_active_out = their count.  One workgroup.
+hipError_t launch_compact(const int32_t* done, int n, int32_t* act, int32_t* n_active_out, hipStream_t st);
+
+// Decode row arrays for rows 0 .. R-1 from the row -> sequence map.
+struct GatherRowsArgs {
+  const int32_t* act; int R;
+  const int32_t* pending; const int32_t* seq_slot; const int32_t* pos; const int32_t* done;
+  int32_t* row_tok; int32_t* row_slot; int32_t* row_pos; int32_t* row_done;
+};
+hipError_t launch_gather_rows(const GatherRowsArgs& a, hipStream_t st);
+
+// dst[act[r]][0 .. V) = src[r][0 .. V) for rows 0 .. R-1 (debug logits by sequence).
+hipError_t launch_scatter_rows(const float* src, const int32_t* act, int R, int V, float* dst, hipStream_t st);
 
 // dst[i] = src[idx[i]]
 hipError_t launch_gather_i32(const int32_t* src, const int32_t* idx, int n, int32_t* dst, hipStream_t st);

@@ -11,6 +11,7 @@
 // sequences of the batch.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -28,6 +29,8 @@ thread_local std::string g_err = "no error";
 
 constexpr int kSplitMax = 16;         // split-K slices of a decode projection
 constexpr int kVocabChunk = 4096;     // vocabulary entries per sampling workgroup
+constexpr int kCompactEvery = 32;     // decode steps between compactions of the batch (EOS runs)
+constexpr int kCompactBucket = 32;    // the launched row count is a multiple of this
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -83,7 +86,7 @@ struct Plan {
   int n_chunks;
   ModelPlan m[2];
   size_t kv_bytes;
-  size_t off_state, off_seq_slot, off_rows, off_prompt, off_partials, off_count;
+  size_t off_state, off_seq_slot, off_rows, off_prompt, off_partials, off_count, off_act, off_drows;
   size_t scratch_bytes;
 };
 
@@ -209,6 +212,8 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
   P.off_prompt = sc; sc = align_up(sc + 2 * S * 4, kAlign);
   P.off_partials = sc; sc = align_up(sc + S * P.n_chunks * 5 * 4, kAlign);
   P.off_count = sc; sc = align_up(sc + 4, kAlign);
+  P.off_act = sc; sc = align_up(sc + S * 4, kAlign);
+  P.off_drows = sc; sc = align_up(sc + 4 * S * 4, kAlign);
   P.scratch_bytes = sc;
   return P;
 }
@@ -237,7 +242,15 @@ struct tandem_handle {
   int n_cu = 256;             // compute units of the device (split-K sizing)
   int32_t *owner, *c, *t, *pos, *pending, *done;
   int32_t* seq_slot;
-  int32_t *row_slot, *row_pos, *row_tok, *row_src;
+  int32_t *row_slot, *row_pos, *row_tok, *row_src;      // prompt rows
+  // Decode rows: row r carries sequence act[r].  After a prefill act is the
+  // identity; with EOS on, a stable partition (unfinished first) runs every
+  // kCompactEvery steps and the launched row count shrinks to the smallest
+  // multiple of kCompactBucket that covers the unfinished sequences.
+  int32_t* act;
+  int32_t *drow_tok, *drow_slot, *drow_pos, *drow_done;
+  int R_launch = 0;
+  int steps_since_compact = 0;
   int32_t *p_end, *p_len;
   float* partials;
   int32_t* d_count;
@@ -504,10 +517,15 @@ tandem_status forward_pair(tandem_handle* h, int R, const int32_t* row_tok, cons
 
 // Enqueue one decode step (both forwards, sampling, outputs, handoff rule).
 tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg) {
-  const int R = h->n_seq;
+  const int R = h->R_launch;
   hipStream_t st = h->stream;
   {
-    tandem_status s = forward_pair(h, R, h->pending, h->seq_slot, h->pos, h->done, true);
+    GatherRowsArgs ga{};
+    ga.act = h->act; ga.R = R;
+    ga.pending = h->pending; ga.seq_slot = h->seq_slot; ga.pos = h->pos; ga.done = h->done;
+    ga.row_tok = h->drow_tok; ga.row_slot = h->drow_slot; ga.row_pos = h->drow_pos; ga.row_done = h->drow_done;
+    TIMED(TANDEM_K_OTHER, launch_gather_rows(ga, st));
+    tandem_status s = forward_pair(h, R, h->drow_tok, h->drow_slot, h->drow_pos, h->drow_done, true);
     if (s != TANDEM_OK) return s;
   }
   const int V = h->m[0].cfg.vocab;
@@ -516,17 +534,15 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
   sa.temp = h->smp.temperature; sa.eos_id = h->smp.eos_id;
   sa.eos_bias_sen = h->smp.eos_bias_senior; sa.eos_bias_jun = h->smp.eos_bias_junior;
   sa.key0 = h->key0; sa.key1 = h->key1;
-  sa.owner = h->owner; sa.t = h->t; sa.done = h->done;
+  sa.owner = h->owner; sa.t = h->t; sa.done = h->done; sa.act = h->act;
   sa.partials = h->partials; sa.chunk = kVocabChunk;
   TIMED(TANDEM_K_SAMPLE, launch_sample_partials(sa, h->plan.n_chunks, st));
   if (dbg) {
-    if (dbg->logits_senior)
-      HIPCHK(hipMemcpyAsync(dbg->logits_senior, h->m[0].logits, (size_t)R * V * 4, hipMemcpyDeviceToDevice, st));
-    if (dbg->logits_junior)
-      HIPCHK(hipMemcpyAsync(dbg->logits_junior, h->m[1].logits, (size_t)R * V * 4, hipMemcpyDeviceToDevice, st));
+    if (dbg->logits_senior) HIPCHK(launch_scatter_rows(h->m[0].logits, h->act, R, V, dbg->logits_senior, st));
+    if (dbg->logits_junior) HIPCHK(launch_scatter_rows(h->m[1].logits, h->act, R, V, dbg->logits_junior, st));
   }
   FinishArgs fa{};
-  fa.z_sen = h->m[0].logits; fa.R = R; fa.V = V;
+  fa.z_sen = h->m[0].logits; fa.R = R; fa.V = V; fa.act = h->act;
   fa.temp = h->smp.temperature; fa.eos_id = h->smp.eos_id; fa.eos_bias_sen = h->smp.eos_bias_senior;
   fa.partials = h->partials; fa.n_chunks = h->plan.n_chunks;
   fa.forced = forced;
@@ -537,6 +553,26 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
   fa.out_len = h->out.length; fa.ld_out = h->smp.max_new_tokens;
   fa.dbg_sampled = dbg ? dbg->sampled : nullptr; fa.dbg_margin = dbg ? dbg->margin : nullptr;
   TIMED(TANDEM_K_SAMPLE, launch_sample_finish(fa, st));
+  return TANDEM_OK;
+}
+
+// With EOS on, sequences finish at different steps: every kCompactEvery steps
+// partition the batch (unfinished sequences first, stable) and shrink the
+// launched row count.  One host synchronisation per compaction.
+tandem_status maybe_compact(tandem_handle* h) {
+  if (h->smp.eos_id < 0 || ++h->steps_since_compact < kCompactEvery) return TANDEM_OK;
+  h->steps_since_compact = 0;
+  hipStream_t st = h->stream;
+  HIPCHK(launch_compact(h->done, h->n_seq, h->act, h->d_count, st));
+  HIPCHK(hipMemcpyAsync(h->h_count, h->d_count, 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipStreamSynchronize(st));
+  const int n_act = *h->h_count;
+  int R = (std::max(n_act, 1) + kCompactBucket - 1) / kCompactBucket * kCompactBucket;
+  if (R > h->n_seq) R = h->n_seq;
+  if (R < h->R_launch) {
+    h->R_launch = R;
+    drop_graphs(h);                   // captured for the old row count
+  }
   return TANDEM_OK;
 }
 
@@ -566,7 +602,11 @@ tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_de
   if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
   if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
   if (!h->prefilled) return fail(&h->err, TANDEM_E_STATE, "tandem_step before tandem_prefill");
-  const int R = h->n_seq;
+  {
+    tandem_status s = maybe_compact(h);
+    if (s != TANDEM_OK) return s;
+  }
+  const int R = h->R_launch;
   hipStream_t st = h->stream;
   const bool timed = (h->timing & ((1 << TANDEM_K_CLASSES) - 1)) != 0;
   const bool graph = !forced && !dbg && !timed && !(h->timing & TANDEM_TIMING_EAGER);
@@ -591,7 +631,7 @@ tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_de
     if (s != TANDEM_OK) return s;
   }
   if (n_active) {
-    HIPCHK(launch_count_active(h->done, R, h->d_count, st));
+    HIPCHK(launch_count_active(h->done, h->n_seq, h->d_count, st));
     HIPCHK(hipMemcpyAsync(h->h_count, h->d_count, 4, hipMemcpyDeviceToHost, st));
     HIPCHK(hipStreamSynchronize(st));
     *n_active = *h->h_count;
@@ -738,6 +778,9 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   h->p_end = pr; h->p_len = pr + S;
   h->partials = (float*)(sc + P.off_partials);
   h->d_count = (int32_t*)(sc + P.off_count);
+  h->act = (int32_t*)(sc + P.off_act);
+  int32_t* drows = (int32_t*)(sc + P.off_drows);
+  h->drow_tok = drows; h->drow_slot = drows + S; h->drow_pos = drows + 2 * S; h->drow_done = drows + 3 * S;
   h->h_count = nullptr;
 
   // --- HIP work from here on
@@ -909,7 +952,10 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
   is.owner = h->owner; is.c = h->c; is.t = h->t; is.pos = h->pos; is.pending = h->pending; is.done = h->done;
   is.out_len = h->out.length;
   HIPCHK(launch_init_state(is, st));
+  HIPCHK(hipMemcpyAsync(h->act, h->seq_slot, (size_t)n_seq * 4, hipMemcpyDeviceToDevice, st));   // identity
   h->n_seq = n_seq;
+  h->R_launch = n_seq;
+  h->steps_since_compact = 0;
   h->prefilled = true;
   return TANDEM_OK;
 }

@@ -153,3 +153,21 @@ def test_step_graph_replays_match_eager_steps():
     for a, b in zip(*states):
         for k in a:
             np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+
+
+def test_eos_compaction_shrinks_the_batch():
+    """EOS-terminated rows are partitioned out of the batch every 32 steps and
+    the launched row count shrinks in 32-row buckets; every sequence, wherever
+    compaction moves it, still matches the oracle (teacher-forced)."""
+    P.log("case EOS compaction: small shapes 2+1 layers, 3 prompts x G=32 = 96 rows, ragged 40..60, strong EOS bias")
+    wl = _small_reduced()
+    wl.n_prompts, wl.group, wl.prompt_len = 3, 32, 60
+    wl.sample.max_new = 80
+    wl.sample.eos_id = wl.senior.vocab - 1
+    wl.sample.eos_bias_senior = wl.sample.eos_bias_junior = 7.5
+    p = P.run(wl, logits_at=(1, 40, 80), max_prefill_tokens=256)
+    ended = p.ref.length < wl.sample.max_new
+    assert ended.mean() > 0.5, "most sequences should end early"
+    # by step 64 (the second compaction) fewer than 64 sequences are alive
+    assert (p.ref.length > 64).sum() < 64
+    P.check(p, P.TOL_BF16)
