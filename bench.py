@@ -46,6 +46,8 @@ DESCRIPTIONS = {
     "small": "8-layer d=1024 senior + 4-layer d=512 junior, bf16, 8 prompts x G=8, prompt 128, 512 new tokens, switch p=0.1",
     "wide": "small shapes, 64 prompts x G=16 = 1024 sequences, prompt 256, 4096 new tokens, switch p=0.5",
     "tiny": "2-layer d=128 senior + 1-layer d=64 junior, fp32, 1 prompt x G=4, 32 new tokens",
+    "longcot": "small shapes, 32 prompts x G=8 = 256 sequences, ragged prompts 64..512, up to 8192 new tokens, "
+               "EOS bias for mean length 4000, ownership switch p=0.3 per 32-token chunk, finished sequences compacted",
 }
 
 
@@ -67,10 +69,21 @@ def weight_bytes(s: W.ModelShape) -> int:
     return esz * (body + d * s.vocab)
 
 
-def decode_step_bytes(wl: W.Workload, plens, t: int) -> int:
-    """Bytes the decode step t must move: both models' weights once, every row's
-    K/V context for both models, the K/V append and the embedding rows."""
-    rows = [p for p in plens for _ in range(wl.group)]
+def _active(plens, group, lengths, t):
+    """Prompt length of every sequence still generating at decode step t
+    (lengths: tokens each sequence generated; None: all run every step)."""
+    rows = [p for p in plens for _ in range(group)]
+    if lengths is None:
+        return rows
+    return [P for P, n in zip(rows, lengths) if t <= n]
+
+
+def decode_step_bytes(wl: W.Workload, plens, t: int, lengths=None) -> int:
+    """Bytes the decode step t must move: both models' weights once, every active
+    row's K/V context for both models, the K/V append and the embedding rows."""
+    rows = _active(plens, wl.group, lengths, t)
+    if not rows:
+        return 0
     kv = kv_bytes_per_token(wl.senior) + kv_bytes_per_token(wl.junior)
     esz_s = 2 if wl.senior.dtype == "bf16" else 4
     esz_j = 2 if wl.junior.dtype == "bf16" else 4
@@ -79,11 +92,10 @@ def decode_step_bytes(wl: W.Workload, plens, t: int) -> int:
             + len(rows) * (esz_s * wl.senior.d_model + esz_j * wl.junior.d_model))
 
 
-def attention_bytes(wl: W.Workload, plens, steps: int) -> int:
+def attention_bytes(wl: W.Workload, plens, steps: int, lengths=None) -> int:
     """K/V bytes the decode attention kernels read over `steps` decode steps."""
-    rows = [p for p in plens for _ in range(wl.group)]
     kv = kv_bytes_per_token(wl.senior) + kv_bytes_per_token(wl.junior)
-    return sum(kv * (P + t - 1) for P in rows for t in range(1, steps + 1))
+    return sum(kv * (P + t - 1) for t in range(1, steps + 1) for P in _active(plens, wl.group, lengths, t))
 
 
 def prefill_flops(wl: W.Workload, plens) -> float:
@@ -210,12 +222,15 @@ def main():
     wall = time.perf_counter() - t_start
 
     out = eng.outputs()
-    senior_share = float(out["owner"][:, :L].mean())
-    toks = n * L * args.steps
+    lengths = out["length"].tolist() if wl.sample.eos_id >= 0 else None     # every run of this batch is identical
+    gen = int(out["length"].sum())
+    mask = np.arange(L)[None, :] < out["length"][:, None]
+    senior_share = float(out["owner"][:, :L][mask].mean())
+    toks = gen * args.steps
     ms_per_step = wall * 1e3 / args.steps
     value = toks / wall
     dec_s = sum(dec) / 1e3
-    dec_bytes = sum(decode_step_bytes(wl, plens, t) for t in range(1, L + 1)) * args.steps
+    dec_bytes = sum(decode_step_bytes(wl, plens, t, lengths) for t in range(1, L + 1)) * args.steps
     pf = prefill_flops(wl, plens)
     pre_ms = float(np.mean(pre))
 
@@ -229,7 +244,7 @@ def main():
 
     def roofline_of(att, method):
         ms, nl = att
-        nbytes = attention_bytes(wl, plens, L)
+        nbytes = attention_bytes(wl, plens, L, lengths)
         gbs = nbytes / (ms / 1e3) / 1e9
         per = nbytes / max(nl, 1)
         return {"bound": "hbm", "kernel": "decode attention (both models)", "achieved": round(gbs, 1),
@@ -270,13 +285,15 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if wl.senior.dtype == "bf16" else "f32",
         "data": "synthetic",
-        "config": {"workload": DESCRIPTIONS[wl.name], "name": wl.name, "rows": n, "prompt_len": plens[0],
+        "config": {"workload": DESCRIPTIONS[wl.name], "name": wl.name, "rows": n,
+                   "prompt_len": plens[0] if min(plens) == max(plens) else [min(plens), max(plens)],
                    "max_new": L, "senior_layers": wl.senior.n_layers, "junior_layers": wl.junior.n_layers,
                    "vocab": wl.senior.vocab},
         "roofline": roof,
         "roofline_concurrent": roof_conc,
         "cpu_baseline": cpu,
-        "decode_tokens_per_s": round(n * L * args.steps / dec_s, 2),
+        "decode_tokens_per_s": round(gen * args.steps / dec_s, 2),
+        "generated_tokens": gen,
         "decode_ms_per_token_step": round(sum(dec) / (L * args.steps), 4),
         "decode_hbm_gbs": round(dec_bytes / dec_s / 1e9, 1),
         "decode_hbm_frac": round(dec_bytes / dec_s / 1e9 / HBM_PEAK_GBS, 4),

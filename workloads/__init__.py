@@ -132,10 +132,13 @@ def workload(name: str) -> Workload:
                         SwitchSettings(SWITCH, 0.1, -1, "all", SENIOR),
                         SampleSettings(1.0, -1, 0.0, 0.0, 2048), 3)
     if name == "longcot":
+        # EOS biases: per-model logit bias giving a mean EOS probability of
+        # 1/4000 per step (geometric stop lengths of mean 4000), from
+        # oracle/calibrate_eos.py (senior 2.2608, junior 2.0414)
         sen, jun = _small_pair()
         return Workload("longcot", sen, jun, 32, 8, 512, 64,
                         SwitchSettings(SWITCH, 0.3, 31, "none", SENIOR),
-                        SampleSettings(1.0, 31999, 0.0, 0.0, 8192), 4)
+                        SampleSettings(1.0, 31999, 2.2608, 2.0414, 8192), 4)
     if name == "wide":
         sen, jun = _small_pair()
         return Workload("wide", sen, jun, 64, 16, 256, None,
