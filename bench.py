@@ -119,7 +119,8 @@ def measured_traffic_ratio():
     on a different version of the kernel source."""
     import hashlib
     try:
-        d = json.loads(open(TRAFFIC_FILE).read().split("\n\n", 1)[1])
+        txt = open(TRAFFIC_FILE).read()
+        d = json.loads(txt[txt.index("\n{") + 1:])
         src = os.path.join(ROOT, "paper_2606_28166_amd", "csrc", "k_attn.hip")
         digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
         if d["kernel_source_sha256_16"] != digest:
