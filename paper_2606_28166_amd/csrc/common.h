@@ -53,6 +53,19 @@ __device__ __forceinline__ float split_load(const bf16_t* row, int k) {
   return bf2f(p[0]) + bf2f(p[8]);
 }
 
+// ------------------------------------------------------------ fp16 format
+// The inputs of the FFN projections and the LM head at decode are plain
+// fp16 (one rounding, 2^-11 relative; the two-part split is kept where the
+// attention consumes the result): 2 bytes per value and one MFMA per
+// fragment.  Values are saturated to the fp16 range.
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ uint16_t f2h(float x) {
+  return __builtin_bit_cast(uint16_t, (_Float16)fminf(fmaxf(x, -65504.f), 65504.f));
+}
+
+// Activation formats written by the norm passes.
+enum { ACT_F32 = 0, ACT_SPLIT = 1, ACT_F16 = 2 };
+
 // Activation row store in either format (split for bf16 models, plain fp32 otherwise).
 template <bool SPLIT>
 __device__ __forceinline__ void act_store(void* base, size_t row, int K, int k, float x) {

@@ -19,12 +19,18 @@ constexpr int kSplitMaxDev = 16;   // split-K slices a consumer sums (>= the hos
 // order s = 0..S-1), so a row costs one memory round trip, not S.
 constexpr int kMaxV4 = 8;          // d_model <= 8192
 
-template <bool SPLIT>
+template <int FMT>
 __device__ __forceinline__ void norm_store(void* x, int r, int d, int i4, float4 v, float rs, const float* gain) {
   const float4 gg = *reinterpret_cast<const float4*>(gain + 4 * i4);
   const float y[4] = {v.x * rs * gg.x, v.y * rs * gg.y, v.z * rs * gg.z, v.w * rs * gg.w};
+  if (FMT == ACT_F16) {
+    const uint2 w = make_uint2((uint32_t)f2h(y[0]) | ((uint32_t)f2h(y[1]) << 16),
+                               (uint32_t)f2h(y[2]) | ((uint32_t)f2h(y[3]) << 16));
+    reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(x) + (size_t)r * d)[i4] = w;
+    return;
+  }
 #pragma unroll
-  for (int e = 0; e < 4; ++e) act_store<SPLIT>(x, r, d, 4 * i4 + e, y[e]);
+  for (int e = 0; e < 4; ++e) act_store<FMT == ACT_SPLIT>(x, r, d, 4 * i4 + e, y[e]);
 }
 
 template <typename WT, bool SPLIT>
@@ -54,12 +60,12 @@ __global__ __launch_bounds__(kNT) void embed_norm_kernel(const int32_t* __restri
     const int i4 = tid + k * kNT;
     if (i4 < n4) {
       reinterpret_cast<float4*>(h + (size_t)r * d)[i4] = v[k];
-      norm_store<SPLIT>(x, r, d, i4, v[k], rs, gain);
+      norm_store<SPLIT ? ACT_SPLIT : ACT_F32>(x, r, d, i4, v[k], rs, gain);
     }
   }
 }
 
-template <bool SPLIT>
+template <int FMT>
 __global__ __launch_bounds__(kNT) void resid_norm_kernel(const float* __restrict__ ws, int S,
                                                          long ws_stride, float* __restrict__ h,
                                                          const float* __restrict__ gain, float eps,
@@ -94,7 +100,7 @@ __global__ __launch_bounds__(kNT) void resid_norm_kernel(const float* __restrict
     const int i4 = tid + k * kNT;
     if (i4 < n4) {
       hrow[i4] = v[k];
-      norm_store<SPLIT>(x, r, d, i4, v[k], rs, gain);
+      norm_store<FMT>(x, r, d, i4, v[k], rs, gain);
     }
   }
 }
@@ -102,7 +108,8 @@ __global__ __launch_bounds__(kNT) void resid_norm_kernel(const float* __restrict
 // ------------------------------------------------------------ SwiGLU finish
 // One thread per 8 consecutive outputs of a row (one split-format piece).
 __global__ __launch_bounds__(kNT) void swiglu_finish_kernel(const float* __restrict__ ws, int S, long ws_stride,
-                                                            int M, int ffn, int interleaved, bf16_t* __restrict__ out) {
+                                                            int M, int ffn, int interleaved, int f16_out,
+                                                            bf16_t* __restrict__ out) {
   const long e = (long)blockIdx.x * kNT + threadIdx.x;
   const int np = ffn / 8;
   if (e >= (long)M * np) return;
@@ -126,6 +133,16 @@ __global__ __launch_bounds__(kNT) void swiglu_finish_kernel(const float* __restr
       u[4] += u1.x; u[5] += u1.y; u[6] += u1.z; u[7] += u1.w;
     }
   uint32_t hw[4], lw[4];
+  if (f16_out) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float y0 = g[2 * i] / (1.f + expf(-g[2 * i])) * u[2 * i];
+      const float y1 = g[2 * i + 1] / (1.f + expf(-g[2 * i + 1])) * u[2 * i + 1];
+      hw[i] = (uint32_t)f2h(y0) | ((uint32_t)f2h(y1) << 16);
+    }
+    reinterpret_cast<uint4*>(out + (size_t)m * ffn)[p] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const float y0 = g[2 * i] / (1.f + expf(-g[2 * i])) * u[2 * i];
@@ -497,24 +514,26 @@ hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, c
   return hipGetLastError();
 }
 
-hipError_t launch_swiglu_finish(const float* ws, int S, long ws_stride, int M, int ffn, bool interleaved, void* out,
-                                hipStream_t st) {
+hipError_t launch_swiglu_finish(const float* ws, int S, long ws_stride, int M, int ffn, bool interleaved, bool f16_out,
+                                void* out, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (S > kSplitMaxDev || ffn % (interleaved ? 16 : 8)) return hipErrorInvalidValue;
   const long n = (long)M * (ffn / 8);
   hipLaunchKernelGGL(swiglu_finish_kernel, dim3((unsigned)((n + kNT - 1) / kNT)), dim3(kNT), 0, st, ws, S, ws_stride,
-                     M, ffn, interleaved ? 1 : 0, (bf16_t*)out);
+                     M, ffn, interleaved ? 1 : 0, f16_out ? 1 : 0, (bf16_t*)out);
   return hipGetLastError();
 }
 
 hipError_t launch_resid_norm(int dt, const float* ws, int S, long ws_stride, float* h, const float* gain,
-                             float eps, void* x, int R, int d, hipStream_t st) {
+                             float eps, void* x, int R, int d, bool f16_out, hipStream_t st) {
   if (R <= 0) return hipSuccess;
-  if (S > kSplitMaxDev) return hipErrorInvalidValue;
-  if (dt == DT_BF16)
-    hipLaunchKernelGGL((resid_norm_kernel<true>), dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
+  if (S > kSplitMaxDev || (f16_out && dt != DT_BF16)) return hipErrorInvalidValue;
+  if (f16_out)
+    hipLaunchKernelGGL((resid_norm_kernel<ACT_F16>), dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
+  else if (dt == DT_BF16)
+    hipLaunchKernelGGL((resid_norm_kernel<ACT_SPLIT>), dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
   else
-    hipLaunchKernelGGL((resid_norm_kernel<false>), dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
+    hipLaunchKernelGGL((resid_norm_kernel<ACT_F32>), dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
   return hipGetLastError();
 }
 

@@ -13,14 +13,20 @@
 //     straight into VGPRs, NS - 1 chunks ahead of the arithmetic (512 KB of
 //     register file per compute unit holds far more bytes in flight than the
 //     160 KB of LDS).
-//   * The activations (split format: bf16 high and low parts, so the product
-//     keeps fp32-level inputs) are the operand every wave shares; they stream
+//   * The activations are the operand every wave shares; they stream
 //     through an NS-stage LDS ring by direct global->LDS loads, XOR-swizzled
-//     so the fragment reads are free of bank conflicts.
-// A workgroup is 4 waves, one per SIMD.  Wave w owns NBW 32-row weight blocks
-// and all MB 32-row activation blocks, so each A fragment read from LDS feeds
-// 2 * NBW MFMAs.  The work is a list of items (a group of 128 * NBW weight
-// rows x one K slice); the grid is at most one workgroup per compute unit
+//     so the fragment reads are free of bank conflicts.  They come in one of
+//     two formats: split (bf16 high and low parts, two MFMAs per fragment,
+//     fp32-level inputs: QKV and O, whose results feed the attention) or
+//     fp16 (one MFMA per fragment against an fp16 copy of the weights: the
+//     FFN and the LM head).  Every activation byte delivered to the CU is
+//     traffic beside the weight stream: at 128 rows the split tile is twice
+//     the bytes of its weights, the fp16 tile as many, which is most of the
+//     difference in speed between the two.
+// A workgroup is 4 waves, one per SIMD.  Wave w owns 32-row weight block w
+// of the item and all MB 32-row activation blocks.  The work is a list of
+// items (a group of 128 weight rows x one K slice); the grid is at most one
+// workgroup per compute unit
 // and each workgroup walks its items as one continuous chunk stream, so the
 // prefetch runs on across item boundaries.  K slices > 1 write split-K
 // partial tiles that the consuming kernel sums in a fixed order.
@@ -45,7 +51,7 @@ constexpr int SNW = 4;             // waves per workgroup
 // in its last 16, so one MFMA output tile holds both halves of 16 SwiGLU
 // outputs.
 __global__ __launch_bounds__(256) void pack_weights_kernel(const bf16_t* __restrict__ W, int N, int K, int pair_rows,
-                                                           bf16_t* __restrict__ out, long n_pieces) {
+                                                           int to_f16, bf16_t* __restrict__ out, long n_pieces) {
   const int ksn = K / 16;
   for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_pieces; i += (long)gridDim.x * blockDim.x) {
     const long f = i >> 6;                        // fragment = (32-row block, 16-k step)
@@ -57,26 +63,40 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const bf16_t* __restr
     const int k = 16 * ks + 8 * (lane >> 5);
     uint4 v = make_uint4(0u, 0u, 0u, 0u);
     if (row < N) v = *reinterpret_cast<const uint4*>(W + row * (long)K + k);
+    if (to_f16) {
+      uint32_t* w = reinterpret_cast<uint32_t*>(&v);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint16_t lo = __builtin_bit_cast(uint16_t, (_Float16)bf2f((bf16_t)(w[e] & 0xFFFFu)));
+        const uint16_t hi = __builtin_bit_cast(uint16_t, (_Float16)bf2f((bf16_t)(w[e] >> 16)));
+        w[e] = (uint32_t)lo | ((uint32_t)hi << 16);
+      }
+    }
     reinterpret_cast<uint4*>(out)[i] = v;
   }
 }
 
-// Two prefetch distances: weights (from HBM) are loaded NS - 1 chunks ahead
-// into a ring of NS register sets; activations (L2-resident) one chunk ahead
-// into a 2-stage LDS ring.  Iteration c issues A(c + 1) then W(c + NS - 1);
-// loads retire in order, so waiting for A(c) (vmcnt <= the NWL weight loads
-// issued after it) also covers W(c), issued earlier.
-template <int MB, int NBW, int NS>
+// Both operands are loaded NS - 1 chunks ahead of the arithmetic: weights
+// (from HBM) into a ring of NS register sets, activations (L2-resident) into
+// an NS-stage LDS ring.  Iteration c issues A(c + NS - 1) then W(c + NS - 1).
+// Vector loads retire in order, so the two rings must be equally deep: a
+// wait for an activation stage also waits for every weight load issued
+// before it.
+template <int MB, int NS, bool A16>
 struct StreamShape {
   static constexpr int BM = 32 * MB;                 // activation rows of the tile
-  static constexpr int ASTAGE = BM * SBK * 4;        // bytes of one activation stage (hi + lo)
-  static constexpr int NA = BM / (4 * SNW);          // activation DMA instructions per wave per chunk
-  static constexpr int NWL = 4 * NBW;                // weight loads per wave per chunk
-  static constexpr int DW = NS - 1;                  // weight chunks in flight ahead of the arithmetic
-  static constexpr int WAIT = NWL;                   // vmcnt once A(c) (and so W(c)) has landed
-  static constexpr int COLS = SNW * NBW * 32;        // weight rows per item
-  static_assert(NS >= 2 && NS % 2 == 0, "ring of register sets (even: the LDS stage is c % 2)");
-  static_assert(2 * ASTAGE <= 160 * 1024, "LDS ring");
+  static constexpr int PARTS = A16 ? 1 : 2;          // MFMA operand parts per value (fp16, or bf16 hi + lo)
+  static constexpr int RB = SBK * 2 * PARTS;         // bytes of one activation row per chunk
+  static constexpr int NPC = RB / 16;                // 16-byte pieces per row (XOR-swizzled)
+  static constexpr int RPI = 64 / NPC;               // rows per 1 KB DMA instruction
+  static constexpr int ASTAGE = BM * RB;             // bytes of one activation stage
+  static constexpr int NA = BM / (RPI * SNW);        // activation DMA instructions per wave per chunk
+  static constexpr int NWL = 4;                      // weight loads per wave per chunk
+  static constexpr int DW = NS - 1;                  // chunks in flight ahead of the arithmetic
+  static constexpr int WAIT = (DW - 1) * (NA + NWL); // vmcnt once A(c) and W(c) have landed
+  static_assert(NS >= 2, "ring of register sets and LDS stages");
+  static_assert(NS * ASTAGE <= 160 * 1024, "LDS ring");
+  static_assert(WAIT < 64, "vmcnt range");
   static_assert(NA >= 1, "at least one activation DMA per wave");
 };
 
@@ -88,12 +108,13 @@ struct Cursor {
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); }
 
-template <int MB, int NBW, int NS, int EPI>
+template <int MB, int NS, bool A16, int EPI>
 __global__ __launch_bounds__(256) void gemm_stream_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ Wp, int M, int N, int K, int n_groups, int S, int cps,
     float* __restrict__ out, int ldo, long split_stride) {
-  using G = StreamShape<MB, NBW, NS>;
-  __shared__ __attribute__((aligned(1024))) unsigned char ring[2 * G::ASTAGE];
+  using G = StreamShape<MB, NS, A16>;
+  constexpr int PARTS = G::PARTS, NPC = G::NPC;
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[NS * G::ASTAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, c32 = lane & 31;
@@ -117,92 +138,89 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(
     if (u.item + grid < n_items) set_item(u, u.item + grid);
   };
 
-  // Activation DMA: instruction i of wave w covers tile rows r0 + 16 i .. +4
-  // (r0 = 4 w + lane / 16; 256 B per row: 8 hi pieces and 8 lo pieces);
-  // physical piece lane & 15 holds logical piece (lane & 15) ^ (row & 15).
-  const int r0 = 4 * wave + (lane >> 4);
-  const int lc = (lane & 15) ^ (r0 & 15);
+  // Activation DMA: instruction i of wave w covers tile rows
+  // r0 + RPI SNW i .. +RPI - 1 (r0 = RPI w + lane / NPC; a row is NPC 16-byte
+  // pieces: split format 8 hi and 8 lo pieces, fp16 8 pieces); physical piece
+  // lane % NPC holds logical piece (lane % NPC) ^ (row % NPC).
+  const int r0 = G::RPI * wave + lane / NPC;
+  const int lc = (lane % NPC) ^ (r0 % NPC);
+  const size_t lda = (size_t)K * PARTS;                    // row stride (2-byte elements)
   const __amdgpu_buffer_rsrc_t wr = buf_rsrc(Wp, (uint32_t)((size_t)nblk * (K / 16) * 1024));
   const int kfr = K / 16;                                  // fragments per 32-row block
 
-  u32x4_t wb[NS][NBW][4];
+  u32x4_t wb[NS][4];
   auto issue_a = [&](const Cursor& u, int stage) {
     const int kc = u.s * cps + u.c;
     unsigned char* st = ring + stage * G::ASTAGE;
 #pragma unroll
     for (int i = 0; i < G::NA; ++i) {
-      const bf16_t* src = A + (size_t)min(r0 + 16 * i, M - 1) * 2 * (size_t)K + (size_t)kc * 2 * SBK + lc * 8;
+      const bf16_t* src = A + (size_t)min(r0 + G::RPI * SNW * i, M - 1) * lda + (size_t)kc * PARTS * SBK + lc * 8;
       load_lds16(src, st + 4 * (SNW * i + wave) * 256);
     }
   };
-  auto issue_w = [&](const Cursor& u, u32x4_t (&w)[NBW][4]) {
+  auto issue_w = [&](const Cursor& u, u32x4_t (&w)[4]) {
     const int kc = u.s * cps + u.c;
+    const int nb = min(u.grp * SNW + wave, nblk - 1);
+    const int base = (nb * kfr + 4 * kc) * 1024 + lane * 16;
 #pragma unroll
-    for (int b = 0; b < NBW; ++b) {
-      const int nb = min(u.grp * (SNW * NBW) + wave * NBW + b, nblk - 1);
-      const int base = (nb * kfr + 4 * kc) * 1024 + lane * 16;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) w[b][j] = buf_load16_nt(wr, base + j * 1024, 0);
-    }
+    for (int j = 0; j < 4; ++j) w[j] = buf_load16_nt(wr, base + j * 1024, 0);
   };
   // keeps the loads issued so far above the arithmetic of this chunk and
   // makes the compiler wait for this chunk's weights here, not earlier
-  auto pin = [&](u32x4_t (&w)[NBW][4]) {
+  auto pin = [&](u32x4_t (&w)[4]) {
 #pragma unroll
-    for (int b = 0; b < NBW; ++b)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(w[b][j]) : : "memory");
+    for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(w[j]) : : "memory");
   };
 
-  f32x16_t acc[MB][NBW];
+  f32x16_t acc[MB];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int b = 0; b < NBW; ++b) acc[mb][b] = f32x16_t{};
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x16_t{};
 
   const uint32_t ring_addr = lds_addr_of(ring);
-  // A fragments of k-step j (k-values 16 j + 8 g .. +7 of the chunk = group 2 j + g)
-  auto read_a = [&](uint32_t st, int j, u32x4_t (&f)[MB][2]) {
+  // A fragments of k-step j (k-values 16 j + 8 g .. +7 of the chunk = group 2 j + g:
+  // pieces 2 q and 2 q + 1 of a split row, piece q of an fp16 row)
+  auto read_a = [&](uint32_t st, int j, u32x4_t (&f)[MB][PARTS]) {
     const int q = 2 * j + g;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       const int r = mb * 32 + c32;
-      const uint32_t row = st + (uint32_t)(r * 256);
-      f[mb][0] = lds_read16(row + (uint32_t)(((2 * q) ^ (r & 15)) * 16));
-      f[mb][1] = lds_read16(row + (uint32_t)(((2 * q + 1) ^ (r & 15)) * 16));
+      const uint32_t row = st + (uint32_t)(r * G::RB);
+#pragma unroll
+      for (int part = 0; part < PARTS; ++part)
+        f[mb][part] = lds_read16(row + (uint32_t)(((PARTS * q + part) ^ (r % NPC)) * 16));
     }
   };
-  auto fence_a = [&](u32x4_t (&f)[MB][2]) {
+  auto fence_a = [&](u32x4_t (&f)[MB][PARTS]) {
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      lds_fence_value(f[mb][0]);
-      lds_fence_value(f[mb][1]);
-    }
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int part = 0; part < PARTS; ++part) lds_fence_value(f[mb][part]);
   };
   // one chunk = 4 k-steps; the A fragments of k-step j + 1 are read while the
-  // MFMAs of k-step j run (high parts of every block, then low parts, so
-  // consecutive MFMAs never share an accumulator when MB * NBW > 1)
-  auto compute = [&](int stage, u32x4_t (&w)[NBW][4]) {
+  // MFMAs of k-step j run (split format: high parts of every block, then low
+  // parts, so consecutive MFMAs never share an accumulator when MB > 1)
+  auto compute = [&](int stage, u32x4_t (&w)[4]) {
     const uint32_t st = ring_addr + (uint32_t)(stage * G::ASTAGE);
-    u32x4_t fa[MB][2], fb[MB][2];
+    u32x4_t fa[MB][PARTS], fb[MB][PARTS];
     read_a(st, 0, fa);
     pin(w);
     lds_wait();
     fence_a(fa);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      u32x4_t (&cur)[MB][2] = (j & 1) ? fb : fa;
-      u32x4_t (&nxt)[MB][2] = (j & 1) ? fa : fb;
+      u32x4_t (&cur)[MB][PARTS] = (j & 1) ? fb : fa;
+      u32x4_t (&nxt)[MB][PARTS] = (j & 1) ? fa : fb;
       if (j < 3) read_a(st, j + 1, nxt);
 #pragma unroll
-      for (int part = 0; part < 2; ++part)
+      for (int part = 0; part < PARTS; ++part)
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
-          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, cur[mb][part]);
-#pragma unroll
-          for (int b = 0; b < NBW; ++b)
-            acc[mb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, w[b][j]),
-                                                                 acc[mb][b], 0, 0, 0);
+          if (A16)
+            acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, cur[mb][part]),
+                                                             __builtin_bit_cast(f16x8_t, w[j]), acc[mb], 0, 0, 0);
+          else
+            acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, cur[mb][part]),
+                                                              __builtin_bit_cast(bf16x8_t, w[j]), acc[mb], 0, 0, 0);
         }
       if (j < 3) {
         lds_wait();
@@ -211,54 +229,49 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(
     }
   };
   auto epilogue = [&](const Cursor& u) {
+    const int nb = u.grp * SNW + wave;                   // this wave's 32-row weight block
     if (EPI == EPI_SWIGLU) {
       // columns c < 16 of a block are gate sums, c + 16 the matching up sums
-      // (pair-interleaved packing); output column 16 nb + c, split format
+      // (pair-interleaved packing); output column 16 nb + c, in the input's
+      // format (fp16, or split)
+      const int j = nb * 16 + (c32 & 15);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int b = 0; b < NBW; ++b) {
-          const int nb = u.grp * (SNW * NBW) + wave * NBW + b;
-          const int j = nb * 16 + (c32 & 15);
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const float v = acc[mb][b][i];
-            const float up = __shfl_xor(v, 16, 64);
-            const int m = mb * 32 + 8 * (i >> 2) + 4 * g + (i & 3);
-            if (m < M && c32 < 16 && j < ldo)
-              split_store(reinterpret_cast<bf16_t*>(out) + (size_t)m * 2 * ldo, j, silu_f(v) * up);
-            acc[mb][b][i] = 0.f;
+        for (int i = 0; i < 16; ++i) {
+          const float v = acc[mb][i];
+          const float up = __shfl_xor(v, 16, 64);
+          const int m = mb * 32 + 8 * (i >> 2) + 4 * g + (i & 3);
+          if (m < M && c32 < 16 && j < ldo) {
+            if (A16) reinterpret_cast<uint16_t*>(out)[(size_t)m * ldo + j] = f2h(silu_f(v) * up);
+            else split_store(reinterpret_cast<bf16_t*>(out) + (size_t)m * 2 * ldo, j, silu_f(v) * up);
           }
+          acc[mb][i] = 0.f;
         }
       return;
     }
     float* o = out + (size_t)u.s * split_stride;
+    const int n = nb * 32 + c32;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int b = 0; b < NBW; ++b) {
-        const int n = (u.grp * (SNW * NBW) + wave * NBW + b) * 32 + c32;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int m = mb * 32 + 8 * (i >> 2) + 4 * g + (i & 3);
-          if (m < M && n < N) o[(size_t)m * ldo + n] = acc[mb][b][i];
-          acc[mb][b][i] = 0.f;
-        }
+      for (int i = 0; i < 16; ++i) {
+        const int m = mb * 32 + 8 * (i >> 2) + 4 * g + (i & 3);
+        if (m < M && n < N) o[(size_t)m * ldo + n] = acc[mb][i];
+        acc[mb][i] = 0.f;
       }
   };
 
   // Every item's chunk count is a multiple of NS (the host guarantees
   // K % (64 NS) == 0 and cps % NS == 0), so chunk c of an item sits in
-  // register set c % NS and LDS stage c % 2: compile-time indices below.
-  Cursor la, lw, cp;                    // activation / weight load cursors, compute cursor
+  // register set and LDS stage c % NS: compile-time indices below.
+  Cursor la, cp;                        // load cursor (both operands), compute cursor
   set_item(la, blockIdx.x);
-  lw = la;
-  issue_a(la, 0);
-  advance(la);
 #pragma unroll
   for (int d = 0; d < G::DW; ++d) {
-    issue_w(lw, wb[d]);
-    advance(lw);
+    issue_a(la, d);
+    issue_w(la, wb[d]);
+    advance(la);
   }
   for (int item = blockIdx.x; item < n_items; item += grid) {
     set_item(cp, item);
@@ -267,30 +280,33 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(
       for (int u = 0; u < NS; ++u) {
         wait_vmcnt<G::WAIT>();          // A(c) and W(c) of this wave have landed
         lds_wait();                     // and its LDS reads of the previous chunk are done
-        __builtin_amdgcn_s_barrier();   // ... in every wave: A(c) is complete, the other stage is free
-        issue_a(la, (u + 1) & 1);
+        __builtin_amdgcn_s_barrier();   // ... in every wave: A(c) is complete, stage c - 1 is free
+        issue_a(la, (u + G::DW) % NS);
+        issue_w(la, wb[(u + G::DW) % NS]);
         advance(la);
-        issue_w(lw, wb[(u + G::DW) % NS]);
-        advance(lw);
-        compute(u & 1, wb[u]);
+        compute(u, wb[u]);
       }
     }
     epilogue(cp);
   }
 }
 
-template <int MB, int NBW, int EPI>
+template <int MB, bool A16, int EPI>
 hipError_t run_stream(const GemmStreamArgs& a, int grid, hipStream_t st) {
   constexpr int NS = kStreamStages;
-  hipLaunchKernelGGL((gemm_stream_kernel<MB, NBW, NS, EPI>), dim3(grid), dim3(64 * SNW), 0, st,
+  hipLaunchKernelGGL((gemm_stream_kernel<MB, NS, A16, EPI>), dim3(grid), dim3(64 * SNW), 0, st,
                      (const bf16_t*)a.A, (const bf16_t*)a.Wp, a.M, a.N, a.K, a.n_groups, a.S, a.cps, a.out, a.ldo,
                      a.split_stride);
   return hipGetLastError();
 }
 
 template <int MB>
-hipError_t dispatch_nbw(const GemmStreamArgs& a, int grid, hipStream_t st) {
-  return a.epi == EPI_SWIGLU ? run_stream<MB, 1, EPI_SWIGLU>(a, grid, st) : run_stream<MB, 1, EPI_PARTIAL>(a, grid, st);
+hipError_t dispatch_epi(const GemmStreamArgs& a, int grid, hipStream_t st) {
+  if (a.a16)
+    return a.epi == EPI_SWIGLU ? run_stream<MB, true, EPI_SWIGLU>(a, grid, st)
+                               : run_stream<MB, true, EPI_PARTIAL>(a, grid, st);
+  return a.epi == EPI_SWIGLU ? run_stream<MB, false, EPI_SWIGLU>(a, grid, st)
+                             : run_stream<MB, false, EPI_PARTIAL>(a, grid, st);
 }
 
 }  // namespace
@@ -302,12 +318,12 @@ bool stream_gemm_ok(int M, int N, int K) {
          packed_weight_bytes(N, K) < ((size_t)1 << 31);
 }
 
-hipError_t launch_pack_weights(const void* W, int N, int K, int pair_rows, void* out, hipStream_t st) {
+hipError_t launch_pack_weights(const void* W, int N, int K, int pair_rows, bool to_f16, void* out, hipStream_t st) {
   if (pair_rows > 0 && (N != 2 * pair_rows || pair_rows % 16)) return hipErrorInvalidValue;
   const long pieces = (long)((N + 31) / 32) * (K / 16) * 64;
   const long blocks = std::min<long>((pieces + 255) / 256, 65536);
   hipLaunchKernelGGL(pack_weights_kernel, dim3((unsigned)blocks), dim3(256), 0, st, (const bf16_t*)W, N, K, pair_rows,
-                     (bf16_t*)out, pieces);
+                     to_f16 ? 1 : 0, (bf16_t*)out, pieces);
   return hipGetLastError();
 }
 
@@ -349,9 +365,9 @@ hipError_t launch_gemm_stream(const GemmStreamArgs& a, hipStream_t st) {
     return hipErrorInvalidValue;
   if (a.epi == EPI_SWIGLU && (a.S != 1 || a.N % 32)) return hipErrorInvalidValue;
   const int grid = std::min(a.grid, a.n_groups * a.S);
-  if (a.M <= 32) return dispatch_nbw<1>(a, grid, st);
-  if (a.M <= 64) return dispatch_nbw<2>(a, grid, st);
-  return dispatch_nbw<4>(a, grid, st);
+  if (a.M <= 32) return dispatch_epi<1>(a, grid, st);
+  if (a.M <= 64) return dispatch_epi<2>(a, grid, st);
+  return dispatch_epi<4>(a, grid, st);
 }
 
 }  // namespace tandem

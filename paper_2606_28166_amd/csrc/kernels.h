@@ -37,13 +37,16 @@ constexpr int kGemmBK = 64;
 // each, ordered [row block][k step]; lane l of fragment (nb, ks) holds
 // W[32 nb + l % 32][16 ks + 8 (l / 32) .. +7] (rows >= N are zero).
 constexpr int kStreamMaxRows = 128;
-constexpr int kStreamStages = 4;   // weight register sets; K % 256 == 0 and chunks per K slice % 4 == 0
+constexpr int kStreamStages = 4;   // prefetch ring depth (register sets, LDS stages); K % 256 == 0, chunks per K slice % 4 == 0
 constexpr int kSplitMaxStream = 16;  // K slices at most (the consumers sum up to 16 partials)
 size_t packed_weight_bytes(int N, int K);
 bool stream_gemm_ok(int M, int N, int K);
 // pair_rows F > 0: W is a [2F][K] gate/up matrix, packed pair-interleaved (block b =
 // gate rows 16 b .. +15, then up rows F + 16 b .. +15) for the SwiGLU epilogue.
-hipError_t launch_pack_weights(const void* W, int N, int K, int pair_rows, void* out, hipStream_t st);
+// to_f16: the copy holds fp16 values (for fp16 activations; bf16 -> fp16 is
+// exact down to 2^-17 in magnitude, smaller weights round to the fp16
+// subnormal grid, 2^-24).
+hipError_t launch_pack_weights(const void* W, int N, int K, int pair_rows, bool to_f16, void* out, hipStream_t st);
 struct StreamPlan {
   int nbw;                // 32-row weight blocks per wave (1)
   int S;                  // K slices (split-K partial tiles when > 1)
@@ -58,11 +61,13 @@ struct StreamPlan {
 enum { kPlanStore = 0, kPlanPartial = 1, kPlanSwiglu = 2 };
 StreamPlan plan_stream_gemm(int M, int N, int K, int n_cu, size_t ws_floats, int mode);
 struct GemmStreamArgs {
-  const void* A;          // split activations [M][2K] (bf16 hi/lo pieces)
-  const void* Wp;         // packed weights (pair-interleaved for EPI_SWIGLU)
+  const void* A;          // activations: split [M][2K] (bf16 hi/lo pieces), or fp16 [M][K] when a16
+  const void* Wp;         // packed weights (pair-interleaved for EPI_SWIGLU), fp16 values when a16
   int M, N, K;
+  bool a16;               // fp16 activations and weights
   int epi;                // EPI_PARTIAL / EPI_STORE: out + s * split_stride + m * ldo + n;
-                          // EPI_SWIGLU (S = 1): split-format rows of ldo = N / 2 outputs
+                          // EPI_SWIGLU (S = 1): rows of ldo = N / 2 outputs, fp16 when
+                          // a16, split format otherwise
   float* out;
   int ldo;
   long split_stride;
@@ -72,6 +77,8 @@ hipError_t launch_gemm_stream(const GemmStreamArgs& a, hipStream_t st);
 
 // Activations x feeding a GEMM are in split format for bf16 models (see
 // common.h) and plain fp32 for fp32 models; both take 4 bytes per value.
+// The streaming decode GEMMs of the FFN and the LM head take fp16 rows
+// instead (f16_out below: [R][d] of 2-byte values).
 
 // h[r] = E[tok[r]], x[r] = rmsnorm(h[r]) * gain.
 hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, const float* gain,
@@ -80,14 +87,15 @@ hipError_t launch_embed_norm(int dt, const int32_t* tok, const void* E, int d, c
 // h[r] += sum_s ws[s][r] (fixed order), then x[r] = rmsnorm(h[r]) * gain.
 // SwiGLU of split-K gate/up partials: ws[s][m][0 .. ffn) are gate sums,
 // ws[s][m][ffn .. 2 ffn) the matching up sums; out[m] = silu(gate) * up in
-// split format (row stride 2 * ffn bf16).  ffn % 8 == 0.
+// split format (row stride 2 * ffn bf16), or fp16 (row stride ffn) when
+// f16_out.  ffn % 8 == 0.
 // interleaved: the partial columns follow the pair-interleaved packing (gate
 // j at 32 (j / 16) + j % 16, up j 16 columns later).
-hipError_t launch_swiglu_finish(const float* ws, int S, long ws_stride, int M, int ffn, bool interleaved, void* out,
-                                hipStream_t st);
+hipError_t launch_swiglu_finish(const float* ws, int S, long ws_stride, int M, int ffn, bool interleaved, bool f16_out,
+                                void* out, hipStream_t st);
 
 hipError_t launch_resid_norm(int dt, const float* ws, int S, long ws_stride, float* h,
-                             const float* gain, float eps, void* x, int R, int d, hipStream_t st);
+                             const float* gain, float eps, void* x, int R, int d, bool f16_out, hipStream_t st);
 
 struct CacheGeom {
   void* k;                // layer base of the K cache  [slot][kvh][tiled plane of ctx_stride x hd]

@@ -103,8 +103,13 @@ struct Model {
   long layer_stride;          // elements
   long slot_stride;           // elements
   float* h;
-  void* xa;                   // activation rows (split format for bf16 models)
-  void* xf;
+  void* xa;                   // activation rows (split format for bf16 models; fp16 rows for the
+  void* xf;                   // streaming FFN and LM-head products, see ffn16 / lm16)
+  // The FFN projections (gate/up and down) and the LM head take fp16
+  // activations and fp16 packed weights when they run on the streaming
+  // decode GEMM; QKV and O keep the split format, whose precision the
+  // attention (and the bf16-rounded K/V cache behind it) needs.
+  bool ffn16 = false, lm16 = false;
   float* q;
   float* ws;
   float* logits;
@@ -365,19 +370,23 @@ int choose_splits(int M, int N, int K, size_t ws_floats, int n_cu) {
 // copy for decode-sized M, the tiled kernel otherwise.  EPI_PARTIAL writes
 // split-K partial tiles (stride M * N floats) and returns their count in *S;
 // EPI_STORE writes out[m * N + n].
+// A16: the activations are fp16 rows and Wp an fp16 packed copy (only on the
+// streaming path, which the caller's choice of format has already implied).
 tandem_status gemm(tandem_handle* h, const Model& m, const void* A, const void* W, const void* Wp, int M, int N,
-                   int K, int epi, float* out, int* S, hipStream_t st) {
+                   int K, int epi, float* out, int* S, hipStream_t st, bool a16 = false) {
   const int dt = m.cfg.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32;
   *S = 1;
   if (Wp && M <= kStreamMaxRows) {
     const StreamPlan pl = plan_stream_gemm(M, N, K, h->n_cu, m.p.ws_floats, epi == EPI_STORE ? kPlanStore : kPlanPartial);
     GemmStreamArgs a{};
-    a.A = A; a.Wp = Wp; a.M = M; a.N = N; a.K = K; a.epi = epi; a.out = out; a.ldo = N; a.split_stride = (long)M * N;
+    a.A = A; a.Wp = Wp; a.M = M; a.N = N; a.K = K; a.a16 = a16; a.epi = epi; a.out = out; a.ldo = N;
+    a.split_stride = (long)M * N;
     a.nbw = pl.nbw; a.S = pl.S; a.cps = pl.cps; a.n_groups = pl.n_groups; a.grid = pl.grid;
     *S = pl.S;
     TIMED(TANDEM_K_GEMM, launch_gemm_stream(a, st));
     return TANDEM_OK;
   }
+  if (a16) return fail(&h->err, TANDEM_E_UNSUPPORTED, "fp16 activations off the streaming GEMM");
   GemmArgs g{};
   g.dt = dt; g.A = A; g.W = W; g.M = M; g.N = N; g.K = K; g.epi = epi;
   g.out = out; g.ldo = N; g.split_stride = (long)M * N;
@@ -397,7 +406,7 @@ tandem_status gate_up(tandem_handle* h, const Model& m, const Layer& L, int M, h
   if (L.p_gate_up && M <= kStreamMaxRows) {
     const StreamPlan pl = plan_stream_gemm(M, 2 * F, d, h->n_cu, m.p.ws_floats, kPlanSwiglu);
     GemmStreamArgs a{};
-    a.A = m.xa; a.Wp = L.p_gate_up; a.M = M; a.N = 2 * F; a.K = d;
+    a.A = m.xa; a.Wp = L.p_gate_up; a.M = M; a.N = 2 * F; a.K = d; a.a16 = m.ffn16;
     a.nbw = pl.nbw; a.S = pl.S; a.cps = pl.cps; a.n_groups = pl.n_groups; a.grid = pl.grid;
     if (pl.S == 1) {
       a.epi = EPI_SWIGLU; a.out = (float*)m.xf; a.ldo = F;
@@ -405,7 +414,7 @@ tandem_status gate_up(tandem_handle* h, const Model& m, const Layer& L, int M, h
     } else {
       a.epi = EPI_PARTIAL; a.out = m.ws; a.ldo = 2 * F; a.split_stride = (long)M * 2 * F;
       TIMED(TANDEM_K_GEMM, launch_gemm_stream(a, st));
-      TIMED(TANDEM_K_OTHER, launch_swiglu_finish(m.ws, pl.S, (long)M * 2 * F, M, F, true, m.xf, st));
+      TIMED(TANDEM_K_OTHER, launch_swiglu_finish(m.ws, pl.S, (long)M * 2 * F, M, F, true, m.ffn16, m.xf, st));
     }
     return TANDEM_OK;
   }
@@ -416,7 +425,7 @@ tandem_status gate_up(tandem_handle* h, const Model& m, const Layer& L, int M, h
     g.out = m.ws; g.ldo = 2 * F; g.split_stride = (long)M * 2 * F;
     g.splits = choose_splits(M, 2 * F, d, m.p.ws_floats, h->n_cu);
     TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
-    TIMED(TANDEM_K_OTHER, launch_swiglu_finish(m.ws, S, (long)M * 2 * F, M, F, false, m.xf, st));
+    TIMED(TANDEM_K_OTHER, launch_swiglu_finish(m.ws, S, (long)M * 2 * F, M, F, false, false, m.xf, st));
     return TANDEM_OK;
   }
   GemmArgs g{};
@@ -435,60 +444,90 @@ tandem_status gate_up(tandem_handle* h, const Model& m, const Layer& L, int M, h
 // Forward R rows through one model.  Rows read their token, cache slot and
 // position from the row arrays; done rows (row_done != NULL) skip the cache
 // append and produce zero attention.  With lm_head the logits land in m.logits.
-tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok, const int32_t* row_slot,
-                      const int32_t* row_pos, const int32_t* row_done, bool lm_head, hipStream_t st) {
+// One model's decode/prefill forward in three pieces: embedding + first norm,
+// one layer, final LM head.
+struct FwdRows {
+  int R;
+  const int32_t *tok, *slot, *pos, *done;
+};
+
+tandem_status forward_embed(tandem_handle* h, Model& m, const FwdRows& fr, hipStream_t st) {
+  const tandem_model_cfg& c = m.cfg;
+  const int dt = c.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32;
+  TIMED(TANDEM_K_OTHER, launch_embed_norm(dt, fr.tok, m.embed, c.d_model, m.layers[0].attn_norm, c.rms_eps, m.h,
+                                          m.xa, fr.R, st));
+  return TANDEM_OK;
+}
+
+tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr, hipStream_t st) {
   const tandem_model_cfg& c = m.cfg;
   const int dt = c.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32;
   const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads;
   const int qkv = m.p.qkv_dim, att = m.p.att_dim;
-  TIMED(TANDEM_K_OTHER, launch_embed_norm(dt, row_tok, m.embed, d, m.layers[0].attn_norm, c.rms_eps, m.h, m.xa, R, st));
-  for (int l = 0; l < c.n_layers; ++l) {
-    const Layer& L = m.layers[l];
-    CacheGeom cg;
-    cg.k = m.kc + (size_t)l * m.layer_stride * m.p.esz;
-    cg.v = m.vc + (size_t)l * m.layer_stride * m.p.esz;
-    cg.ctx_stride = h->plan.ctx_stride;
-    cg.slot_stride = m.slot_stride;
+  const int R = fr.R;
+  const Layer& L = m.layers[l];
+  CacheGeom cg;
+  cg.k = m.kc + (size_t)l * m.layer_stride * m.p.esz;
+  cg.v = m.vc + (size_t)l * m.layer_stride * m.p.esz;
+  cg.ctx_stride = h->plan.ctx_stride;
+  cg.slot_stride = m.slot_stride;
 
-    int S = 1;
-    CALL(gemm(h, m, m.xa, L.w_qkv, L.p_qkv, R, qkv, d, EPI_PARTIAL, m.ws, &S, st));
+  int S = 1;
+  CALL(gemm(h, m, m.xa, L.w_qkv, L.p_qkv, R, qkv, d, EPI_PARTIAL, m.ws, &S, st));
 
-    // decode rows (each its own cache slot) on the MFMA attention path get
-    // the QKV post-processing inside the attention kernel
-    const bool fuse = row_done != nullptr && attention_has_mfma(dt, hd, nq / nkv);
-    if (!fuse) {
-      QkvPostArgs qp{};
-      qp.dt = dt; qp.ws = m.ws; qp.S = S; qp.ws_stride = (long)R * qkv;
-      qp.R = R; qp.nq = nq; qp.nkv = nkv; qp.hd = hd;
-      qp.q_norm = c.qk_norm ? L.q_norm : nullptr; qp.k_norm = c.qk_norm ? L.k_norm : nullptr;
-      qp.eps = c.rms_eps; qp.rope = m.rope;
-      qp.row_slot = row_slot; qp.row_pos = row_pos; qp.row_done = row_done;
-      qp.q_out = m.q; qp.cache = cg;
-      TIMED(TANDEM_K_OTHER, launch_qkv_post(qp, st));
-    }
-
-    AttnArgs aa{};
-    aa.dt = dt; aa.q = m.q; aa.R = R; aa.nq = nq; aa.nkv = nkv; aa.hd = hd; aa.cache = cg;
-    aa.row_slot = row_slot; aa.row_pos = row_pos; aa.row_done = row_done; aa.out = m.xa;
-    if (fuse) {
-      aa.fuse.ws = m.ws; aa.fuse.S = S; aa.fuse.ws_stride = (long)R * qkv; aa.fuse.nkv = nkv;
-      aa.fuse.q_norm = c.qk_norm ? L.q_norm : nullptr; aa.fuse.k_norm = c.qk_norm ? L.k_norm : nullptr;
-      aa.fuse.eps = c.rms_eps; aa.fuse.rope = m.rope;
-    }
-    TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
-
-    CALL(gemm(h, m, m.xa, L.w_o, L.p_o, R, d, att, EPI_PARTIAL, m.ws, &S, st));
-    TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, L.ffn_norm, c.rms_eps, m.xa, R, d, st));
-
-    CALL(gate_up(h, m, L, R, st));
-    CALL(gemm(h, m, m.xf, L.w_down, L.p_down, R, d, c.ffn_dim, EPI_PARTIAL, m.ws, &S, st));
-    const float* next_gain = (l + 1 < c.n_layers) ? m.layers[l + 1].attn_norm : m.final_norm;
-    TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, next_gain, c.rms_eps, m.xa, R, d, st));
+  // decode rows (each its own cache slot) on the MFMA attention path get
+  // the QKV post-processing inside the attention kernel
+  const bool fuse = fr.done != nullptr && attention_has_mfma(dt, hd, nq / nkv);
+  if (!fuse) {
+    QkvPostArgs qp{};
+    qp.dt = dt; qp.ws = m.ws; qp.S = S; qp.ws_stride = (long)R * qkv;
+    qp.R = R; qp.nq = nq; qp.nkv = nkv; qp.hd = hd;
+    qp.q_norm = c.qk_norm ? L.q_norm : nullptr; qp.k_norm = c.qk_norm ? L.k_norm : nullptr;
+    qp.eps = c.rms_eps; qp.rope = m.rope;
+    qp.row_slot = fr.slot; qp.row_pos = fr.pos; qp.row_done = fr.done;
+    qp.q_out = m.q; qp.cache = cg;
+    TIMED(TANDEM_K_OTHER, launch_qkv_post(qp, st));
   }
-  if (lm_head) {
-    int S = 1;
-    CALL(gemm(h, m, m.xa, m.lm_head, m.p_lm, R, c.vocab, d, EPI_STORE, m.logits, &S, st));
+
+  AttnArgs aa{};
+  aa.dt = dt; aa.q = m.q; aa.R = R; aa.nq = nq; aa.nkv = nkv; aa.hd = hd; aa.cache = cg;
+  aa.row_slot = fr.slot; aa.row_pos = fr.pos; aa.row_done = fr.done; aa.out = m.xa;
+  if (fuse) {
+    aa.fuse.ws = m.ws; aa.fuse.S = S; aa.fuse.ws_stride = (long)R * qkv; aa.fuse.nkv = nkv;
+    aa.fuse.q_norm = c.qk_norm ? L.q_norm : nullptr; aa.fuse.k_norm = c.qk_norm ? L.k_norm : nullptr;
+    aa.fuse.eps = c.rms_eps; aa.fuse.rope = m.rope;
   }
+  TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
+
+  // the FFN's activations are fp16 when both its products stream (the
+  // output of the last layer's norm feeds the LM head only)
+  const bool f16 = m.ffn16 && R <= kStreamMaxRows;
+  const bool last = l + 1 == c.n_layers;
+  CALL(gemm(h, m, m.xa, L.w_o, L.p_o, R, d, att, EPI_PARTIAL, m.ws, &S, st));
+  TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, L.ffn_norm, c.rms_eps, m.xa, R, d, f16, st));
+
+  CALL(gate_up(h, m, L, R, st));
+  CALL(gemm(h, m, m.xf, L.w_down, L.p_down, R, d, c.ffn_dim, EPI_PARTIAL, m.ws, &S, st, f16));
+  const float* next_gain = last ? m.final_norm : m.layers[l + 1].attn_norm;
+  const bool next16 = last && m.lm16 && R <= kStreamMaxRows;
+  TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, next_gain, c.rms_eps, m.xa, R, d, next16, st));
+  return TANDEM_OK;
+}
+
+tandem_status forward_head(tandem_handle* h, Model& m, const FwdRows& fr, hipStream_t st) {
+  const tandem_model_cfg& c = m.cfg;
+  int S = 1;
+  CALL(gemm(h, m, m.xa, m.lm_head, m.p_lm, fr.R, c.vocab, c.d_model, EPI_STORE, m.logits, &S, st,
+            m.lm16 && fr.R <= kStreamMaxRows));
+  return TANDEM_OK;
+}
+
+tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok, const int32_t* row_slot,
+                      const int32_t* row_pos, const int32_t* row_done, bool lm_head, hipStream_t st) {
+  const FwdRows fr{R, row_tok, row_slot, row_pos, row_done};
+  CALL(forward_embed(h, m, fr, st));
+  for (int l = 0; l < m.cfg.n_layers; ++l) CALL(forward_layer(h, m, l, fr, st));
+  if (lm_head) CALL(forward_head(h, m, fr, st));
   return TANDEM_OK;
 }
 
@@ -506,10 +545,8 @@ tandem_status forward_pair(tandem_handle* h, int R, const int32_t* row_tok, cons
   }
   HIPCHK(hipEventRecord(h->ev_fork, st));
   HIPCHK(hipStreamWaitEvent(h->side, h->ev_fork, 0));
-  tandem_status s = forward(h, h->m[1], R, row_tok, row_slot, row_pos, row_done, lm_head, h->side);
-  if (s != TANDEM_OK) return s;
-  s = forward(h, h->m[0], R, row_tok, row_slot, row_pos, row_done, lm_head, st);
-  if (s != TANDEM_OK) return s;
+  CALL(forward(h, h->m[1], R, row_tok, row_slot, row_pos, row_done, lm_head, h->side));
+  CALL(forward(h, h->m[0], R, row_tok, row_slot, row_pos, row_done, lm_head, st));
   HIPCHK(hipEventRecord(h->ev_join, h->side));
   HIPCHK(hipStreamWaitEvent(st, h->ev_join, 0));
   return TANDEM_OK;
@@ -830,12 +867,15 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     char* dst = sc + m.p.off_packed;
     const auto shapes = packed_shapes(&m.cfg);
     size_t k = 0;
-    auto pack = [&](const void* src, int N, int K, int pair_rows, const void** out) -> hipError_t {
+    const tandem_model_cfg& mc = m.cfg;
+    m.ffn16 = packs(&mc, 2 * mc.ffn_dim, mc.d_model) && packs(&mc, mc.d_model, mc.ffn_dim);
+    m.lm16 = packs(&mc, mc.vocab, mc.d_model);
+    auto pack = [&](const void* src, int N, int K, int pair_rows, bool to_f16, const void** out) -> hipError_t {
       const auto& nk = shapes[k++];
       if (nk.first != N || nk.second != K) return hipErrorInvalidValue;
       *out = nullptr;
       if (!packs(&m.cfg, N, K)) return hipSuccess;
-      hipError_t r = launch_pack_weights(src, N, K, pair_rows, dst, h->stream);
+      hipError_t r = launch_pack_weights(src, N, K, pair_rows, to_f16, dst, h->stream);
       *out = dst;
       dst += align_up(packed_weight_bytes(N, K), kAlign);
       return r;
@@ -843,12 +883,12 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     const tandem_model_cfg& c = m.cfg;
     for (int l = 0; l < c.n_layers && e == hipSuccess; ++l) {
       Layer& L = m.layers[l];
-      if (e == hipSuccess) e = pack(L.w_qkv, m.p.qkv_dim, c.d_model, 0, &L.p_qkv);
-      if (e == hipSuccess) e = pack(L.w_o, c.d_model, m.p.att_dim, 0, &L.p_o);
-      if (e == hipSuccess) e = pack(L.w_gate_up, 2 * c.ffn_dim, c.d_model, c.ffn_dim, &L.p_gate_up);
-      if (e == hipSuccess) e = pack(L.w_down, c.d_model, c.ffn_dim, 0, &L.p_down);
+      if (e == hipSuccess) e = pack(L.w_qkv, m.p.qkv_dim, c.d_model, 0, false, &L.p_qkv);
+      if (e == hipSuccess) e = pack(L.w_o, c.d_model, m.p.att_dim, 0, false, &L.p_o);
+      if (e == hipSuccess) e = pack(L.w_gate_up, 2 * c.ffn_dim, c.d_model, c.ffn_dim, m.ffn16, &L.p_gate_up);
+      if (e == hipSuccess) e = pack(L.w_down, c.d_model, c.ffn_dim, 0, m.ffn16, &L.p_down);
     }
-    if (e == hipSuccess) e = pack(m.lm_head, c.vocab, c.d_model, 0, &m.p_lm);
+    if (e == hipSuccess) e = pack(m.lm_head, c.vocab, c.d_model, 0, m.lm16, &m.p_lm);
     if (e != hipSuccess) return bail(e, "weight packing");
   }
   std::vector<int32_t> ident(S);
