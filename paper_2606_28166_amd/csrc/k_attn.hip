@@ -154,29 +154,17 @@ __device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, con
   }
 }
 
-// FUSED (decode rows: one cache slot per row, so no other workgroup of the
-// launch reads what this one appends): the workgroup also finishes its own
-// heads' QKV projection (sum of the split-K partials, per-head RMSNorm of q
-// and k, rotary embedding at the row's position), appends this row's k and v
-// for its kv head to the cache, and keeps q, k and v in LDS.  The cache
-// stream then covers positions 0 .. pos - 1 only (its first loads are issued
-// before the projection is finished), and the new position enters at the
-// final softmax merge from LDS.
-template <int HD, int GQA, bool FUSED>
+template <int HD, int GQA>
 __global__ __launch_bounds__(256) void attn_mfma_kernel(
-    const float* __restrict__ q, bf16_t* __restrict__ kc, bf16_t* __restrict__ vc,
+    const float* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     int ctx_stride, long slot_stride, const int32_t* __restrict__ row_slot,
     const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
-    bf16_t* __restrict__ out, int nq, QkvFuse fz) {
+    bf16_t* __restrict__ out, int nq) {
   constexpr int DC = HD / 32;     // k-steps of the S product
   constexpr int DB = HD / 16;     // 16-dim blocks of the O product
-  constexpr int QH = FUSED ? GQA : 1;
   __shared__ float sm_m[4][16];
   __shared__ float sm_l[4][16];
   __shared__ float sm_o[4][GQA][HD];
-  __shared__ float sm_q[QH][HD];
-  __shared__ float sm_kv[FUSED ? 2 : 1][HD];          // the new position's k and v (bf16 values)
-  __shared__ float sm_s[QH];                           // its score per head (log2 units)
 
   const int kh = blockIdx.x, r = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -189,96 +177,25 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   }
   const int slot = row_slot[r];
   const int pos = row_pos[r];
-  const int ctx = FUSED ? pos : pos + 1;              // positions streamed from the cache
+  const int ctx = pos + 1;                            // positions streamed from the cache
   const size_t plane = (size_t)slot * slot_stride + (size_t)kh * ctx_stride * HD;
   const __amdgpu_buffer_rsrc_t kr = buf_rsrc(kc + plane, (uint32_t)ctx_stride * HD * 2);
   const __amdgpu_buffer_rsrc_t vr = buf_rsrc(vc + plane, (uint32_t)ctx_stride * HD * 2);
   const float scale = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
 
   // Wave w owns chunks w, w + 4, w + 8, ... of the stream; its first chunk
-  // is requested before anything else.
+  // is requested before the query is read.
   const int nchunk = (ctx + 15) >> 4;
   const int nmine = nchunk > wave ? (nchunk - wave + 3) >> 2 : 0;
   auto chunk_at = [&](int i) { return wave + 4 * min(i, nmine - 1); };
   KV16<HD> ca, cb;
   if (nmine > 0) load_chunk<HD>(ca, kr, vr, chunk_at(0), lane);
 
-  if (FUSED) {
-    // heads of this workgroup: its GQA query heads, then its k head, then its
-    // v head; wave w takes heads w, w + 4, ...; lane i < HD / 2 owns the
-    // rotary pair (i, i + HD / 2)
-    constexpr int HALF = HD / 2;
-    const int nh = nq + 2 * fz.nkv;
-    const float* prow = fz.ws + (size_t)r * nh * HD;
-    for (int t = wave; t < GQA + 2; t += 4) {
-      const int head = t < GQA ? kh * GQA + t : (t == GQA ? nq + kh : nq + fz.nkv + kh);
-      float x1 = 0.f, x2 = 0.f;
-      if (lane < HALF) {
-        float a1[16], a2[16];
-#pragma unroll
-        for (int s = 0; s < 16; ++s)
-          if (s < fz.S) {
-            a1[s] = prow[s * fz.ws_stride + head * HD + lane];
-            a2[s] = prow[s * fz.ws_stride + head * HD + lane + HALF];
-          }
-#pragma unroll
-        for (int s = 0; s < 16; ++s)
-          if (s < fz.S) {
-            x1 += a1[s];
-            x2 += a2[s];
-          }
-      }
-      if (t == GQA + 1) {                       // v: stored as is
-        if (lane < HALF) {
-          const bf16_t b1 = f2bf(x1), b2 = f2bf(x2);
-          vc[plane + kv_v_index(pos, lane, HD)] = b1;
-          vc[plane + kv_v_index(pos, lane + HALF, HD)] = b2;
-          sm_kv[FUSED ? 1 : 0][lane] = bf2f(b1);
-          sm_kv[FUSED ? 1 : 0][lane + HALF] = bf2f(b2);
-        }
-        continue;
-      }
-      const float* gn = t < GQA ? fz.q_norm : fz.k_norm;
-      if (gn) {
-        const float ss = wave_sum(x1 * x1 + x2 * x2);
-        const float rs = 1.f / sqrtf(ss / (float)HD + fz.eps);
-        if (lane < HALF) {
-          x1 *= rs * gn[lane];
-          x2 *= rs * gn[lane + HALF];
-        }
-      }
-      if (lane < HALF) {
-        const float2 cs = fz.rope[(size_t)pos * HALF + lane];
-        const float y1 = x1 * cs.x - x2 * cs.y;
-        const float y2 = x2 * cs.x + x1 * cs.y;
-        if (t < GQA) {
-          sm_q[t < GQA ? t : 0][lane] = y1;
-          sm_q[t < GQA ? t : 0][lane + HALF] = y2;
-        } else {
-          const bf16_t b1 = f2bf(y1), b2 = f2bf(y2);
-          kc[plane + kv_k_index(pos, lane, HD)] = b1;
-          kc[plane + kv_k_index(pos, lane + HALF, HD)] = b2;
-          sm_kv[0][lane] = bf2f(b1);
-          sm_kv[0][lane + HALF] = bf2f(b2);
-        }
-      }
-    }
-    __syncthreads();
-    // score of the new position for each query head (log2 units)
-    for (int t = wave; t < GQA; t += 4) {
-      float a = 0.f;
-      for (int d = lane; d < HD; d += 64) a += sm_q[t < GQA ? t : 0][d] * sm_kv[0][d];
-      a = wave_sum(a);
-      if (lane == 0) sm_s[t < GQA ? t : 0] = a * scale;
-    }
-  }
-
   // Q^T operand: column = query head c16 of this group, k = dims 32dc + 8g .. +7
   bf16x8_t qh[DC], ql[DC];
   {
     const bool valid = c16 < GQA;
-    const float* qp = FUSED ? &sm_q[0][0] + (valid ? c16 : 0) * HD + 8 * g
-                            : q + ((size_t)r * nq + kh * GQA + (valid ? c16 : 0)) * HD + 8 * g;
+    const float* qp = q + ((size_t)r * nq + kh * GQA + (valid ? c16 : 0)) * HD + 8 * g;
 #pragma unroll
     for (int dc = 0; dc < DC; ++dc) {
       const float4 a = *reinterpret_cast<const float4*>(qp + 32 * dc);
@@ -333,18 +250,12 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
     float M = sm_m[0][h];
 #pragma unroll
     for (int w = 1; w < 4; ++w) M = fmaxf(M, sm_m[w][h]);
-    if (FUSED) M = fmaxf(M, sm_s[FUSED ? h : 0]);
     float num = 0.f, den = 0.f;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const float f = exp2f(sm_m[w][h] - M);
       num += sm_o[w][h][d] * f;
       den += sm_l[w][h] * f;
-    }
-    if (FUSED) {
-      const float f = exp2f(sm_s[FUSED ? h : 0] - M);
-      num += sm_kv[FUSED ? 1 : 0][d] * f;
-      den += f;
     }
     split_store(orow, col0 + e, num / den);
   }
@@ -411,14 +322,9 @@ __global__ __launch_bounds__(128) void attn_valu_kernel(
 
 template <int HD, int GQA>
 hipError_t run_mfma(const AttnArgs& a, hipStream_t st) {
-  if (a.fuse.ws)
-    hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, true>), dim3(a.nkv, a.R), dim3(256), 0, st, a.q,
-                       (bf16_t*)a.cache.k, (bf16_t*)a.cache.v, a.cache.ctx_stride, a.cache.slot_stride,
-                       a.row_slot, a.row_pos, a.row_done, (bf16_t*)a.out, a.nq, a.fuse);
-  else
-    hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, false>), dim3(a.nkv, a.R), dim3(256), 0, st, a.q,
-                       (bf16_t*)a.cache.k, (bf16_t*)a.cache.v, a.cache.ctx_stride, a.cache.slot_stride,
-                       a.row_slot, a.row_pos, a.row_done, (bf16_t*)a.out, a.nq, a.fuse);
+  hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA>), dim3(a.nkv, a.R), dim3(256), 0, st, a.q,
+                     (const bf16_t*)a.cache.k, (const bf16_t*)a.cache.v, a.cache.ctx_stride, a.cache.slot_stride,
+                     a.row_slot, a.row_pos, a.row_done, (bf16_t*)a.out, a.nq);
   return hipGetLastError();
 }
 
@@ -443,8 +349,6 @@ bool attention_has_mfma(int dt, int hd, int gqa) {
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st) {
   if (a.R <= 0) return hipSuccess;
   const int gqa = a.nq / a.nkv;
-  if (a.fuse.ws && (!attention_has_mfma(a.dt, a.hd, gqa) || a.fuse.S < 1 || a.fuse.S > 16 || a.fuse.nkv != a.nkv))
-    return hipErrorInvalidValue;
   if (attention_has_mfma(a.dt, a.hd, gqa)) {
     if (a.hd == 64) return dispatch_gqa<64>(a, gqa, st);
     return dispatch_gqa<128>(a, gqa, st);

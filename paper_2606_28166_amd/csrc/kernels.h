@@ -123,13 +123,6 @@ hipError_t launch_qkv_post(const QkvPostArgs& a, hipStream_t st);
 // attention workgroup of (kv head, row) sums its heads' split-K partials,
 // normalises and rotates q and k, appends k and v to the cache and keeps q
 // in LDS.  Only for decode rows (distinct cache slots) on the MFMA path.
-struct QkvFuse {
-  const float* ws;        // QKV partials: ws + s * ws_stride + (r * (nq + 2 nkv) + head) * hd
-  int S; long ws_stride;
-  int nkv;
-  const float* q_norm; const float* k_norm; float eps;
-  const float2* rope;     // [ctx_stride][hd/2] (cos, sin)
-};
 
 // Decode/prefill attention of every row's query heads over positions
 // 0..row_pos[r] of its slot; out[r][h * hd + d] (an activation row of width
@@ -140,7 +133,6 @@ struct AttnArgs {
   CacheGeom cache;
   const int32_t* row_slot; const int32_t* row_pos; const int32_t* row_done;
   void* out;
-  QkvFuse fuse;           // fuse.ws == NULL: q comes from `q`, k and v are already in the cache
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
 

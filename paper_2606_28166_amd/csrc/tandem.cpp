@@ -475,10 +475,7 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   int S = 1;
   CALL(gemm(h, m, m.xa, L.w_qkv, L.p_qkv, R, qkv, d, EPI_PARTIAL, m.ws, &S, st));
 
-  // decode rows (each its own cache slot) on the MFMA attention path get
-  // the QKV post-processing inside the attention kernel
-  const bool fuse = fr.done != nullptr && attention_has_mfma(dt, hd, nq / nkv);
-  if (!fuse) {
+  {
     QkvPostArgs qp{};
     qp.dt = dt; qp.ws = m.ws; qp.S = S; qp.ws_stride = (long)R * qkv;
     qp.R = R; qp.nq = nq; qp.nkv = nkv; qp.hd = hd;
@@ -492,11 +489,6 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   AttnArgs aa{};
   aa.dt = dt; aa.q = m.q; aa.R = R; aa.nq = nq; aa.nkv = nkv; aa.hd = hd; aa.cache = cg;
   aa.row_slot = fr.slot; aa.row_pos = fr.pos; aa.row_done = fr.done; aa.out = m.xa;
-  if (fuse) {
-    aa.fuse.ws = m.ws; aa.fuse.S = S; aa.fuse.ws_stride = (long)R * qkv; aa.fuse.nkv = nkv;
-    aa.fuse.q_norm = c.qk_norm ? L.q_norm : nullptr; aa.fuse.k_norm = c.qk_norm ? L.k_norm : nullptr;
-    aa.fuse.eps = c.rms_eps; aa.fuse.rope = m.rope;
-  }
   TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
 
   // the FFN's activations are fp16 when both its products stream (the

@@ -92,7 +92,10 @@ def analyze(fetch_csv: str, write_csv: str) -> dict:
         if not copies:
             raise SystemExit(f"no copy kernel in {path}")
         cal = max(copies)                        # KiB the counter reports for COPY_BYTES
-        att = [(k, v) for _, k, v in rows if "attn_mfma_kernel" in k and "true" in k]
+        # the decode launches are the last STEPS * (both models' layers)
+        # attention dispatches (the prefill's come first)
+        n_dec = STEPS * (wl.senior.n_layers + wl.junior.n_layers)
+        att = [(k, v) for _, k, v in rows if "attn_mfma_kernel" in k][-n_dec:]
         res[name] = {"copy_counter_kib": cal, "scale_bytes_per_kib": COPY_BYTES / cal,
                      "attention_dispatches": len(att)}
         res[name]["attention_counter_kib"] = [v for _, v in att]
