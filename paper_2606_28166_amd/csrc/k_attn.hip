@@ -91,9 +91,13 @@ struct AttnState {
   f32x4_t o[HD / 16];             // O[head 4g + i][dim 16 db + c16]
 };
 
-template <int HD>
+// ctx: this lane's query column attends positions < ctx; ctx_max: positions
+// >= ctx_max hold stale cache contents.  GUARD: a column may see a chunk with
+// no position it attends before any it does (several query rows per
+// workgroup); its running max then stays -inf and nothing is added.
+template <int HD, bool GUARD>
 __device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, const bf16x8_t* qh, const bf16x8_t* ql,
-                                             int p0, int ctx, float scale, int g) {
+                                             int p0, int ctx, int ctx_max, float scale, int g) {
   constexpr int DC = HD / 32, DB = HD / 16;
   f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -111,10 +115,11 @@ __device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, con
   mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
   const float m_new = fmaxf(st.m_run, mx);
-  const float alpha = exp2f(st.m_run - m_new);
+  const bool none = GUARD && m_new == -INFINITY;
+  const float alpha = none ? 1.f : exp2f(st.m_run - m_new);
   float pr[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) pr[i] = exp2f(s[i] - m_new);
+  for (int i = 0; i < 4; ++i) pr[i] = none ? 0.f : exp2f(s[i] - m_new);
   st.l_run = st.l_run * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
   st.m_run = m_new;
   s16x4_t ph, pl;
@@ -131,9 +136,9 @@ __device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, con
   }
   // positions at or past the context hold stale cache contents: zero them so
   // that 0 * (stale) cannot produce NaN
-  if (p0 + 16 > ctx) {
+  if (p0 + 16 > ctx_max) {
     // keep the first nv of this lane's four positions (16 bits each)
-    const int nv = min(max(ctx - pg, 0), 4);
+    const int nv = min(max(ctx_max - pg, 0), 4);
     const uint64_t keep = nv == 4 ? ~0ull : (1ull << (16 * nv)) - 1ull;
     const uint32_t klo = (uint32_t)keep, khi = (uint32_t)(keep >> 32);
 #pragma unroll
@@ -154,30 +159,51 @@ __device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, con
   }
 }
 
-template <int HD, int GQA>
+// Workgroup (kv head, block of query rows).  Decode (ROWS = 1): one row per
+// workgroup, query columns = the GQA heads of the group.  Prompt rows (ROWS =
+// 16 / GQA): ROWS consecutive rows of one prompt share the workgroup, query
+// column c = (row c / GQA, head c % GQA), each with its own causal limit; the
+// workgroup streams the positions its last row attends, so a prompt's K/V is
+// read once per ROWS rows rather than once per row.
+template <int HD, int GQA, int ROWS>
 __global__ __launch_bounds__(256) void attn_mfma_kernel(
     const float* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     int ctx_stride, long slot_stride, const int32_t* __restrict__ row_slot,
     const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
+    const int32_t* __restrict__ grp_row0, const int32_t* __restrict__ grp_n,
     bf16_t* __restrict__ out, int nq) {
   constexpr int DC = HD / 32;     // k-steps of the S product
   constexpr int DB = HD / 16;     // 16-dim blocks of the O product
+  constexpr int NCOL = GQA * ROWS;
+  static_assert(NCOL <= 16, "16 query columns per workgroup");
   __shared__ float sm_m[4][16];
   __shared__ float sm_l[4][16];
-  __shared__ float sm_o[4][GQA][HD];
+  __shared__ float sm_o[4][NCOL][HD];
 
-  const int kh = blockIdx.x, r = blockIdx.y;
+  const int kh = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
-  bf16_t* orow = out + (size_t)r * 2 * nq * HD;       // split-format activation row
+  // rows r0 .. r0 + nr - 1 (16-row groups of one prompt, split in 16 / ROWS)
+  int r0 = blockIdx.y, nr = 1;
+  if (ROWS > 1) {
+    constexpr int SUB = 16 / ROWS;
+    const int grp = blockIdx.y / SUB, sub = blockIdx.y % SUB;
+    r0 = grp_row0[grp] + sub * ROWS;
+    nr = min(ROWS, grp_n[grp] - sub * ROWS);
+    if (nr <= 0) return;
+  }
   const int col0 = kh * GQA * HD;
-  if (row_done && row_done[r]) {
+  if (ROWS == 1 && row_done && row_done[r0]) {
+    bf16_t* orow = out + (size_t)r0 * 2 * nq * HD;     // split-format activation row
     for (int e = tid; e < GQA * HD; e += 256) split_store(orow, col0 + e, 0.f);
     return;
   }
-  const int slot = row_slot[r];
-  const int pos = row_pos[r];
-  const int ctx = pos + 1;                            // positions streamed from the cache
+  const int slot = row_slot[r0];
+  const int ctx_max = row_pos[r0 + nr - 1] + 1;       // positions streamed from the cache
+  const int ri = c16 / GQA, hq = c16 % GQA;           // this lane's query column
+  const bool valid = c16 < NCOL && ri < nr;
+  const int rr = r0 + (valid ? ri : 0);
+  const int ctx = valid ? row_pos[rr] + 1 : ctx_max;  // positions the column attends
   const size_t plane = (size_t)slot * slot_stride + (size_t)kh * ctx_stride * HD;
   const __amdgpu_buffer_rsrc_t kr = buf_rsrc(kc + plane, (uint32_t)ctx_stride * HD * 2);
   const __amdgpu_buffer_rsrc_t vr = buf_rsrc(vc + plane, (uint32_t)ctx_stride * HD * 2);
@@ -185,17 +211,16 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
 
   // Wave w owns chunks w, w + 4, w + 8, ... of the stream; its first chunk
   // is requested before the query is read.
-  const int nchunk = (ctx + 15) >> 4;
+  const int nchunk = (ctx_max + 15) >> 4;
   const int nmine = nchunk > wave ? (nchunk - wave + 3) >> 2 : 0;
   auto chunk_at = [&](int i) { return wave + 4 * min(i, nmine - 1); };
   KV16<HD> ca, cb;
   if (nmine > 0) load_chunk<HD>(ca, kr, vr, chunk_at(0), lane);
 
-  // Q^T operand: column = query head c16 of this group, k = dims 32dc + 8g .. +7
+  // Q^T operand: column c16, k = dims 32dc + 8g .. +7 (zero for unused columns)
   bf16x8_t qh[DC], ql[DC];
   {
-    const bool valid = c16 < GQA;
-    const float* qp = q + ((size_t)r * nq + kh * GQA + (valid ? c16 : 0)) * HD + 8 * g;
+    const float* qp = q + ((size_t)rr * nq + kh * GQA + (valid ? hq : 0)) * HD + 8 * g;
 #pragma unroll
     for (int dc = 0; dc < DC; ++dc) {
       const float4 a = *reinterpret_cast<const float4*>(qp + 32 * dc);
@@ -222,11 +247,11 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   for (int i = 0; i < nmine; i += 2) {
     if (i + 1 < nmine) load_chunk<HD>(cb, kr, vr, chunk_at(i + 1), lane);
     pin_chunk<HD>(ca);
-    attend_chunk<HD>(st, ca, qh, ql, 16 * chunk_at(i), ctx, scale, g);
+    attend_chunk<HD, (ROWS > 1)>(st, ca, qh, ql, 16 * chunk_at(i), ctx, ctx_max, scale, g);
     if (i + 2 < nmine) load_chunk<HD>(ca, kr, vr, chunk_at(i + 2), lane);
     if (i + 1 < nmine) {
       pin_chunk<HD>(cb);
-      attend_chunk<HD>(st, cb, qh, ql, 16 * chunk_at(i + 1), ctx, scale, g);
+      attend_chunk<HD, (ROWS > 1)>(st, cb, qh, ql, 16 * chunk_at(i + 1), ctx, ctx_max, scale, g);
     }
   }
 
@@ -242,11 +267,12 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int h = 4 * g + i;
-      if (h < GQA) sm_o[wave][h][db * 16 + c16] = st.o[db][i];
+      if (h < NCOL) sm_o[wave][h][db * 16 + c16] = st.o[db][i];
     }
   __syncthreads();
-  for (int e = tid; e < GQA * HD; e += 256) {
+  for (int e = tid; e < NCOL * HD; e += 256) {
     const int h = e / HD, d = e % HD;
+    if (h / GQA >= nr) continue;
     float M = sm_m[0][h];
 #pragma unroll
     for (int w = 1; w < 4; ++w) M = fmaxf(M, sm_m[w][h]);
@@ -257,7 +283,8 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
       num += sm_o[w][h][d] * f;
       den += sm_l[w][h] * f;
     }
-    split_store(orow, col0 + e, num / den);
+    bf16_t* orow = out + (size_t)(r0 + h / GQA) * 2 * nq * HD;
+    split_store(orow, col0 + (h % GQA) * HD + d, num / den);
   }
 }
 
@@ -322,9 +349,18 @@ __global__ __launch_bounds__(128) void attn_valu_kernel(
 
 template <int HD, int GQA>
 hipError_t run_mfma(const AttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA>), dim3(a.nkv, a.R), dim3(256), 0, st, a.q,
+  constexpr int ROWS = 16 / GQA;
+  if (ROWS > 1 && a.grp_row0) {
+    hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, (ROWS > 1 ? ROWS : 1)>), dim3(a.nkv, a.n_groups * (16 / ROWS)),
+                       dim3(256), 0, st, a.q, (const bf16_t*)a.cache.k, (const bf16_t*)a.cache.v, a.cache.ctx_stride,
+                       a.cache.slot_stride, a.row_slot, a.row_pos, a.row_done, a.grp_row0, a.grp_n, (bf16_t*)a.out,
+                       a.nq);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, 1>), dim3(a.nkv, a.R), dim3(256), 0, st, a.q,
                      (const bf16_t*)a.cache.k, (const bf16_t*)a.cache.v, a.cache.ctx_stride, a.cache.slot_stride,
-                     a.row_slot, a.row_pos, a.row_done, (bf16_t*)a.out, a.nq);
+                     a.row_slot, a.row_pos, a.row_done, (const int32_t*)nullptr, (const int32_t*)nullptr,
+                     (bf16_t*)a.out, a.nq);
   return hipGetLastError();
 }
 

@@ -133,6 +133,10 @@ struct AttnArgs {
   CacheGeom cache;
   const int32_t* row_slot; const int32_t* row_pos; const int32_t* row_done;
   void* out;
+  // prompt rows (row_done NULL): n_groups groups of at most 16 consecutive
+  // rows of one prompt, rows grp_row0[g] .. + grp_n[g] - 1 in increasing
+  // position order; NULL: one workgroup per row
+  const int32_t* grp_row0; const int32_t* grp_n; int n_groups;
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
 

@@ -213,7 +213,7 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
   const size_t S = (size_t)cap->max_seqs;
   P.off_state = sc; sc = align_up(sc + 6 * S * 4, kAlign);
   P.off_seq_slot = sc; sc = align_up(sc + S * 4, kAlign);
-  P.off_rows = sc; sc = align_up(sc + 4 * (size_t)cap->max_prefill_tokens * 4, kAlign);
+  P.off_rows = sc; sc = align_up(sc + 6 * (size_t)cap->max_prefill_tokens * 4, kAlign);
   P.off_prompt = sc; sc = align_up(sc + 2 * S * 4, kAlign);
   P.off_partials = sc; sc = align_up(sc + S * P.n_chunks * 5 * 4, kAlign);
   P.off_count = sc; sc = align_up(sc + 4, kAlign);
@@ -248,6 +248,7 @@ struct tandem_handle {
   int32_t *owner, *c, *t, *pos, *pending, *done;
   int32_t* seq_slot;
   int32_t *row_slot, *row_pos, *row_tok, *row_src;      // prompt rows
+  int32_t *grp_row0, *grp_n;                            // their 16-row groups (attention)
   // Decode rows: row r carries sequence act[r].  After a prefill act is the
   // identity; with EOS on, a stable partition (unfinished first) runs every
   // kCompactEvery steps and the launched row count shrinks to the smallest
@@ -449,6 +450,10 @@ tandem_status gate_up(tandem_handle* h, const Model& m, const Layer& L, int M, h
 struct FwdRows {
   int R;
   const int32_t *tok, *slot, *pos, *done;
+  // prompt rows: groups of at most 16 consecutive rows of one prompt (the
+  // attention's row blocks); NULL at decode
+  const int32_t *grp_row0 = nullptr, *grp_n = nullptr;
+  int n_groups = 0;
 };
 
 tandem_status forward_embed(tandem_handle* h, Model& m, const FwdRows& fr, hipStream_t st) {
@@ -489,6 +494,7 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   AttnArgs aa{};
   aa.dt = dt; aa.q = m.q; aa.R = R; aa.nq = nq; aa.nkv = nkv; aa.hd = hd; aa.cache = cg;
   aa.row_slot = fr.slot; aa.row_pos = fr.pos; aa.row_done = fr.done; aa.out = m.xa;
+  aa.grp_row0 = fr.grp_row0; aa.grp_n = fr.grp_n; aa.n_groups = fr.n_groups;
   TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
 
   // the FFN's activations are fp16 when both its products stream (the
@@ -514,9 +520,7 @@ tandem_status forward_head(tandem_handle* h, Model& m, const FwdRows& fr, hipStr
   return TANDEM_OK;
 }
 
-tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok, const int32_t* row_slot,
-                      const int32_t* row_pos, const int32_t* row_done, bool lm_head, hipStream_t st) {
-  const FwdRows fr{R, row_tok, row_slot, row_pos, row_done};
+tandem_status forward(tandem_handle* h, Model& m, const FwdRows& fr, bool lm_head, hipStream_t st) {
   CALL(forward_embed(h, m, fr, st));
   for (int l = 0; l < m.cfg.n_layers; ++l) CALL(forward_layer(h, m, l, fr, st));
   if (lm_head) CALL(forward_head(h, m, fr, st));
@@ -525,20 +529,16 @@ tandem_status forward(tandem_handle* h, Model& m, int R, const int32_t* row_tok,
 
 // Both models' forwards over the same rows: the junior on the side stream,
 // the senior on the main stream, joined before anything that reads either.
-tandem_status forward_pair(tandem_handle* h, int R, const int32_t* row_tok, const int32_t* row_slot,
-                           const int32_t* row_pos, const int32_t* row_done, bool lm_head) {
+tandem_status forward_pair(tandem_handle* h, const FwdRows& fr, bool lm_head) {
   hipStream_t st = h->stream;
   if (h->timing & TANDEM_TIMING_SERIAL) {
-    for (int i = 0; i < 2; ++i) {
-      tandem_status s = forward(h, h->m[i], R, row_tok, row_slot, row_pos, row_done, lm_head, st);
-      if (s != TANDEM_OK) return s;
-    }
+    for (int i = 0; i < 2; ++i) CALL(forward(h, h->m[i], fr, lm_head, st));
     return TANDEM_OK;
   }
   HIPCHK(hipEventRecord(h->ev_fork, st));
   HIPCHK(hipStreamWaitEvent(h->side, h->ev_fork, 0));
-  CALL(forward(h, h->m[1], R, row_tok, row_slot, row_pos, row_done, lm_head, h->side));
-  CALL(forward(h, h->m[0], R, row_tok, row_slot, row_pos, row_done, lm_head, st));
+  CALL(forward(h, h->m[1], fr, lm_head, h->side));
+  CALL(forward(h, h->m[0], fr, lm_head, st));
   HIPCHK(hipEventRecord(h->ev_join, h->side));
   HIPCHK(hipStreamWaitEvent(st, h->ev_join, 0));
   return TANDEM_OK;
@@ -554,7 +554,7 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
     ga.pending = h->pending; ga.seq_slot = h->seq_slot; ga.pos = h->pos; ga.done = h->done;
     ga.row_tok = h->drow_tok; ga.row_slot = h->drow_slot; ga.row_pos = h->drow_pos; ga.row_done = h->drow_done;
     TIMED(TANDEM_K_OTHER, launch_gather_rows(ga, st));
-    tandem_status s = forward_pair(h, R, h->drow_tok, h->drow_slot, h->drow_pos, h->drow_done, true);
+    tandem_status s = forward_pair(h, FwdRows{R, h->drow_tok, h->drow_slot, h->drow_pos, h->drow_done}, true);
     if (s != TANDEM_OK) return s;
   }
   const int V = h->m[0].cfg.vocab;
@@ -803,6 +803,7 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   int32_t* rows = (int32_t*)(sc + P.off_rows);
   const size_t PT = (size_t)cap->max_prefill_tokens;
   h->row_slot = rows; h->row_pos = rows + PT; h->row_tok = rows + 2 * PT; h->row_src = rows + 3 * PT;
+  h->grp_row0 = rows + 4 * PT; h->grp_n = rows + 5 * PT;
   int32_t* pr = (int32_t*)(sc + P.off_prompt);
   h->p_end = pr; h->p_len = pr + S;
   h->partials = (float*)(sc + P.off_partials);
@@ -946,22 +947,31 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
       ++j1;
     }
     if (nr > 0) {
-      rows.assign(3 * (size_t)nr, 0);
-      int r = 0;
+      rows.assign(5 * (size_t)nr, 0);
+      int r = 0, ng = 0;
       for (int j = j0; j < j1; ++j) {
         const int P = prompt_offsets[j + 1] - prompt_offsets[j];
         for (int i = 0; i < P - 1; ++i, ++r) {
           rows[r] = j * G;                            // slot of the prompt's first sequence
           rows[nr + r] = i;                           // position
           rows[2 * nr + r] = prompt_offsets[j] + i;   // source token index
+          if (i % 16 == 0) {                          // groups of 16 rows within the prompt
+            rows[3 * nr + ng] = r;
+            rows[4 * nr + ng] = std::min(16, P - 1 - i);
+            ++ng;
+          }
         }
       }
       HIPCHK(hipMemcpyAsync(h->row_slot, rows.data(), (size_t)nr * 4, hipMemcpyHostToDevice, st));
       HIPCHK(hipMemcpyAsync(h->row_pos, rows.data() + nr, (size_t)nr * 4, hipMemcpyHostToDevice, st));
       HIPCHK(hipMemcpyAsync(h->row_src, rows.data() + 2 * nr, (size_t)nr * 4, hipMemcpyHostToDevice, st));
+      HIPCHK(hipMemcpyAsync(h->grp_row0, rows.data() + 3 * nr, (size_t)ng * 4, hipMemcpyHostToDevice, st));
+      HIPCHK(hipMemcpyAsync(h->grp_n, rows.data() + 4 * nr, (size_t)ng * 4, hipMemcpyHostToDevice, st));
       TIMED(TANDEM_K_OTHER, launch_gather_i32(prompt_tokens, h->row_src, nr, h->row_tok, st));
       {
-        tandem_status s = forward_pair(h, nr, h->row_tok, h->row_slot, h->row_pos, nullptr, false);
+        FwdRows fr{nr, h->row_tok, h->row_slot, h->row_pos, nullptr};
+        fr.grp_row0 = h->grp_row0; fr.grp_n = h->grp_n; fr.n_groups = ng;
+        tandem_status s = forward_pair(h, fr, false);
         if (s != TANDEM_OK) return s;
       }
       for (int j = j0; j < j1; ++j) {
