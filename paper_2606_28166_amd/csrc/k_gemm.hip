@@ -40,7 +40,7 @@ constexpr int BK = kGemmBK;        // k-values per chunk
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
 
-template <int BMT, int BNT, int NST, int NWT = 4> struct GemmShape {
+template <int BMT, int BNT, int NST, int NWT = 4, bool A16 = false> struct GemmShape {
   static constexpr int NW = NWT;                      // waves per workgroup (4 or 8)
   static constexpr int BM = BMT;
   static constexpr int BN = BNT;                      // weight rows per tile (128 or 256)
@@ -50,10 +50,14 @@ template <int BMT, int BNT, int NST, int NWT = 4> struct GemmShape {
   static constexpr int MBW = MB / WM;                 // 32-row blocks per wave
   static constexpr int NBW = BN / 32 / WN;            // 32-column blocks per wave
   static constexpr int NS = NST;                      // ring stages
-  static constexpr int ASTAGE = BM * BK * 4;          // bytes of one activation stage (hi + lo)
+  static constexpr int PARTS = A16 ? 1 : 2;           // MFMA operand parts per activation (fp16, or hi + lo)
+  static constexpr int RB = BK * 2 * PARTS;           // bytes of one activation row per chunk
+  static constexpr int NPC = RB / 16;                 // 16-byte pieces per activation row
+  static constexpr int RPI = 64 / NPC;                // activation rows per 1 KB DMA instruction
+  static constexpr int ASTAGE = BM * RB;              // bytes of one activation stage
   static constexpr int WSTAGE = BN * BK * 2;          // bytes of one weight stage
   static constexpr int STAGE = ASTAGE + WSTAGE;
-  static constexpr int NA = BM / (4 * NW);            // activation DMA instructions per wave per chunk
+  static constexpr int NA = BM / (RPI * NW);          // activation DMA instructions per wave per chunk
   static constexpr int NWD = BN / (8 * NW);           // weight DMA instructions per wave per chunk
   static constexpr int WAIT = (NS - 2) * (NA + NWD);  // vmcnt that leaves NS - 2 chunks in flight
   static constexpr int OUT_COLS = BN / 2;             // SwiGLU output columns per tile
@@ -61,11 +65,19 @@ template <int BMT, int BNT, int NST, int NWT = 4> struct GemmShape {
   static_assert(NA >= 1 && NWD >= 1 && MBW >= 1 && NBW >= 1, "tile too small for the waves");
 };
 
-template <int BMT, int BNT, int NST, int EPI, int NWT>
+// PK: the weights come from the packed MFMA-fragment copy (pair-interleaved
+// for SwiGLU, like the tile rows below) instead of the row-major matrix: one
+// 1 KB fragment per DMA instruction, lane-contiguous fragment reads.  The
+// k-order inside a chunk then follows the packed layout (lane half g of k-step
+// j holds k-group 2 j + g).  A16: fp16 activations against fp16 packed weights
+// (PK only).
+template <int BMT, int BNT, int NST, int EPI, int NWT, bool PK = false, bool A16 = false>
 __global__ __launch_bounds__(64 * NWT) void gemm_mfma_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, int M, int N, int K, int cps,
     float* __restrict__ out, int ldo, long split_stride) {
-  using G = GemmShape<BMT, BNT, NST, NWT>;
+  using G = GemmShape<BMT, BNT, NST, NWT, A16>;
+  static_assert(PK || !A16, "fp16 activations need the fp16 packed weights");
+  constexpr int PARTS = G::PARTS, NPC = G::NPC;
   __shared__ __attribute__((aligned(1024))) unsigned char ring[G::NS * G::STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -92,32 +104,45 @@ __global__ __launch_bounds__(64 * NWT) void gemm_mfma_kernel(
   // DMA sources.  Weight stage: instruction i of wave w covers tile rows
   // (BN/NW) w + 8i .. +8 (128 B each); lane -> row (lane >> 3), physical
   // piece lane & 7 holding logical piece (lane & 7) ^ ((row >> 1) & 7).
+  // Packed weights: instruction i of wave w moves fragment f = NW i + w of
+  // the stage (32-row block f / 4 of the tile, k-step f % 4), 1 KB.
   const bf16_t* wsrc[G::NWD];
+  const int kfr = K / 16;                               // fragments per packed 32-row block
 #pragma unroll
   for (int i = 0; i < G::NWD; ++i) {
-    const int t = (G::BN / G::NW) * wave + 8 * i + (lane >> 3);
-    const int lp = (lane & 7) ^ ((t >> 1) & 7);
-    wsrc[i] = W + (size_t)wrow_of(t) * K + lp * 8;
+    if (PK) {
+      const int f = G::NW * i + wave;
+      const int blk = min(blockIdx.x * (G::BN / 32) + f / 4, ((EPI == EPI_SWIGLU ? 2 * N : N) + 31) / 32 - 1);
+      wsrc[i] = W + ((size_t)blk * kfr + f % 4) * 512 + lane * 8;
+    } else {
+      const int t = (G::BN / G::NW) * wave + 8 * i + (lane >> 3);
+      const int lp = (lane & 7) ^ ((t >> 1) & 7);
+      wsrc[i] = W + (size_t)wrow_of(t) * K + lp * 8;
+    }
   }
-  // Activation stage: instruction i of wave w covers tile rows 4 (NW i + w) .. +4
-  // (256 B each: 8 hi pieces and 8 lo pieces); physical piece lane & 15 holds
-  // logical piece (lane & 15) ^ (row & 15).
+  // Activation stage: instruction i of wave w covers tile rows RPI (NW i + w) ..
+  // +RPI - 1 (a row is NPC 16-byte pieces: split format 8 hi and 8 lo pieces,
+  // fp16 8 pieces); physical piece lane % NPC holds logical piece
+  // (lane % NPC) ^ (row % NPC).
   const bf16_t* asrc[G::NA];
 #pragma unroll
   for (int i = 0; i < G::NA; ++i) {
-    const int r = 4 * (G::NW * i + wave) + (lane >> 4);
-    const int lc = (lane & 15) ^ (r & 15);
-    asrc[i] = A + (size_t)min(m0 + r, M - 1) * 2 * (size_t)K + lc * 8;
+    const int r = G::RPI * (G::NW * i + wave) + lane / NPC;
+    const int lc = (lane % NPC) ^ (r % NPC);
+    asrc[i] = A + (size_t)min(m0 + r, M - 1) * PARTS * (size_t)K + lc * 8;
   }
   unsigned char* const ring0 = ring;
   auto issue = [&](int it) {
     const int c = kc0 + min(it, nloc - 1);
     unsigned char* st = ring0 + (it % G::NS) * G::STAGE;
 #pragma unroll
-    for (int i = 0; i < G::NA; ++i) load_lds16(asrc[i] + (size_t)c * 2 * BK, st + 4 * (G::NW * i + wave) * 256);
+    for (int i = 0; i < G::NA; ++i)
+      load_lds16(asrc[i] + (size_t)c * PARTS * BK, st + (G::NW * i + wave) * 1024);
 #pragma unroll
-    for (int i = 0; i < G::NWD; ++i)
-      load_lds16_nt(wsrc[i] + (size_t)c * BK, st + G::ASTAGE + ((G::BN / G::NW) * wave + 8 * i) * 128);
+    for (int i = 0; i < G::NWD; ++i) {
+      if (PK) load_lds16_nt(wsrc[i] + (size_t)c * 4 * 512, st + G::ASTAGE + (G::NW * i + wave) * 1024);
+      else load_lds16_nt(wsrc[i] + (size_t)c * BK, st + G::ASTAGE + ((G::BN / G::NW) * wave + 8 * i) * 128);
+    }
   };
 
   f32x16_t acc[G::MBW][G::NBW];
@@ -128,45 +153,55 @@ __global__ __launch_bounds__(64 * NWT) void gemm_mfma_kernel(
 
   const uint32_t ring_addr = lds_addr_of(ring);
   struct Frags {
-    u32x4_t a[G::MBW][2];
+    u32x4_t a[G::MBW][PARTS];
     u32x4_t w[G::NBW];
   };
-  // fragments of k-step j: k-group q = 4g + j of rows / columns c32 of each block
+  // fragments of k-step j: k-group q of rows / columns c32 of each block
+  // (q = 4 g + j for row-major weights, 2 j + g for packed ones)
   auto read_frags = [&](uint32_t st, int j, Frags& f) {
-    const int q = 4 * g + j;
+    const int q = PK ? 2 * j + g : 4 * g + j;
 #pragma unroll
     for (int mb = 0; mb < G::MBW; ++mb) {
       const int r = (wm * G::MBW + mb) * 32 + c32;
-      const uint32_t rowa = st + (uint32_t)(r * 256);
-      f.a[mb][0] = lds_read16(rowa + (uint32_t)(((2 * q) ^ (r & 15)) * 16));
-      f.a[mb][1] = lds_read16(rowa + (uint32_t)(((2 * q + 1) ^ (r & 15)) * 16));
+      const uint32_t rowa = st + (uint32_t)(r * G::RB);
+#pragma unroll
+      for (int part = 0; part < PARTS; ++part)
+        f.a[mb][part] = lds_read16(rowa + (uint32_t)(((PARTS * q + part) ^ (r % NPC)) * 16));
     }
 #pragma unroll
     for (int nb = 0; nb < G::NBW; ++nb) {
-      const int t = (wn * G::NBW + nb) * 32 + c32;
-      f.w[nb] = lds_read16(st + G::ASTAGE + (uint32_t)(t * 128 + ((q ^ ((t >> 1) & 7)) * 16)));
+      if (PK) {
+        const int blk = wn * G::NBW + nb;
+        f.w[nb] = lds_read16(st + G::ASTAGE + (uint32_t)((blk * 4 + j) * 1024 + lane * 16));
+      } else {
+        const int t = (wn * G::NBW + nb) * 32 + c32;
+        f.w[nb] = lds_read16(st + G::ASTAGE + (uint32_t)(t * 128 + ((q ^ ((t >> 1) & 7)) * 16)));
+      }
     }
   };
   auto fence = [&](Frags& f) {
 #pragma unroll
-    for (int mb = 0; mb < G::MBW; ++mb) {
-      lds_fence_value(f.a[mb][0]);
-      lds_fence_value(f.a[mb][1]);
-    }
+    for (int mb = 0; mb < G::MBW; ++mb)
+#pragma unroll
+      for (int part = 0; part < PARTS; ++part) lds_fence_value(f.a[mb][part]);
 #pragma unroll
     for (int nb = 0; nb < G::NBW; ++nb) lds_fence_value(f.w[nb]);
   };
-  // hi parts for every accumulator, then lo parts
+  // split format: hi parts for every accumulator, then lo parts
   auto mfma_step = [&](const Frags& f) {
 #pragma unroll
-    for (int part = 0; part < 2; ++part)
+    for (int part = 0; part < PARTS; ++part)
 #pragma unroll
       for (int mb = 0; mb < G::MBW; ++mb) {
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, f.a[mb][part]);
 #pragma unroll
-        for (int nb = 0; nb < G::NBW; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, f.w[nb]),
-                                                                acc[mb][nb], 0, 0, 0);
+        for (int nb = 0; nb < G::NBW; ++nb) {
+          if (A16)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, f.a[mb][part]),
+                                                                 __builtin_bit_cast(f16x8_t, f.w[nb]), acc[mb][nb], 0, 0, 0);
+          else
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, f.a[mb][part]),
+                                                                  __builtin_bit_cast(bf16x8_t, f.w[nb]), acc[mb][nb], 0, 0, 0);
+        }
       }
   };
 
@@ -210,8 +245,10 @@ __global__ __launch_bounds__(64 * NWT) void gemm_mfma_kernel(
           // columns 0..15 of the block are gate values, 16..31 the matching up values
           const float up = __shfl_xor(v, 16, 64);
           const int j = blockIdx.x * G::OUT_COLS + 16 * (wn * G::NBW + nb) + (c32 & 15);
-          if (m < M && c32 < 16 && j < N)
-            split_store(reinterpret_cast<bf16_t*>(out) + (size_t)m * 2 * ldo, j, silu(v) * up);
+          if (m < M && c32 < 16 && j < N) {
+            if (A16) reinterpret_cast<uint16_t*>(out)[(size_t)m * ldo + j] = f2h(silu(v) * up);
+            else split_store(reinterpret_cast<bf16_t*>(out) + (size_t)m * 2 * ldo, j, silu(v) * up);
+          }
         } else {
           const int n = blockIdx.x * G::BN + (wn * G::NBW + nb) * 32 + c32;
           if (m < M && n < N) out[blockIdx.z * split_stride + (size_t)m * ldo + n] = v;
@@ -278,19 +315,23 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(
     }
 }
 
-template <int BMT, int BNT, int NST, int EPI>
+template <int BMT, int BNT, int NST, int EPI, bool PK = false, bool A16 = false>
 hipError_t run_mfma(const GemmArgs& a, int S, int cps, hipStream_t st) {
   constexpr int NW = (BMT == 128) ? 8 : 4;    // 128-row tiles: two waves per SIMD
-  using G = GemmShape<BMT, BNT, NST, NW>;
+  using G = GemmShape<BMT, BNT, NST, NW, A16>;
   const int cols = (EPI == EPI_SWIGLU) ? G::OUT_COLS : G::BN;
   dim3 grid((a.N + cols - 1) / cols, (a.M + BMT - 1) / BMT, S);
-  hipLaunchKernelGGL((gemm_mfma_kernel<BMT, BNT, NST, EPI, NW>), grid, dim3(64 * NW), 0, st, (const bf16_t*)a.A,
-                     (const bf16_t*)a.W, a.M, a.N, a.K, cps, a.out, a.ldo, a.split_stride);
+  hipLaunchKernelGGL((gemm_mfma_kernel<BMT, BNT, NST, EPI, NW, PK, A16>), grid, dim3(64 * NW), 0, st,
+                     (const bf16_t*)a.A, (const bf16_t*)(PK ? a.Wp : a.W), a.M, a.N, a.K, cps, a.out, a.ldo,
+                     a.split_stride);
   return hipGetLastError();
 }
 
 template <int EPI>
 hipError_t dispatch_mfma(const GemmArgs& a, int S, int cps, hipStream_t st) {
+  if (a.Wp && a.M > 64)
+    return a.a16 ? run_mfma<128, 128, 3, EPI, true, true>(a, S, cps, st)
+                 : run_mfma<128, 128, 3, EPI, true, false>(a, S, cps, st);
   if (a.M <= 32) return run_mfma<32, 128, 4, EPI>(a, S, cps, st);
   if (a.M <= 64) return run_mfma<64, 128, 4, EPI>(a, S, cps, st);
   return run_mfma<128, 128, 3, EPI>(a, S, cps, st);
@@ -317,6 +358,9 @@ hipError_t launch_gemm(const GemmArgs& a, int* splits_used, hipStream_t st) {
   }
   int S = a.epi == EPI_PARTIAL ? (a.splits < 1 ? 1 : a.splits) : 1;
   const bool mfma = (a.dt == DT_BF16) && (a.K % BK == 0);
+  // packed weights take 128-row tiles (M > 64); fp16 activations need them
+  if ((a.a16 && (!a.Wp || a.M <= 64)) || (a.Wp && (!mfma || (a.epi == EPI_SWIGLU && a.N % 16))))
+    return hipErrorInvalidValue;
   if (mfma) {
     const int nch = a.K / BK;
     if (S > nch) S = nch;

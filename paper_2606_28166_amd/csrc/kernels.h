@@ -18,8 +18,10 @@ enum Epi { EPI_PARTIAL = 0, EPI_STORE = 1, EPI_SWIGLU = 2 };
 // actually used (may be lower when K is short).
 struct GemmArgs {
   int dt;                 // weight dtype
-  const void* A;          // activations [M][K] (split for bf16 weights, else fp32)
+  const void* A;          // activations [M][K] (split for bf16 weights, else fp32; fp16 when a16)
   const void* W;          // weights [rows][K]
+  const void* Wp;         // the packed copy of W (bf16 models, M > 64), or NULL
+  bool a16;               // fp16 activations against an fp16 packed copy (Wp required)
   int M, N, K;
   int epi;
   float* out;             // EPI_SWIGLU: activation rows of width ldo (split for bf16)

@@ -387,9 +387,9 @@ tandem_status gemm(tandem_handle* h, const Model& m, const void* A, const void* 
     TIMED(TANDEM_K_GEMM, launch_gemm_stream(a, st));
     return TANDEM_OK;
   }
-  if (a16) return fail(&h->err, TANDEM_E_UNSUPPORTED, "fp16 activations off the streaming GEMM");
   GemmArgs g{};
   g.dt = dt; g.A = A; g.W = W; g.M = M; g.N = N; g.K = K; g.epi = epi;
+  g.Wp = Wp; g.a16 = a16;                  // prefill-sized products read the packed copy too
   g.out = out; g.ldo = N; g.split_stride = (long)M * N;
   g.splits = epi == EPI_PARTIAL ? choose_splits(M, N, K, m.p.ws_floats, h->n_cu) : 1;
   TIMED(TANDEM_K_GEMM, launch_gemm(g, S, st));
@@ -419,18 +419,25 @@ tandem_status gate_up(tandem_handle* h, const Model& m, const Layer& L, int M, h
     }
     return TANDEM_OK;
   }
+  // prefill-sized: the tiled GEMM on the packed (pair-interleaved) copy when
+  // there is one, fp16 activations with it (the partial columns then follow
+  // the interleaved order)
   int S = 1;
+  const bool pk = L.p_gate_up != nullptr && M > 64;
+  const bool a16 = pk && m.ffn16;
   if (split_gate_up(&c)) {
     GemmArgs g{};
     g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = M; g.N = 2 * F; g.K = d; g.epi = EPI_PARTIAL;
+    g.Wp = pk ? L.p_gate_up : nullptr; g.a16 = a16;
     g.out = m.ws; g.ldo = 2 * F; g.split_stride = (long)M * 2 * F;
     g.splits = choose_splits(M, 2 * F, d, m.p.ws_floats, h->n_cu);
     TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
-    TIMED(TANDEM_K_OTHER, launch_swiglu_finish(m.ws, S, (long)M * 2 * F, M, F, false, false, m.xf, st));
+    TIMED(TANDEM_K_OTHER, launch_swiglu_finish(m.ws, S, (long)M * 2 * F, M, F, pk, a16, m.xf, st));
     return TANDEM_OK;
   }
   GemmArgs g{};
   g.dt = dt; g.A = m.xa; g.W = L.w_gate_up; g.M = M; g.N = F; g.K = d; g.epi = EPI_SWIGLU;
+  g.Wp = pk ? L.p_gate_up : nullptr; g.a16 = a16;
   g.out = (float*)m.xf; g.ldo = F; g.splits = 1;
   TIMED(TANDEM_K_GEMM, launch_gemm(g, &S, st));
   return TANDEM_OK;
@@ -497,9 +504,10 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   aa.grp_row0 = fr.grp_row0; aa.grp_n = fr.grp_n; aa.n_groups = fr.n_groups;
   TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
 
-  // the FFN's activations are fp16 when both its products stream (the
+  // the FFN's activations are fp16 when both its products have fp16 packed
+  // copies (the streaming GEMM up to 128 rows, the tiled one above; the
   // output of the last layer's norm feeds the LM head only)
-  const bool f16 = m.ffn16 && R <= kStreamMaxRows;
+  const bool f16 = m.ffn16;
   const bool last = l + 1 == c.n_layers;
   CALL(gemm(h, m, m.xa, L.w_o, L.p_o, R, d, att, EPI_PARTIAL, m.ws, &S, st));
   TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, L.ffn_norm, c.rms_eps, m.xa, R, d, f16, st));
@@ -507,7 +515,7 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   CALL(gate_up(h, m, L, R, st));
   CALL(gemm(h, m, m.xf, L.w_down, L.p_down, R, d, c.ffn_dim, EPI_PARTIAL, m.ws, &S, st, f16));
   const float* next_gain = last ? m.final_norm : m.layers[l + 1].attn_norm;
-  const bool next16 = last && m.lm16 && R <= kStreamMaxRows;
+  const bool next16 = last && m.lm16;
   TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, next_gain, c.rms_eps, m.xa, R, d, next16, st));
   return TANDEM_OK;
 }
@@ -515,8 +523,7 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
 tandem_status forward_head(tandem_handle* h, Model& m, const FwdRows& fr, hipStream_t st) {
   const tandem_model_cfg& c = m.cfg;
   int S = 1;
-  CALL(gemm(h, m, m.xa, m.lm_head, m.p_lm, fr.R, c.vocab, c.d_model, EPI_STORE, m.logits, &S, st,
-            m.lm16 && fr.R <= kStreamMaxRows));
+  CALL(gemm(h, m, m.xa, m.lm_head, m.p_lm, fr.R, c.vocab, c.d_model, EPI_STORE, m.logits, &S, st, m.lm16));
   return TANDEM_OK;
 }
 
