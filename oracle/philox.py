@@ -14,7 +14,7 @@ from that published description:
   * between rounds the key is bumped by the Weyl constants;
   * Philox4x32-10 runs 10 rounds with 32-bit words.
 
-Counter layout of this build (no counterpart in the paper):
+Counter layout used by the library and this oracle (the paper fixes none):
   key = (seed mod 2^32, seed >> 32)
   sampling noise for vocab entry v:  ctr = (v >> 2, t, s, 0), word v & 3
   handoff coin:                      ctr = (0,      t, s, 1), word 0
