@@ -121,11 +121,6 @@ struct QkvPostArgs {
 };
 hipError_t launch_qkv_post(const QkvPostArgs& a, hipStream_t st);
 
-// QKV post-processing folded into decode attention (ws != NULL): the
-// attention workgroup of (kv head, row) sums its heads' split-K partials,
-// normalises and rotates q and k, appends k and v to the cache and keeps q
-// in LDS.  Only for decode rows (distinct cache slots) on the MFMA path.
-
 // Decode/prefill attention of every row's query heads over positions
 // 0..row_pos[r] of its slot; out[r][h * hd + d] (an activation row of width
 // nq * hd, split for bf16 models).
