@@ -239,6 +239,9 @@ struct tandem_handle {
   // runs on a second stream forked from and joined back into `stream`.
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  // one event per layer of each model, recorded after that layer's attention
+  // launch (the two streams' attentions take turns, see forward_pair)
+  std::vector<hipEvent_t> ev_att[2];
   // Step graphs are captured on and replayed on a stream of the library's own
   // (the caller's may be the legacy null stream, which cannot be captured),
   // ordered after and before the caller's stream by a pair of events.
@@ -471,7 +474,10 @@ tandem_status forward_embed(tandem_handle* h, Model& m, const FwdRows& fr, hipSt
   return TANDEM_OK;
 }
 
-tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr, hipStream_t st) {
+// att_wait: an event the layer's attention waits for first (NULL: none);
+// att_done: recorded right after the attention launch (NULL: none).
+tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr, hipStream_t st,
+                            hipEvent_t att_wait = nullptr, hipEvent_t att_done = nullptr) {
   const tandem_model_cfg& c = m.cfg;
   const int dt = c.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32;
   const int d = c.d_model, hd = c.head_dim, nq = c.n_q_heads, nkv = c.n_kv_heads;
@@ -502,7 +508,9 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   aa.dt = dt; aa.q = m.q; aa.R = R; aa.nq = nq; aa.nkv = nkv; aa.hd = hd; aa.cache = cg;
   aa.row_slot = fr.slot; aa.row_pos = fr.pos; aa.row_done = fr.done; aa.out = m.xa;
   aa.grp_row0 = fr.grp_row0; aa.grp_n = fr.grp_n; aa.n_groups = fr.n_groups;
+  if (att_wait) HIPCHK(hipStreamWaitEvent(st, att_wait, 0));
   TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
+  if (att_done) HIPCHK(hipEventRecord(att_done, st));
 
   // the FFN's activations are fp16 when both its products have fp16 packed
   // copies (the streaming GEMM up to 128 rows, the tiled one above; the
@@ -536,6 +544,13 @@ tandem_status forward(tandem_handle* h, Model& m, const FwdRows& fr, bool lm_hea
 
 // Both models' forwards over the same rows: the junior on the side stream,
 // the senior on the main stream, joined before anything that reads either.
+// The two models' decode attentions are bound by HBM bandwidth, their
+// projections mostly by latency: the step runs both forwards on two streams
+// and lets the attention launches take turns, so each model's attention runs
+// beside the other model's projections rather than beside its attention.
+// The turn order interleaves the layers evenly (layer l of a model with L
+// layers at (l + 1/2) / L); an attention waits for the previous attention of
+// the other model in that order.
 tandem_status forward_pair(tandem_handle* h, const FwdRows& fr, bool lm_head) {
   hipStream_t st = h->stream;
   if (h->timing & TANDEM_TIMING_SERIAL) {
@@ -544,8 +559,30 @@ tandem_status forward_pair(tandem_handle* h, const FwdRows& fr, bool lm_head) {
   }
   HIPCHK(hipEventRecord(h->ev_fork, st));
   HIPCHK(hipStreamWaitEvent(h->side, h->ev_fork, 0));
-  CALL(forward(h, h->m[1], fr, lm_head, h->side));
-  CALL(forward(h, h->m[0], fr, lm_head, st));
+  hipStream_t sts[2] = {st, h->side};
+  Model* ms[2] = {&h->m[0], &h->m[1]};
+  {
+    const int L[2] = {ms[0]->cfg.n_layers, ms[1]->cfg.n_layers};
+    CALL(forward_embed(h, *ms[0], fr, sts[0]));
+    CALL(forward_embed(h, *ms[1], fr, sts[1]));
+    int next[2] = {0, 0}, prev_model = -1, prev_layer = -1;
+    while (next[0] < L[0] || next[1] < L[1]) {
+      // the model whose next layer comes first in the interleaved order
+      int i;
+      if (next[0] >= L[0]) i = 1;
+      else if (next[1] >= L[1]) i = 0;
+      else i = (2 * next[0] + 1) * (long)L[1] <= (2 * next[1] + 1) * (long)L[0] ? 0 : 1;
+      const int l = next[i]++;
+      hipEvent_t wait = (prev_model >= 0 && prev_model != i) ? h->ev_att[prev_model][prev_layer] : nullptr;
+      CALL(forward_layer(h, *ms[i], l, fr, sts[i], wait, h->ev_att[i][l]));
+      prev_model = i;
+      prev_layer = l;
+    }
+    if (lm_head) {
+      CALL(forward_head(h, *ms[1], fr, sts[1]));
+      CALL(forward_head(h, *ms[0], fr, sts[0]));
+    }
+  }
   HIPCHK(hipEventRecord(h->ev_join, h->side));
   HIPCHK(hipStreamWaitEvent(st, h->ev_join, 0));
   return TANDEM_OK;
@@ -824,6 +861,8 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   auto bail = [&](hipError_t e, const char* what) {
     std::string msg = std::string("HIP error in tandem_init (") + what + "): " + hipGetErrorString(e);
     if (h->h_count) (void)hipHostFree(h->h_count);
+    for (int i = 0; i < 2; ++i)
+      for (hipEvent_t ev : h->ev_att[i]) (void)hipEventDestroy(ev);
     if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
     if (h->ev_join) (void)hipEventDestroy(h->ev_join);
     if (h->side) (void)hipStreamDestroy(h->side);
@@ -855,6 +894,13 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   if (e != hipSuccess) { h->ev_in = nullptr; return bail(e, "graph entry event"); }
   e = hipEventCreateWithFlags(&h->ev_out, hipEventDisableTiming);
   if (e != hipSuccess) { h->ev_out = nullptr; return bail(e, "graph exit event"); }
+  for (int i = 0; i < 2; ++i)
+    for (int l = 0; l < h->m[i].cfg.n_layers; ++l) {
+      hipEvent_t ev;
+      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (e != hipSuccess) return bail(e, "attention event");
+      h->ev_att[i].push_back(ev);
+    }
   for (int i = 0; i < 2; ++i) {
     e = launch_rope_table(h->m[i].cfg.rope_theta, h->m[i].cfg.head_dim, P.ctx_stride, h->m[i].rope, h->stream);
     if (e != hipSuccess) return bail(e, "rope table");
@@ -1064,6 +1110,8 @@ void tandem_destroy(tandem_handle* h) {
   if (h->gstream) (void)hipStreamSynchronize(h->gstream);
   drop_graphs(h);
   for (hipEvent_t e : h->ev_pool) (void)hipEventDestroy(e);
+  for (int i = 0; i < 2; ++i)
+    for (hipEvent_t e : h->ev_att[i]) (void)hipEventDestroy(e);
   if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   if (h->ev_join) (void)hipEventDestroy(h->ev_join);
   if (h->side) (void)hipStreamDestroy(h->side);
