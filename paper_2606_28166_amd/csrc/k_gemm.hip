@@ -5,11 +5,11 @@
 //   * A holds the activations in split format (per 8 values: 8 bf16 high
 //     parts, then 8 bf16 low parts), so every weight fragment meets hi and lo
 //     in two MFMAs: fp32-level activations, bf16 weights, fp32 accumulation.
-//   * One workgroup computes a BM x 128 output tile (BM in {32, 64, 128})
-//     over its slice of K, 64 k-values per chunk.  With BM = 128 its 8 waves
-//     (two per SIMD, so one issues MFMAs while the other waits on LDS) tile
-//     the 32 x 32 MFMA blocks 4 x 2; smaller tiles use 4 waves (2 x 2, or
-//     1 x 4 when BM = 32).  The 32 x 32 x 16 shape keeps the matrix cores
+//   * One workgroup computes a BM x BN output tile (BM in {32, 64, 128, 256},
+//     BN 128 or 256) over its slice of K, 64 k-values per chunk.  With BM >=
+//     128 its 8 waves (two per SIMD, so one issues MFMAs while the other
+//     waits on LDS) tile the 32 x 32 MFMA blocks 4 x 2; smaller tiles use 4
+//     waves (2 x 2, or 1 x 4 when BM = 32).  The 32 x 32 x 16 shape keeps the matrix cores
 //     near their peak with only a few accumulators per wave.
 //   * Weight rows and activation rows of each chunk stream into an NS-stage
 //     LDS ring with global_load_lds_dwordx4 (no register staging); 16-byte
@@ -317,7 +317,7 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(
 
 template <int BMT, int BNT, int NST, int EPI, bool PK = false, bool A16 = false>
 hipError_t run_mfma(const GemmArgs& a, int S, int cps, hipStream_t st) {
-  constexpr int NW = (BMT == 128) ? 8 : 4;    // 128-row tiles: two waves per SIMD
+  constexpr int NW = (BMT >= 128) ? 8 : 4;    // 128-row and larger tiles: two waves per SIMD
   using G = GemmShape<BMT, BNT, NST, NW, A16>;
   const int cols = (EPI == EPI_SWIGLU) ? G::OUT_COLS : G::BN;
   dim3 grid((a.N + cols - 1) / cols, (a.M + BMT - 1) / BMT, S);
@@ -329,9 +329,20 @@ hipError_t run_mfma(const GemmArgs& a, int S, int cps, hipStream_t st) {
 
 template <int EPI>
 hipError_t dispatch_mfma(const GemmArgs& a, int S, int cps, hipStream_t st) {
-  if (a.Wp && a.M > 64)
-    return a.a16 ? run_mfma<128, 128, 3, EPI, true, true>(a, S, cps, st)
-                 : run_mfma<128, 128, 3, EPI, true, false>(a, S, cps, st);
+  if (a.Wp && a.M > 64) {
+    // Per MFMA a wave of a 128 x 128 tile reads 1.25 KB of fragments from LDS
+    // (fp16: 1 activation + 4 weight fragments for 4 MFMAs), more than the LDS
+    // delivers at the matrix cores' rate.  A 256 x 256 fp16 tile (2 + 4
+    // fragments for 8 MFMAs) and a 128 x 256 split tile (hi and lo: 2 + 4 for
+    // 8) need 0.75 KB, but their grids fill the 256 CUs only for large M x N.
+    const int rows = EPI == EPI_SWIGLU ? 2 * a.N : a.N;
+    auto tiles = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((rows + bn - 1) / bn) * S; };
+    if (a.a16)
+      return tiles(256, 256) >= 128 ? run_mfma<256, 256, 2, EPI, true, true>(a, S, cps, st)
+                                    : run_mfma<128, 128, 3, EPI, true, true>(a, S, cps, st);
+    return tiles(128, 256) >= 256 ? run_mfma<128, 256, 2, EPI, true, false>(a, S, cps, st)
+                                  : run_mfma<128, 128, 3, EPI, true, false>(a, S, cps, st);
+  }
   if (a.M <= 32) return run_mfma<32, 128, 4, EPI>(a, S, cps, st);
   if (a.M <= 64) return run_mfma<64, 128, 4, EPI>(a, S, cps, st);
   return run_mfma<128, 128, 3, EPI>(a, S, cps, st);
