@@ -9,11 +9,15 @@ prefill of both models on every prompt, then max_new tandem decode steps
 Prints ONE JSON line:
   value            co-generated tokens / s over the whole job (prefill + decode)
   roofline         decode attention (the dominant kernel): algorithmic K/V
-                   bytes per launch / its average launch time, from HIP event
-                   pairs around every launch (on the stream it runs on) in an
+                   bytes per attention call / its average time, from HIP event
+                   pairs around every call (on the stream it runs on) in an
                    extra rollout whose two forwards run one after the other, so
-                   each launch has the GPU to itself; the per-class breakdown
-                   comes from the same rollout
+                   each call has the GPU to itself; the per-class breakdown
+                   comes from the same rollout.  A call is one launch, or two
+                   when the G sequences of a prompt share its K/V prefix (a
+                   pass over the prefix for blocks of rows, then the per-row
+                   pass); the algorithmic bytes then count the prefix once per
+                   group
   roofline_concurrent the same in the two-stream schedule of the timed region
                    (the junior's forward overlapping the senior's)
   (the timed region replays the captured step graph; graph-captured event
@@ -69,33 +73,54 @@ def weight_bytes(s: W.ModelShape) -> int:
     return esz * (body + d * s.vocab)
 
 
-def _active(plens, group, lengths, t):
-    """Prompt length of every sequence still generating at decode step t
-    (lengths: tokens each sequence generated; None: all run every step)."""
-    rows = [p for p in plens for _ in range(group)]
-    if lengths is None:
-        return rows
-    return [P for P, n in zip(rows, lengths) if t <= n]
+def shares_prefix(wl: W.Workload) -> bool:
+    """Whether decode attention reads a prompt's K/V prefix once per group of
+    its G sequences (bf16 models, head_dim 64 or 128, at most 8 query heads per
+    kv head, G > 1), as the library decides at prefill."""
+    def ok(s):
+        g = s.n_q_heads // s.n_kv_heads
+        return s.dtype == "bf16" and s.head_dim in (64, 128) and g in (1, 2, 4, 8) and s.n_q_heads % s.n_kv_heads == 0
+    return wl.group > 1 and ok(wl.senior) and ok(wl.junior)
+
+
+def _context_positions(wl: W.Workload, plens, t: int, lengths=None):
+    """(active rows, K/V positions decode step t must read per layer of a model).
+    Row r of prompt j attends positions 0 .. P_j + t - 2.  With a shared prefix
+    the first lo_j = (P_j - 1) rounded down to 16 positions count once per group
+    with an active row, the rest once per row; otherwise every row counts its
+    whole context (lengths: tokens each sequence generated; None: all run every
+    step)."""
+    share = shares_prefix(wl)
+    n_rows, pos = 0, 0
+    for j, P in enumerate(plens):
+        act = wl.group if lengths is None else sum(1 for i in range(wl.group) if t <= lengths[j * wl.group + i])
+        if act == 0:
+            continue
+        lo = (P - 1) // 16 * 16 if share else 0
+        n_rows += act
+        pos += lo + act * (P + t - 1 - lo)
+    return n_rows, pos
 
 
 def decode_step_bytes(wl: W.Workload, plens, t: int, lengths=None) -> int:
-    """Bytes the decode step t must move: both models' weights once, every active
-    row's K/V context for both models, the K/V append and the embedding rows."""
-    rows = _active(plens, wl.group, lengths, t)
-    if not rows:
+    """Bytes the decode step t must move: both models' weights once, the K/V
+    context of every active row for both models (a shared prompt prefix once
+    per group), the K/V append and the embedding rows."""
+    n_rows, pos = _context_positions(wl, plens, t, lengths)
+    if n_rows == 0:
         return 0
     kv = kv_bytes_per_token(wl.senior) + kv_bytes_per_token(wl.junior)
     esz_s = 2 if wl.senior.dtype == "bf16" else 4
     esz_j = 2 if wl.junior.dtype == "bf16" else 4
-    ctx = sum(P + t - 1 for P in rows)
-    return (weight_bytes(wl.senior) + weight_bytes(wl.junior) + ctx * kv + len(rows) * kv
-            + len(rows) * (esz_s * wl.senior.d_model + esz_j * wl.junior.d_model))
+    return (weight_bytes(wl.senior) + weight_bytes(wl.junior) + pos * kv + n_rows * kv
+            + n_rows * (esz_s * wl.senior.d_model + esz_j * wl.junior.d_model))
 
 
 def attention_bytes(wl: W.Workload, plens, steps: int, lengths=None) -> int:
-    """K/V bytes the decode attention kernels read over `steps` decode steps."""
+    """K/V bytes the decode attention must read over `steps` decode steps (a
+    shared prompt prefix once per group)."""
     kv = kv_bytes_per_token(wl.senior) + kv_bytes_per_token(wl.junior)
-    return sum(kv * (P + t - 1) for t in range(1, steps + 1) for P in _active(plens, wl.group, lengths, t))
+    return sum(kv * _context_positions(wl, plens, t, lengths)[1] for t in range(1, steps + 1))
 
 
 def prefill_flops(wl: W.Workload, plens) -> float:
@@ -248,7 +273,7 @@ def main():
         nbytes = attention_bytes(wl, plens, L, lengths)
         gbs = nbytes / (ms / 1e3) / 1e9
         per = nbytes / max(nl, 1)
-        return {"bound": "hbm", "kernel": "decode attention (both models)", "achieved": round(gbs, 1),
+        return {"bound": "hbm", "kernel": "decode attention (both models; per call a shared-prefix pass and a per-row pass)" if shares_prefix(wl) else "decode attention (both models)", "achieved": round(gbs, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                 "traffic": None if traffic_ratio is None else int(per * traffic_ratio),
                 "launches": nl, "avg_launch_us": round(ms * 1e3 / max(nl, 1), 2),
@@ -259,12 +284,12 @@ def main():
         _, d_ser, tr = rollout_once(0b1111 | LIB.TIMING_SERIAL)
         breakdown = {k: {"ms": round(v[0], 3), "launches": v[1]} for k, v in tr.items()}
         roof = roofline_of(tr["attention"], "one rollout's decode steps, the two forwards serialized and launched "
-                                            "from the host, a HIP event pair around every launch")
+                                            "from the host, a HIP event pair around every attention call")
         log(f"[bench] serialized rollout: decode {d_ser:.1f} ms, attention {tr['attention'][0]:.1f} ms / "
             f"{tr['attention'][1]} launches -> {roof['achieved']:.0f} GB/s")
         _, d_con, tr = rollout_once(1 << LIB.K_ATTENTION)
         roof_conc = roofline_of(tr["attention"], "one rollout's decode steps in the two-stream schedule, launched "
-                                                 "from the host, a HIP event pair around every attention launch")
+                                                 "from the host, a HIP event pair around every attention call")
         log(f"[bench] concurrent instrumented rollout: decode {d_con:.1f} ms, attention -> {roof_conc['achieved']:.0f} GB/s")
 
     cpu = None

@@ -164,18 +164,33 @@ __device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, con
 // 16 / GQA): ROWS consecutive rows of one prompt share the workgroup, query
 // column c = (row c / GQA, head c % GQA), each with its own causal limit; the
 // workgroup streams the positions its last row attends, so a prompt's K/V is
-// read once per ROWS rows rather than once per row.
-template <int HD, int GQA, int ROWS>
+// read once per ROWS rows rather than once per row.  Row groups of at most 16
+// rows are split over sub_per_grp workgroups of ROWS rows.
+//
+// Shared prompt prefix (decode rows of one prompt's G sequences): the
+// softmax over positions [0, n) splits exactly into two partial softmaxes
+// over [0, lo) and [lo, n), each carried as (running max M, sum of
+// exponentials, unnormalised weighted sum of V), merged by rescaling both to
+// the larger max:
+//   * PREFIX (ROWS > 1, the prefix pass): every column attends positions
+//     [0, row_pos + 1) of the group's source slot and the workgroup writes its
+//     column's partial (HD weighted sums, then M and the sum) to
+//     part[row][head][HD + 2] instead of an output row;
+//   * ROWS = 1 with row_lo != NULL (the suffix pass): the row attends positions
+//     [row_lo[r], pos] of its own slot (row_lo a multiple of 16) and, when
+//     row_lo[r] > 0, merges the prefix partial of its row before normalising.
+template <int HD, int GQA, int ROWS, bool PREFIX = false>
 __global__ __launch_bounds__(256) void attn_mfma_kernel(
     const float* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     int ctx_stride, long slot_stride, const int32_t* __restrict__ row_slot,
     const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
-    const int32_t* __restrict__ grp_row0, const int32_t* __restrict__ grp_n,
-    bf16_t* __restrict__ out, int nq) {
+    const int32_t* __restrict__ grp_row0, const int32_t* __restrict__ grp_n, int sub_per_grp,
+    const int32_t* __restrict__ row_lo, float* __restrict__ part, bf16_t* __restrict__ out, int nq) {
   constexpr int DC = HD / 32;     // k-steps of the S product
   constexpr int DB = HD / 16;     // 16-dim blocks of the O product
   constexpr int NCOL = GQA * ROWS;
   static_assert(NCOL <= 16, "16 query columns per workgroup");
+  static_assert(!PREFIX || ROWS > 1, "the prefix pass serves several rows");
   __shared__ float sm_m[4][16];
   __shared__ float sm_l[4][16];
   __shared__ float sm_o[4][NCOL][HD];
@@ -183,11 +198,11 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   const int kh = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
-  // rows r0 .. r0 + nr - 1 (16-row groups of one prompt, split in 16 / ROWS)
+  // rows r0 .. r0 + nr - 1 (groups of at most 16 rows of one prompt, split in
+  // sub_per_grp blocks of ROWS)
   int r0 = blockIdx.y, nr = 1;
   if (ROWS > 1) {
-    constexpr int SUB = 16 / ROWS;
-    const int grp = blockIdx.y / SUB, sub = blockIdx.y % SUB;
+    const int grp = blockIdx.y / sub_per_grp, sub = blockIdx.y % sub_per_grp;
     r0 = grp_row0[grp] + sub * ROWS;
     nr = min(ROWS, grp_n[grp] - sub * ROWS);
     if (nr <= 0) return;
@@ -209,11 +224,14 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   const __amdgpu_buffer_rsrc_t vr = buf_rsrc(vc + plane, (uint32_t)ctx_stride * HD * 2);
   const float scale = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
 
-  // Wave w owns chunks w, w + 4, w + 8, ... of the stream; its first chunk
-  // is requested before the query is read.
-  const int nchunk = (ctx_max + 15) >> 4;
+  // positions before lo belong to the shared prefix (suffix pass only)
+  const int lo = (ROWS == 1 && row_lo) ? row_lo[r0] : 0;
+  const int c0 = lo >> 4;
+  // Wave w owns chunks c0 + w, c0 + w + 4, ... of the stream; its first
+  // chunk is requested before the query is read.
+  const int nchunk = ((ctx_max + 15) >> 4) - c0;
   const int nmine = nchunk > wave ? (nchunk - wave + 3) >> 2 : 0;
-  auto chunk_at = [&](int i) { return wave + 4 * min(i, nmine - 1); };
+  auto chunk_at = [&](int i) { return c0 + wave + 4 * min(i, nmine - 1); };
   KV16<HD> ca, cb;
   if (nmine > 0) load_chunk<HD>(ca, kr, vr, chunk_at(0), lane);
 
@@ -270,18 +288,38 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
       if (h < NCOL) sm_o[wave][h][db * 16 + c16] = st.o[db][i];
     }
   __syncthreads();
+  const bool merge = ROWS == 1 && lo > 0;
   for (int e = tid; e < NCOL * HD; e += 256) {
     const int h = e / HD, d = e % HD;
     if (h / GQA >= nr) continue;
     float M = sm_m[0][h];
 #pragma unroll
     for (int w = 1; w < 4; ++w) M = fmaxf(M, sm_m[w][h]);
+    float* pp = (PREFIX || merge) ? part + ((size_t)(r0 + h / GQA) * nq + kh * GQA + h % GQA) * (HD + 2) : nullptr;
+    float pm = -INFINITY;
+    if (merge) {
+      pm = pp[HD];
+      M = fmaxf(M, pm);
+    }
     float num = 0.f, den = 0.f;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const float f = exp2f(sm_m[w][h] - M);
       num += sm_o[w][h][d] * f;
       den += sm_l[w][h] * f;
+    }
+    if (PREFIX) {                      // the partial, relative to M
+      pp[d] = num;
+      if (d == 0) {
+        pp[HD] = M;
+        pp[HD + 1] = den;
+      }
+      continue;
+    }
+    if (merge) {
+      const float f = exp2f(pm - M);
+      num += pp[d] * f;
+      den += pp[HD + 1] * f;
     }
     bf16_t* orow = out + (size_t)(r0 + h / GQA) * 2 * nq * HD;
     split_store(orow, col0 + (h % GQA) * HD + d, num / den);
@@ -350,16 +388,27 @@ __global__ __launch_bounds__(128) void attn_valu_kernel(
 template <int HD, int GQA>
 hipError_t run_mfma(const AttnArgs& a, hipStream_t st) {
   constexpr int ROWS = 16 / GQA;
-  if (ROWS > 1 && a.grp_row0) {
-    hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, (ROWS > 1 ? ROWS : 1)>), dim3(a.nkv, a.n_groups * (16 / ROWS)),
-                       dim3(256), 0, st, a.q, (const bf16_t*)a.cache.k, (const bf16_t*)a.cache.v, a.cache.ctx_stride,
-                       a.cache.slot_stride, a.row_slot, a.row_pos, a.row_done, a.grp_row0, a.grp_n, (bf16_t*)a.out,
-                       a.nq);
+  constexpr int RB = ROWS > 1 ? ROWS : 1;
+  const bf16_t* kc = (const bf16_t*)a.cache.k;
+  const bf16_t* vc = (const bf16_t*)a.cache.v;
+  if (ROWS > 1 && a.grp_row0) {         // prompt rows
+    hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, RB>), dim3(a.nkv, a.n_groups * (16 / RB)), dim3(256), 0, st, a.q,
+                       kc, vc, a.cache.ctx_stride, a.cache.slot_stride, a.row_slot, a.row_pos, a.row_done, a.grp_row0,
+                       a.grp_n, 16 / RB, (const int32_t*)nullptr, (float*)nullptr, (bf16_t*)a.out, a.nq);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, 1>), dim3(a.nkv, a.R), dim3(256), 0, st, a.q,
-                     (const bf16_t*)a.cache.k, (const bf16_t*)a.cache.v, a.cache.ctx_stride, a.cache.slot_stride,
-                     a.row_slot, a.row_pos, a.row_done, (const int32_t*)nullptr, (const int32_t*)nullptr,
+  if (a.part) {                         // decode rows with a shared prompt prefix: the prefix pass first
+    if (ROWS == 1) return hipErrorInvalidValue;
+    const int sub = (a.pfx_rows + RB - 1) / RB;
+    if (a.pfx_groups > 0)
+      hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, RB, true>), dim3(a.nkv, a.pfx_groups * sub), dim3(256), 0, st, a.q,
+                         kc, vc, a.cache.ctx_stride, a.cache.slot_stride, a.pfx_slot, a.pfx_pos,
+                         (const int32_t*)nullptr, a.pfx_row0, a.pfx_n, sub, (const int32_t*)nullptr, a.part,
+                         (bf16_t*)nullptr, a.nq);
+  }
+  hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, 1>), dim3(a.nkv, a.R), dim3(256), 0, st, a.q, kc, vc,
+                     a.cache.ctx_stride, a.cache.slot_stride, a.row_slot, a.row_pos, a.row_done,
+                     (const int32_t*)nullptr, (const int32_t*)nullptr, 1, a.part ? a.row_lo : nullptr, a.part,
                      (bf16_t*)a.out, a.nq);
   return hipGetLastError();
 }
@@ -381,6 +430,8 @@ hipError_t dispatch_gqa(const AttnArgs& a, int gqa, hipStream_t st) {
 bool attention_has_mfma(int dt, int hd, int gqa) {
   return dt == DT_BF16 && (hd == 64 || hd == 128) && (gqa == 1 || gqa == 2 || gqa == 4 || gqa == 8 || gqa == 16);
 }
+
+bool attention_shares_prefix(int dt, int hd, int gqa) { return attention_has_mfma(dt, hd, gqa) && gqa <= 8; }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st) {
   if (a.R <= 0) return hipSuccess;

@@ -383,20 +383,21 @@ __global__ __launch_bounds__(64) void sample_finish_kernel(FinishArgs a) {
 template <typename T>
 __global__ __launch_bounds__(kNT) void kv_replicate_kernel(T* kc, T* vc, int nkv, int hd, int ctx_stride,
                                                            long layer_stride, long slot_stride, int src,
-                                                           int dst0, int n_pos) {
+                                                           int dst0, int p0, int n_pos) {
   const int lk = blockIdx.x;                 // layer * nkv + kv head
   const int layer = lk / nkv, kh = lk % nkv;
   const int dst = dst0 + blockIdx.y;
   const size_t kh_off = (size_t)kh * ctx_stride * hd;
-  // positions 0 .. n_pos-1 occupy the whole 16-position chunks that hold
-  // them: a contiguous prefix of each tiled plane
+  // positions p0 .. n_pos-1 (p0 a multiple of 16) occupy the whole
+  // 16-position chunks that hold them: a contiguous range of each tiled plane
+  const long e0 = (long)p0 * hd;
   const long n = (long)((n_pos + 15) >> 4) * 16 * hd;
   const T* ks = kc + layer * layer_stride + (size_t)src * slot_stride + kh_off;
   T* kd = kc + layer * layer_stride + (size_t)dst * slot_stride + kh_off;
-  for (long e = threadIdx.x; e < n; e += kNT) kd[e] = ks[e];
+  for (long e = e0 + threadIdx.x; e < n; e += kNT) kd[e] = ks[e];
   const T* vs = vc + layer * layer_stride + (size_t)src * slot_stride + kh_off;
   T* vd = vc + layer * layer_stride + (size_t)dst * slot_stride + kh_off;
-  for (long e = threadIdx.x; e < n; e += kNT) vd[e] = vs[e];
+  for (long e = e0 + threadIdx.x; e < n; e += kNT) vd[e] = vs[e];
 }
 
 __global__ void init_state_kernel(InitStateArgs a) {
@@ -573,15 +574,16 @@ hipError_t launch_sample_finish(const FinishArgs& a, hipStream_t st) {
 
 hipError_t launch_kv_replicate(int dt, void* kc, void* vc, int n_layers, long layer_stride,
                                long slot_stride, int nkv, int hd, int ctx_stride, int src,
-                               int dst0, int n_dst, int n_pos, hipStream_t st) {
-  if (n_dst <= 0 || n_pos <= 0) return hipSuccess;
+                               int dst0, int n_dst, int p0, int n_pos, hipStream_t st) {
+  if (n_dst <= 0 || n_pos <= p0) return hipSuccess;
+  if (p0 < 0 || p0 % 16 || n_pos > ctx_stride) return hipErrorInvalidValue;
   dim3 grid(n_layers * nkv, n_dst);
   if (dt == DT_BF16)
     hipLaunchKernelGGL((kv_replicate_kernel<bf16_t>), grid, dim3(kNT), 0, st, (bf16_t*)kc, (bf16_t*)vc,
-                       nkv, hd, ctx_stride, layer_stride, slot_stride, src, dst0, n_pos);
+                       nkv, hd, ctx_stride, layer_stride, slot_stride, src, dst0, p0, n_pos);
   else
     hipLaunchKernelGGL((kv_replicate_kernel<float>), grid, dim3(kNT), 0, st, (float*)kc, (float*)vc,
-                       nkv, hd, ctx_stride, layer_stride, slot_stride, src, dst0, n_pos);
+                       nkv, hd, ctx_stride, layer_stride, slot_stride, src, dst0, p0, n_pos);
   return hipGetLastError();
 }
 

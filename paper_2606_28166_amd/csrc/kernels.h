@@ -134,6 +134,17 @@ struct AttnArgs {
   // rows of one prompt, rows grp_row0[g] .. + grp_n[g] - 1 in increasing
   // position order; NULL: one workgroup per row
   const int32_t* grp_row0; const int32_t* grp_n; int n_groups;
+  // Decode rows whose prompt prefix is shared (part != NULL): row r attends
+  // positions [0, row_lo[r]) in slot pfx_slot[r] (pfx_pos[r] = row_lo[r] - 1)
+  // and [row_lo[r], row_pos[r]] in its own slot; row_lo is a multiple of 16
+  // (0: no shared prefix).  pfx_groups groups of at most pfx_rows (<= 16)
+  // consecutive rows with the same prefix (pfx_row0, pfx_n; a group with
+  // pfx_n = 0 is skipped) cover every row with row_lo > 0.  part: [R][nq][hd + 2]
+  // floats of prefix partials (the model's own: the passes of the two models
+  // may run at the same time).
+  const int32_t* row_lo; float* part;
+  const int32_t* pfx_row0; const int32_t* pfx_n; int pfx_groups; int pfx_rows;
+  const int32_t* pfx_slot; const int32_t* pfx_pos;
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
 
@@ -170,11 +181,11 @@ struct FinishArgs {
 };
 hipError_t launch_sample_finish(const FinishArgs& a, hipStream_t st);
 
-// Copy positions [0, n_pos) of slot src into slots dst0 .. dst0 + n_dst - 1
-// for every layer and kv head (K and transposed V).
+// Copy positions [p0, n_pos) of slot src into slots dst0 .. dst0 + n_dst - 1
+// for every layer and kv head (K and transposed V); p0 % 16 == 0.
 hipError_t launch_kv_replicate(int dt, void* kc, void* vc, int n_layers, long layer_stride,
                                long slot_stride, int nkv, int hd, int ctx_stride, int src,
-                               int dst0, int n_dst, int n_pos, hipStream_t st);
+                               int dst0, int n_dst, int p0, int n_pos, hipStream_t st);
 
 // Per-sequence state after prefill.
 struct InitStateArgs {
@@ -210,5 +221,7 @@ hipError_t launch_gather_i32(const int32_t* src, const int32_t* idx, int n, int3
 
 // true when the MFMA attention kernel covers this (dtype, head_dim, group size)
 bool attention_has_mfma(int dt, int hd, int gqa);
+// true when decode attention can read a shared prompt prefix once per row block
+bool attention_shares_prefix(int dt, int hd, int gqa);
 
 }  // namespace tandem

@@ -57,6 +57,7 @@ struct ModelPlan {            // byte offsets / sizes of one model's buffers
   size_t ws_floats;
   size_t kv_half;             // bytes of the K (= V) cache
   size_t off_h, off_xa, off_xf, off_q, off_ws, off_logits, off_rope;
+  size_t off_part;            // prefix partials of the decode attention [max_seqs][n_q][hd + 2]
   size_t off_packed, packed_bytes;   // MFMA-ordered copies of the projection and LM-head weights
 };
 
@@ -87,6 +88,7 @@ struct Plan {
   ModelPlan m[2];
   size_t kv_bytes;
   size_t off_state, off_seq_slot, off_rows, off_prompt, off_partials, off_count, off_act, off_drows;
+  size_t off_pfx;             // shared-prefix tables of the decode rows (5 x max_seqs int32)
   size_t scratch_bytes;
 };
 
@@ -114,6 +116,7 @@ struct Model {
   float* ws;
   float* logits;
   float2* rope;
+  float* part;
 };
 
 tandem_status fail(std::string* where, tandem_status s, const std::string& msg) {
@@ -204,6 +207,7 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
     m.off_ws = sc; sc = align_up(sc + m.ws_floats * 4, kAlign);
     m.off_logits = sc; sc = align_up(sc + (size_t)cap->max_seqs * c->vocab * 4, kAlign);
     m.off_rope = sc; sc = align_up(sc + (size_t)P.ctx_stride * (c->head_dim / 2) * 8, kAlign);
+    m.off_part = sc; sc = align_up(sc + (size_t)cap->max_seqs * c->n_q_heads * (c->head_dim + 2) * 4, kAlign);
     m.packed_bytes = 0;
     for (const auto& nk : packed_shapes(c))
       if (packs(c, nk.first, nk.second)) m.packed_bytes += align_up(packed_weight_bytes(nk.first, nk.second), kAlign);
@@ -219,6 +223,7 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
   P.off_count = sc; sc = align_up(sc + 4, kAlign);
   P.off_act = sc; sc = align_up(sc + S * 4, kAlign);
   P.off_drows = sc; sc = align_up(sc + 4 * S * 4, kAlign);
+  P.off_pfx = sc; sc = align_up(sc + 5 * S * 4, kAlign);
   P.scratch_bytes = sc;
   return P;
 }
@@ -259,6 +264,18 @@ struct tandem_handle {
   int32_t* act;
   int32_t *drow_tok, *drow_slot, *drow_pos, *drow_done;
   int R_launch = 0;
+  // Shared prompt prefix.  The G sequences of a prompt hold the same K/V at
+  // the prompt positions: decode attention reads positions [0, lo) (lo = the
+  // prompt length - 1 rounded down to 16) once per block of rows from the
+  // slot of the prompt's first sequence, and each row's own slot from lo on.
+  // The tables depend on the act order only (rebuilt at prefill and at each
+  // compaction): per row lo, prefix slot and lo - 1; then pfx_max groups of
+  // at most pfx_rows consecutive rows with the same prefix (unused: 0 rows).
+  bool share = false;
+  int32_t *row_lo, *pfx_slot, *pfx_pos, *pfx_row0, *pfx_n;
+  int pfx_max = 0, pfx_rows = 0, G = 1;
+  std::vector<int32_t> lo_of_prompt;                 // host, per prompt
+  std::vector<int32_t> h_pfx, h_act;                 // host staging (kept until the next rebuild)
   int steps_since_compact = 0;
   int32_t *p_end, *p_len;
   float* partials;
@@ -464,6 +481,7 @@ struct FwdRows {
   // attention's row blocks); NULL at decode
   const int32_t *grp_row0 = nullptr, *grp_n = nullptr;
   int n_groups = 0;
+  bool shared_prefix = false;   // decode rows reading the prompt prefix through the prefix tables
 };
 
 tandem_status forward_embed(tandem_handle* h, Model& m, const FwdRows& fr, hipStream_t st) {
@@ -508,6 +526,11 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   aa.dt = dt; aa.q = m.q; aa.R = R; aa.nq = nq; aa.nkv = nkv; aa.hd = hd; aa.cache = cg;
   aa.row_slot = fr.slot; aa.row_pos = fr.pos; aa.row_done = fr.done; aa.out = m.xa;
   aa.grp_row0 = fr.grp_row0; aa.grp_n = fr.grp_n; aa.n_groups = fr.n_groups;
+  if (fr.shared_prefix) {
+    aa.row_lo = h->row_lo; aa.part = m.part;
+    aa.pfx_row0 = h->pfx_row0; aa.pfx_n = h->pfx_n; aa.pfx_groups = h->pfx_max; aa.pfx_rows = h->pfx_rows;
+    aa.pfx_slot = h->pfx_slot; aa.pfx_pos = h->pfx_pos;
+  }
   if (att_wait) HIPCHK(hipStreamWaitEvent(st, att_wait, 0));
   TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
   if (att_done) HIPCHK(hipEventRecord(att_done, st));
@@ -598,7 +621,9 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
     ga.pending = h->pending; ga.seq_slot = h->seq_slot; ga.pos = h->pos; ga.done = h->done;
     ga.row_tok = h->drow_tok; ga.row_slot = h->drow_slot; ga.row_pos = h->drow_pos; ga.row_done = h->drow_done;
     TIMED(TANDEM_K_OTHER, launch_gather_rows(ga, st));
-    tandem_status s = forward_pair(h, FwdRows{R, h->drow_tok, h->drow_slot, h->drow_pos, h->drow_done}, true);
+    FwdRows fr{R, h->drow_tok, h->drow_slot, h->drow_pos, h->drow_done};
+    fr.shared_prefix = h->share;
+    tandem_status s = forward_pair(h, fr, true);
     if (s != TANDEM_OK) return s;
   }
   const int V = h->m[0].cfg.vocab;
@@ -629,6 +654,39 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
   return TANDEM_OK;
 }
 
+// Shared-prefix tables of decode rows 0 .. R-1 in the act order act_host
+// (see tandem_handle::share), copied to the device on the handle's stream.
+// Rows of one prompt are consecutive in any act order (sequence ids grow
+// within each part of the partition), so a group is a run of rows with the
+// same prompt and the same 16-block of sequence index within the prompt:
+// at most 16 rows, and at most two runs per (prompt, block).
+tandem_status upload_prefix_tables(tandem_handle* h, const int32_t* act_host, int R) {
+  const int S = h->cap.max_seqs, G = h->G;
+  std::vector<int32_t>& t = h->h_pfx;
+  t.assign(5 * (size_t)S, 0);
+  int32_t *lo = t.data(), *ps = lo + S, *pp = lo + 2 * S, *g0 = lo + 3 * S, *gn = lo + 4 * S;
+  int ng = 0;
+  for (int r = 0; r < R; ++r) {
+    const int s = act_host[r], j = s / G;
+    lo[r] = h->lo_of_prompt[j];
+    if (lo[r] == 0) continue;
+    ps[r] = j * G;                 // slot of the prompt's first sequence (slots follow sequence ids)
+    pp[r] = lo[r] - 1;
+    const bool cont = ng > 0 && g0[ng - 1] + gn[ng - 1] == r && act_host[r - 1] / G == j &&
+                      (act_host[r - 1] % G) / 16 == (s % G) / 16;
+    if (cont) {
+      ++gn[ng - 1];
+      continue;
+    }
+    if (ng == h->pfx_max) return fail(&h->err, TANDEM_E_STATE, "shared-prefix table overflow");
+    g0[ng] = r;
+    gn[ng] = 1;
+    ++ng;
+  }
+  HIPCHK(hipMemcpyAsync(h->row_lo, t.data(), t.size() * 4, hipMemcpyHostToDevice, h->stream));
+  return TANDEM_OK;
+}
+
 // With EOS on, sequences finish at different steps: every kCompactEvery steps
 // partition the batch (unfinished sequences first, stable) and shrink the
 // launched row count.  One host synchronisation per compaction.
@@ -645,6 +703,11 @@ tandem_status maybe_compact(tandem_handle* h) {
   if (R < h->R_launch) {
     h->R_launch = R;
     drop_graphs(h);                   // captured for the old row count
+  }
+  if (h->share) {                     // the act order changed: new prefix tables (same launch bounds)
+    h->h_act.resize((size_t)h->n_seq);
+    HIPCHK(hipMemcpy(h->h_act.data(), h->act, (size_t)h->n_seq * 4, hipMemcpyDeviceToHost));
+    CALL(upload_prefix_tables(h, h->h_act.data(), h->R_launch));
   }
   return TANDEM_OK;
 }
@@ -837,6 +900,7 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     m.ws = (float*)(sc + m.p.off_ws);
     m.logits = (float*)(sc + m.p.off_logits);
     m.rope = (float2*)(sc + m.p.off_rope);
+    m.part = (float*)(sc + m.p.off_part);
     m.p_lm = nullptr;
   }
   const size_t S = (size_t)cap->max_seqs;
@@ -855,6 +919,8 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   h->act = (int32_t*)(sc + P.off_act);
   int32_t* drows = (int32_t*)(sc + P.off_drows);
   h->drow_tok = drows; h->drow_slot = drows + S; h->drow_pos = drows + 2 * S; h->drow_done = drows + 3 * S;
+  int32_t* pfx = (int32_t*)(sc + P.off_pfx);
+  h->row_lo = pfx; h->pfx_slot = pfx + S; h->pfx_pos = pfx + 2 * S; h->pfx_row0 = pfx + 3 * S; h->pfx_n = pfx + 4 * S;
   h->h_count = nullptr;
 
   // --- HIP work from here on
@@ -988,6 +1054,23 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
   HIPCHK(hipMemcpyAsync(h->p_end, h->hbuf.data(), (size_t)n_prompts * 4, hipMemcpyHostToDevice, st));
   HIPCHK(hipMemcpyAsync(h->p_len, h->hbuf.data() + n_prompts, (size_t)n_prompts * 4, hipMemcpyHostToDevice, st));
   HIPCHK(hipStreamSynchronize(st));
+  // the G sequences of a prompt share its prefix in decode attention when
+  // both models' attention kernels can (otherwise every slot gets a copy)
+  {
+    bool share = G > 1;
+    for (int i = 0; i < 2; ++i) {
+      const tandem_model_cfg& c = h->m[i].cfg;
+      share = share && attention_shares_prefix(c.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32, c.head_dim,
+                                               c.n_q_heads / c.n_kv_heads);
+    }
+    h->share = share;
+    h->G = G;
+    h->lo_of_prompt.assign((size_t)n_prompts, 0);
+    if (share)
+      for (int j = 0; j < n_prompts; ++j) h->lo_of_prompt[j] = (prompt_offsets[j + 1] - prompt_offsets[j] - 1) / 16 * 16;
+    h->pfx_rows = std::min(G, 16);
+    h->pfx_max = (int)std::min<long>((long)2 * n_prompts * ((G + 15) / 16), h->cap.max_seqs);
+  }
   // chunks of whole prompts whose (P - 1) rows fit max_prefill_tokens
   int j0 = 0;
   std::vector<int32_t> rows;
@@ -1034,7 +1117,8 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
           Model& m = h->m[i];
           TIMED(TANDEM_K_OTHER, launch_kv_replicate(m.cfg.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32, m.kc, m.vc,
                                      m.cfg.n_layers, m.layer_stride, m.slot_stride, m.cfg.n_kv_heads,
-                                     m.cfg.head_dim, h->plan.ctx_stride, j * G, j * G + 1, G - 1, P - 1, st));
+                                     m.cfg.head_dim, h->plan.ctx_stride, j * G, j * G + 1, G - 1,
+                                     h->lo_of_prompt[j], P - 1, st));
         }
       }
       HIPCHK(hipStreamSynchronize(st));   // the host row arrays are reused by the next chunk
@@ -1050,6 +1134,11 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
   HIPCHK(hipMemcpyAsync(h->act, h->seq_slot, (size_t)n_seq * 4, hipMemcpyDeviceToDevice, st));   // identity
   h->n_seq = n_seq;
   h->R_launch = n_seq;
+  if (h->share) {
+    h->h_act.resize((size_t)n_seq);
+    for (int s = 0; s < n_seq; ++s) h->h_act[s] = s;
+    CALL(upload_prefix_tables(h, h->h_act.data(), n_seq));
+  }
   h->steps_since_compact = 0;
   h->prefilled = true;
   return TANDEM_OK;

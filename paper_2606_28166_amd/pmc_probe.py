@@ -2,20 +2,24 @@
 
 Run mode (the program rocprofv3 profiles): a plain device copy of known size
 (the calibration: what FETCH_SIZE / WRITE_SIZE report for exactly N bytes
-read and N bytes written), then a short tandem rollout of the Qwen-shaped
-models (128 rows, prompts of PROMPT_LEN tokens so the contexts sit in the
-middle of the benchmark's rollout) with eagerly launched decode steps (one
-dispatch per kernel):
+read and N bytes written), then the benchmark's Qwen-shaped rollout (16
+prompts of 256 tokens x G = 8 rows): WARM decode steps replayed from the
+step graph, so that the contexts reach the middle of the benchmark's
+2048-token rollout, then STEPS decode steps launched eagerly (one dispatch
+per kernel).  Counters are collected for the attention kernels and the copy
+only:
 
-    cd /tmp && rocprofv3 --pmc FETCH_SIZE -d <dir> -o fetch --output-format csv -- \\
-        python3 <repo>/paper_2606_28166_amd/pmc_probe.py
-    cd /tmp && rocprofv3 --pmc WRITE_SIZE -d <dir> -o write --output-format csv -- \\
-        python3 <repo>/paper_2606_28166_amd/pmc_probe.py
+    cd /tmp && rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'attn_mfma|copy' -d <dir> -o fetch \\
+        --output-format csv -- python3 <repo>/paper_2606_28166_amd/pmc_probe.py
+    cd /tmp && rocprofv3 --pmc WRITE_SIZE --kernel-include-regex 'attn_mfma|copy' -d <dir> -o write \\
+        --output-format csv -- python3 <repo>/paper_2606_28166_amd/pmc_probe.py
 
-Analysis mode: per attention dispatch, counter KiB x (copy bytes / copy
-counter KiB) against the algorithmic K/V bytes of that dispatch; prints a
-JSON summary (the ratio traffic / algorithmic bytes is what the benchmark
-applies to its own launches):
+Analysis mode: the counters of the last STEPS steps' attention dispatches
+(both models; the shared-prefix pass and the per-row pass of every call) x
+(copy bytes / copy counter KiB) against the algorithmic K/V bytes of those
+steps (a shared prompt prefix once per group); prints a JSON summary (the
+ratio traffic / algorithmic bytes is what the benchmark applies to its own
+attention calls):
 
     python3 paper_2606_28166_amd/pmc_probe.py --analyze <fetch csv> <write csv>
 """
@@ -33,8 +37,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 COPY_BYTES = 1 << 30
+WARM = 1000              # graph-replayed steps first: contexts ~1255 .. 1279 in the measured steps
 STEPS = 24
-PROMPT_LEN = 1280        # contexts 1279 .. 1302: the middle of the 2048-token rollout from 256-token prompts
 ATTN_SRC = os.path.join(ROOT, "paper_2606_28166_amd", "csrc", "k_attn.hip")
 
 
@@ -57,13 +61,17 @@ def run() -> None:
     del x, y
 
     wl = W.workload("qwen")
-    wl.sample.max_new = STEPS
-    wl.prompt_len = PROMPT_LEN
+    wl.sample.max_new = WARM + STEPS
     ws, wj, prompts, bnd = W.make_all(wl)
     eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed,
-                       max_seqs=wl.n_seqs, max_ctx=max(len(p) for p in prompts) - 1 + STEPS,
+                       max_seqs=wl.n_seqs, max_ctx=max(len(p) for p in prompts) - 1 + WARM + STEPS,
                        max_prefill_tokens=4096, boundary_words=W.boundary_bits(bnd))
     eng.prefill(prompts, wl.group)
+    for t in range(WARM):
+        eng.step()
+        if (t + 1) % 250 == 0:
+            torch.cuda.synchronize()
+            print(f"pmc_probe: {t + 1} graph steps", flush=True)
     eng.timing(L.TIMING_EAGER)                   # one dispatch per kernel (no graph replay)
     for _ in range(STEPS):
         eng.step()
@@ -83,41 +91,39 @@ def _rows(path):
 def analyze(fetch_csv: str, write_csv: str) -> dict:
     import workloads as W
     wl = W.workload("qwen")
-    wl.prompt_len = PROMPT_LEN
-    res = {"kernel_source_sha256_16": kernel_digest(), "copy_bytes": COPY_BYTES, "prompt_len": PROMPT_LEN,
-           "decode_steps": STEPS}
+    P = wl.prompt_len
+    lo = (P - 1) // 16 * 16                      # the shared prefix (G > 1, bf16, head_dim 128)
+    res = {"kernel_source_sha256_16": kernel_digest(), "copy_bytes": COPY_BYTES, "prompt_len": P,
+           "shared_prefix": lo, "decode_steps": [WARM + 1, WARM + STEPS]}
     for name, path in (("fetch", fetch_csv), ("write", write_csv)):
         rows = _rows(path)
         copies = [v for _, k, v in rows if "copy" in k.lower() or "elementwise" in k.lower()]
         if not copies:
             raise SystemExit(f"no copy kernel in {path}")
         cal = max(copies)                        # KiB the counter reports for COPY_BYTES
-        # the decode launches are the last STEPS * (both models' layers)
-        # attention dispatches (the prefill's come first)
-        n_dec = STEPS * (wl.senior.n_layers + wl.junior.n_layers)
+        # the measured launches are the last STEPS * (both models' layers) x
+        # (prefix pass + per-row pass) attention dispatches
+        n_dec = STEPS * 2 * (wl.senior.n_layers + wl.junior.n_layers)
         att = [(k, v) for _, k, v in rows if "attn_mfma_kernel" in k][-n_dec:]
         res[name] = {"copy_counter_kib": cal, "scale_bytes_per_kib": COPY_BYTES / cal,
                      "attention_dispatches": len(att)}
         res[name]["attention_counter_kib"] = [v for _, v in att]
-    # decode attention dispatches in launch order: per step, the junior's 28
-    # layers and the senior's 36 (two streams); K/V bytes per dispatch depend
-    # only on the model and the step's context
-    kv = {"senior": 2 * wl.senior.n_kv_heads * wl.senior.head_dim * 2,
-          "junior": 2 * wl.junior.n_kv_heads * wl.junior.head_dim * 2}   # bytes per position per layer
-    rows_per = wl.n_seqs
-    P = wl.prompt_len
-    att_alg = []
-    for t in range(1, STEPS + 1):
+    # algorithmic K/V bytes of those steps: per layer of a model, the shared
+    # prefix once per prompt and each row's positions lo .. its context end
+    kv = (2 * wl.senior.n_kv_heads * wl.senior.head_dim * 2 * wl.senior.n_layers
+          + 2 * wl.junior.n_kv_heads * wl.junior.head_dim * 2 * wl.junior.n_layers)   # bytes per position
+    alg = 0
+    for t in range(WARM + 1, WARM + STEPS + 1):
         ctx = P - 1 + t                           # the step's context, new position included
-        att_alg += [rows_per * ctx * kv["junior"]] * wl.junior.n_layers
-        att_alg += [rows_per * ctx * kv["senior"]] * wl.senior.n_layers
+        alg += kv * (wl.n_prompts * lo + wl.n_seqs * (ctx - lo))
     fet = [v * res["fetch"]["scale_bytes_per_kib"] for v in res["fetch"]["attention_counter_kib"]]
     wri = [v * res["write"]["scale_bytes_per_kib"] for v in res["write"]["attention_counter_kib"]]
-    n = min(len(fet), len(att_alg))
-    res["dispatches_compared"] = n
-    res["algorithmic_bytes"] = sum(att_alg[:n])
-    res["fetch_bytes"] = sum(fet[:n])
-    res["write_bytes"] = sum(wri[:n])
+    if len(fet) != n_dec or len(wri) != n_dec:
+        raise SystemExit(f"expected {n_dec} attention dispatches, found {len(fet)} / {len(wri)}")
+    res["dispatches_compared"] = n_dec
+    res["algorithmic_bytes"] = alg
+    res["fetch_bytes"] = sum(fet)
+    res["write_bytes"] = sum(wri)
     res["traffic_over_algorithmic"] = (res["fetch_bytes"] + res["write_bytes"]) / res["algorithmic_bytes"]
     for k in ("fetch", "write"):
         del res[k]["attention_counter_kib"]

@@ -55,6 +55,25 @@ def test_qwen_shapes_bf16_qk_norm():
     P.check(p, P.TOL_BF16)
 
 
+def test_shared_prompt_prefix_edges():
+    """The G sequences of a prompt read its K/V prefix (prompt length - 1,
+    rounded down to 16) once per block of rows: prompt lengths on both sides
+    of every 16-position boundary (no shared prefix at all below 17 tokens,
+    a one-position suffix at the first step for 17, 33, 49), G = 3 rows per
+    prompt (row blocks split inside a group), contexts crossing several chunk
+    boundaries during the rollout."""
+    P.log("case shared prompt prefix: small shapes 2+1 layers, prompt lengths 1..65 around multiples of 16, G=3")
+    wl = _small_reduced()
+    lengths = [1, 2, 16, 17, 18, 32, 33, 48, 49, 65]
+    wl.n_prompts, wl.group, wl.prompt_len, wl.prompt_len_min = len(lengths), 3, max(lengths), None
+    wl.sample.max_new = 40
+    ws, wj, _, bnd = W.make_all(wl)
+    rng = np.random.default_rng(77)
+    prompts = [rng.integers(0, wl.senior.vocab, size=n).astype(np.int32) for n in lengths]
+    p = P.run(wl, logits_at=(1, 17, 40), weights=(ws, wj, prompts, bnd))
+    P.check(p, P.TOL_BF16)
+
+
 def test_paper_schedule_redraw_word_boundaries_and_cap():
     P.log("case paper schedule: REDRAW p=0.5, K=3, drawn first owner, 35% boundary bitmap, T=0.6")
     wl = _tiny("bf16")
