@@ -9,15 +9,14 @@ prefill of both models on every prompt, then max_new tandem decode steps
 Prints ONE JSON line:
   value            co-generated tokens / s over the whole job (prefill + decode)
   roofline         decode attention (the dominant kernel): algorithmic K/V
-                   bytes per attention call / its average time, from HIP event
-                   pairs around every call (on the stream it runs on) in an
+                   bytes per launch / its average launch time, from HIP event
+                   pairs around every launch (on the stream it runs on) in an
                    extra rollout whose two forwards run one after the other, so
-                   each call has the GPU to itself; the per-class breakdown
-                   comes from the same rollout.  A call is one launch, or two
-                   when the G sequences of a prompt share its K/V prefix (a
-                   pass over the prefix for blocks of rows, then the per-row
-                   pass); the algorithmic bytes then count the prefix once per
-                   group
+                   each launch has the GPU to itself; the per-class breakdown
+                   comes from the same rollout.  When the G sequences of a
+                   prompt share its K/V prefix, a launch reads the prefix once
+                   per block of rows and the algorithmic bytes count it once
+                   per group
   roofline_concurrent the same in the two-stream schedule of the timed region
                    (the junior's forward overlapping the senior's)
   (the timed region replays the captured step graph; graph-captured event
@@ -273,7 +272,7 @@ def main():
         nbytes = attention_bytes(wl, plens, L, lengths)
         gbs = nbytes / (ms / 1e3) / 1e9
         per = nbytes / max(nl, 1)
-        return {"bound": "hbm", "kernel": "decode attention (both models; per call a shared-prefix pass and a per-row pass)" if shares_prefix(wl) else "decode attention (both models)", "achieved": round(gbs, 1),
+        return {"bound": "hbm", "kernel": "decode attention (both models; shared prompt prefix)" if shares_prefix(wl) else "decode attention (both models)", "achieved": round(gbs, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                 "traffic": None if traffic_ratio is None else int(per * traffic_ratio),
                 "launches": nl, "avg_launch_us": round(ms * 1e3 / max(nl, 1), 2),
@@ -284,12 +283,12 @@ def main():
         _, d_ser, tr = rollout_once(0b1111 | LIB.TIMING_SERIAL)
         breakdown = {k: {"ms": round(v[0], 3), "launches": v[1]} for k, v in tr.items()}
         roof = roofline_of(tr["attention"], "one rollout's decode steps, the two forwards serialized and launched "
-                                            "from the host, a HIP event pair around every attention call")
+                                            "from the host, a HIP event pair around every attention launch")
         log(f"[bench] serialized rollout: decode {d_ser:.1f} ms, attention {tr['attention'][0]:.1f} ms / "
             f"{tr['attention'][1]} launches -> {roof['achieved']:.0f} GB/s")
         _, d_con, tr = rollout_once(1 << LIB.K_ATTENTION)
         roof_conc = roofline_of(tr["attention"], "one rollout's decode steps in the two-stream schedule, launched "
-                                                 "from the host, a HIP event pair around every attention call")
+                                                 "from the host, a HIP event pair around every attention launch")
         log(f"[bench] concurrent instrumented rollout: decode {d_con:.1f} ms, attention -> {roof_conc['achieved']:.0f} GB/s")
 
     cpu = None

@@ -159,74 +159,35 @@ __device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, con
   }
 }
 
-// Workgroup (kv head, block of query rows).  Decode (ROWS = 1): one row per
-// workgroup, query columns = the GQA heads of the group.  Prompt rows (ROWS =
-// 16 / GQA): ROWS consecutive rows of one prompt share the workgroup, query
-// column c = (row c / GQA, head c % GQA), each with its own causal limit; the
-// workgroup streams the positions its last row attends, so a prompt's K/V is
-// read once per ROWS rows rather than once per row.  Row groups of at most 16
-// rows are split over sub_per_grp workgroups of ROWS rows.
-//
-// Shared prompt prefix (decode rows of one prompt's G sequences): the
-// softmax over positions [0, n) splits exactly into two partial softmaxes
-// over [0, lo) and [lo, n), each carried as (running max M, sum of
-// exponentials, unnormalised weighted sum of V), merged by rescaling both to
-// the larger max:
-//   * PREFIX (ROWS > 1, the prefix pass): every column attends positions
-//     [0, row_pos + 1) of the group's source slot and the workgroup writes its
-//     column's partial (HD weighted sums, then M and the sum) to
-//     part[row][head][HD + 2] instead of an output row;
-//   * ROWS = 1 with row_lo != NULL (the suffix pass): the row attends positions
-//     [row_lo[r], pos] of its own slot (row_lo a multiple of 16) and, when
-//     row_lo[r] > 0, merges the prefix partial of its row before normalising.
-template <int HD, int GQA, int ROWS, bool PREFIX = false>
-__global__ __launch_bounds__(256) void attn_mfma_kernel(
-    const float* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    int ctx_stride, long slot_stride, const int32_t* __restrict__ row_slot,
-    const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
-    const int32_t* __restrict__ grp_row0, const int32_t* __restrict__ grp_n, int sub_per_grp,
-    const int32_t* __restrict__ row_lo, float* __restrict__ part, bf16_t* __restrict__ out, int nq) {
+// One workgroup's attention: query columns c = (row r0 + c / GQA, head
+// kh GQA + c % GQA) for c < NCOL (rows >= r0 + nr are unused columns) over
+// positions [16 c0, ctx_max) of one slot's tiled K/V plane of kv head kh;
+// column c attends the positions below its own limit (row_pos[row] + 1 when
+// row_pos_col is given, else ctx_max).  The four waves take interleaved
+// 16-position chunks with their own online softmax and leave their states
+// in LDS: sm_m[w][c] (running max, log2 units), sm_l[w][c] (sum of
+// exponentials), sm_o[(w NCOL + c) HD + d] (unnormalised weighted sums).
+// GUARD: some column may see a chunk with no position it attends.
+template <int HD, int GQA, int NCOL, bool GUARD>
+__device__ __forceinline__ void attend_block(const float* __restrict__ q, const bf16_t* __restrict__ kc,
+                                             const bf16_t* __restrict__ vc, int ctx_stride, long slot_stride,
+                                             int slot, int kh, int r0, int nr, int c0, int ctx_max,
+                                             const int32_t* __restrict__ row_pos_col, int nq, float (*sm_m)[16],
+                                             float (*sm_l)[16], float* sm_o) {
   constexpr int DC = HD / 32;     // k-steps of the S product
   constexpr int DB = HD / 16;     // 16-dim blocks of the O product
-  constexpr int NCOL = GQA * ROWS;
   static_assert(NCOL <= 16, "16 query columns per workgroup");
-  static_assert(!PREFIX || ROWS > 1, "the prefix pass serves several rows");
-  __shared__ float sm_m[4][16];
-  __shared__ float sm_l[4][16];
-  __shared__ float sm_o[4][NCOL][HD];
-
-  const int kh = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
-  // rows r0 .. r0 + nr - 1 (groups of at most 16 rows of one prompt, split in
-  // sub_per_grp blocks of ROWS)
-  int r0 = blockIdx.y, nr = 1;
-  if (ROWS > 1) {
-    const int grp = blockIdx.y / sub_per_grp, sub = blockIdx.y % sub_per_grp;
-    r0 = grp_row0[grp] + sub * ROWS;
-    nr = min(ROWS, grp_n[grp] - sub * ROWS);
-    if (nr <= 0) return;
-  }
-  const int col0 = kh * GQA * HD;
-  if (ROWS == 1 && row_done && row_done[r0]) {
-    bf16_t* orow = out + (size_t)r0 * 2 * nq * HD;     // split-format activation row
-    for (int e = tid; e < GQA * HD; e += 256) split_store(orow, col0 + e, 0.f);
-    return;
-  }
-  const int slot = row_slot[r0];
-  const int ctx_max = row_pos[r0 + nr - 1] + 1;       // positions streamed from the cache
   const int ri = c16 / GQA, hq = c16 % GQA;           // this lane's query column
   const bool valid = c16 < NCOL && ri < nr;
   const int rr = r0 + (valid ? ri : 0);
-  const int ctx = valid ? row_pos[rr] + 1 : ctx_max;  // positions the column attends
+  const int ctx = (valid && row_pos_col) ? row_pos_col[rr] + 1 : ctx_max;   // positions the column attends
   const size_t plane = (size_t)slot * slot_stride + (size_t)kh * ctx_stride * HD;
   const __amdgpu_buffer_rsrc_t kr = buf_rsrc(kc + plane, (uint32_t)ctx_stride * HD * 2);
   const __amdgpu_buffer_rsrc_t vr = buf_rsrc(vc + plane, (uint32_t)ctx_stride * HD * 2);
   const float scale = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
 
-  // positions before lo belong to the shared prefix (suffix pass only)
-  const int lo = (ROWS == 1 && row_lo) ? row_lo[r0] : 0;
-  const int c0 = lo >> 4;
   // Wave w owns chunks c0 + w, c0 + w + 4, ... of the stream; its first
   // chunk is requested before the query is read.
   const int nchunk = ((ctx_max + 15) >> 4) - c0;
@@ -265,11 +226,11 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   for (int i = 0; i < nmine; i += 2) {
     if (i + 1 < nmine) load_chunk<HD>(cb, kr, vr, chunk_at(i + 1), lane);
     pin_chunk<HD>(ca);
-    attend_chunk<HD, (ROWS > 1)>(st, ca, qh, ql, 16 * chunk_at(i), ctx, ctx_max, scale, g);
+    attend_chunk<HD, GUARD>(st, ca, qh, ql, 16 * chunk_at(i), ctx, ctx_max, scale, g);
     if (i + 2 < nmine) load_chunk<HD>(ca, kr, vr, chunk_at(i + 2), lane);
     if (i + 1 < nmine) {
       pin_chunk<HD>(cb);
-      attend_chunk<HD, (ROWS > 1)>(st, cb, qh, ql, 16 * chunk_at(i + 1), ctx, ctx_max, scale, g);
+      attend_chunk<HD, GUARD>(st, cb, qh, ql, 16 * chunk_at(i + 1), ctx, ctx_max, scale, g);
     }
   }
 
@@ -285,45 +246,224 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int h = 4 * g + i;
-      if (h < NCOL) sm_o[wave][h][db * 16 + c16] = st.o[db][i];
+      if (h < NCOL) sm_o[(wave * NCOL + h) * HD + db * 16 + c16] = st.o[db][i];
     }
   __syncthreads();
-  const bool merge = ROWS == 1 && lo > 0;
-  for (int e = tid; e < NCOL * HD; e += 256) {
-    const int h = e / HD, d = e % HD;
-    if (h / GQA >= nr) continue;
-    float M = sm_m[0][h];
+}
+
+// Column c, dim d of the four waves' states: the running max M over the
+// waves, and the weighted sum and exponential sum rescaled to it (M = -inf
+// and zero sums when no wave saw a position).
+template <int HD, int NCOL>
+__device__ __forceinline__ void waves_merged(const float (*sm_m)[16], const float (*sm_l)[16], const float* sm_o,
+                                             int c, int d, float& M, float& num, float& den) {
+  M = sm_m[0][c];
 #pragma unroll
-    for (int w = 1; w < 4; ++w) M = fmaxf(M, sm_m[w][h]);
-    float* pp = (PREFIX || merge) ? part + ((size_t)(r0 + h / GQA) * nq + kh * GQA + h % GQA) * (HD + 2) : nullptr;
-    float pm = -INFINITY;
-    if (merge) {
-      pm = pp[HD];
-      M = fmaxf(M, pm);
-    }
-    float num = 0.f, den = 0.f;
+  for (int w = 1; w < 4; ++w) M = fmaxf(M, sm_m[w][c]);
+  num = 0.f;
+  den = 0.f;
+  if (M == -INFINITY) return;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float f = exp2f(sm_m[w][h] - M);
-      num += sm_o[w][h][d] * f;
-      den += sm_l[w][h] * f;
-    }
-    if (PREFIX) {                      // the partial, relative to M
-      pp[d] = num;
-      if (d == 0) {
-        pp[HD] = M;
-        pp[HD + 1] = den;
-      }
-      continue;
-    }
-    if (merge) {
-      const float f = exp2f(pm - M);
-      num += pp[d] * f;
-      den += pp[HD + 1] * f;
-    }
-    bf16_t* orow = out + (size_t)(r0 + h / GQA) * 2 * nq * HD;
-    split_store(orow, col0 + (h % GQA) * HD + d, num / den);
+  for (int w = 0; w < 4; ++w) {
+    const float f = exp2f(sm_m[w][c] - M);
+    num += sm_o[(w * NCOL + c) * HD + d] * f;
+    den += sm_l[w][c] * f;
   }
+}
+
+// Workgroup (kv head, block of query rows).  Decode (ROWS = 1): one row per
+// workgroup, query columns = the GQA heads of the group.  Prompt rows (ROWS =
+// 16 / GQA): ROWS consecutive rows of one prompt share the workgroup, each
+// column with its own causal limit; the workgroup streams the positions its
+// last row attends, so a prompt's K/V is read once per ROWS rows rather than
+// once per row.  Row groups of at most 16 rows are split over sub_per_grp
+// workgroups of ROWS rows.
+template <int HD, int GQA, int ROWS>
+__global__ __launch_bounds__(256) void attn_mfma_kernel(
+    const float* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
+    int ctx_stride, long slot_stride, const int32_t* __restrict__ row_slot,
+    const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
+    const int32_t* __restrict__ grp_row0, const int32_t* __restrict__ grp_n, int sub_per_grp,
+    bf16_t* __restrict__ out, int nq) {
+  constexpr int NCOL = GQA * ROWS;
+  __shared__ float sm_m[4][16];
+  __shared__ float sm_l[4][16];
+  __shared__ float sm_o[4 * NCOL * HD];
+
+  const int kh = blockIdx.x, tid = threadIdx.x;
+  int r0 = blockIdx.y, nr = 1;
+  if (ROWS > 1) {
+    const int grp = blockIdx.y / sub_per_grp, sub = blockIdx.y % sub_per_grp;
+    r0 = grp_row0[grp] + sub * ROWS;
+    nr = min(ROWS, grp_n[grp] - sub * ROWS);
+    if (nr <= 0) return;
+  }
+  const int col0 = kh * GQA * HD;
+  if (ROWS == 1 && row_done && row_done[r0]) {
+    bf16_t* orow = out + (size_t)r0 * 2 * nq * HD;     // split-format activation row
+    for (int e = tid; e < GQA * HD; e += 256) split_store(orow, col0 + e, 0.f);
+    return;
+  }
+  attend_block<HD, GQA, NCOL, (ROWS > 1)>(q, kc, vc, ctx_stride, slot_stride, row_slot[r0], kh, r0, nr, 0,
+                                          row_pos[r0 + nr - 1] + 1, ROWS > 1 ? row_pos : nullptr, nq, sm_m, sm_l,
+                                          sm_o);
+  for (int e = tid; e < NCOL * HD; e += 256) {
+    const int c = e / HD, d = e % HD;
+    if (c / GQA >= nr) continue;
+    float M, num, den;
+    waves_merged<HD, NCOL>(sm_m, sm_l, sm_o, c, d, M, num, den);
+    bf16_t* orow = out + (size_t)(r0 + c / GQA) * 2 * nq * HD;
+    split_store(orow, col0 + (c % GQA) * HD + d, num / den);
+  }
+}
+
+// Device-coherent (agent scope) accesses of the partial-softmax exchange:
+// they bypass the per-XCD L2 caches, so a partial written by a workgroup on
+// one XCD is what a workgroup on another reads once the counter says so.
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Both partial softmaxes of a column merged (prefix first, then the row's
+// own part: the same arithmetic whichever workgroup does it).
+__device__ __forceinline__ float merge_partials(float mp, float lp, float np, float ms, float ls, float ns) {
+  const float M = fmaxf(mp, ms);
+  const float fp = exp2f(mp - M), fs = exp2f(ms - M);
+  return (np * fp + ns * fs) / (lp * fp + ls * fs);
+}
+
+// Decode rows whose prompt prefix is shared by the G sequences of the prompt.
+// The softmax over positions [0, n) splits exactly into partial softmaxes over
+// [0, lo) and [lo, n), each carried as (running max M, sum of exponentials,
+// unnormalised weighted sum of V) and merged by rescaling both to the larger
+// max.  One launch holds two kinds of workgroups:
+//   * y < n_pfx (prefix): rows r0 .. r0 + nr - 1 of a prefix group (16 / GQA
+//     rows, query column c = (row c / GQA, head c % GQA)) over positions
+//     [0, lo) of the group's source slot, read once for all of them;
+//   * y = n_pfx + r (row r): positions [lo, pos] of the row's own slot
+//     (lo = row_lo[r], a multiple of 16; 0: no shared prefix, the row's
+//     output directly).
+// The first of the two to finish writes its partial ([row][head][HD + 2]:
+// the weighted sums, M, the sum; part_p and part_s), waits for the stores
+// to complete, and counts itself on the (row, kv head) counter; the second
+// merges both partials into the output row and clears the counter for the
+// next launch.  No workgroup waits for another.  Done rows take no part
+// (zero output).
+template <int HD, int GQA>
+__global__ __launch_bounds__(256) void attn_shared_kernel(
+    const float* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
+    int ctx_stride, long slot_stride, const int32_t* __restrict__ row_slot,
+    const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
+    const int32_t* __restrict__ row_lo, const int32_t* __restrict__ pfx_row0, const int32_t* __restrict__ pfx_n,
+    const int32_t* __restrict__ pfx_slot, int n_pfx, int sub_per_grp, float* __restrict__ part_p,
+    float* __restrict__ part_s, int32_t* __restrict__ cnt, bf16_t* __restrict__ out, int nq, int nkv) {
+  constexpr int RP = 16 / GQA;                     // rows of a prefix workgroup
+  constexpr int W = HD + 2;                        // floats of one column's partial
+  static_assert(RP > 1, "the prefix pass serves several rows");
+  __shared__ float sm_m[4][16];
+  __shared__ float sm_l[4][16];
+  __shared__ float sm_o[4 * 16 * HD];
+  __shared__ int sm_last[RP];
+
+  const int kh = blockIdx.x, tid = threadIdx.x;
+  const int col0 = kh * GQA * HD;
+  if ((int)blockIdx.y < n_pfx) {
+    const int grp = blockIdx.y / sub_per_grp, sub = blockIdx.y % sub_per_grp;
+    const int r0 = pfx_row0[grp] + sub * RP;
+    const int nr = min(RP, pfx_n[grp] - sub * RP);
+    if (nr <= 0) return;
+    constexpr int NCOL = GQA * RP;
+    attend_block<HD, GQA, NCOL, false>(q, kc, vc, ctx_stride, slot_stride, pfx_slot[r0], kh, r0, nr, 0,
+                                       row_lo[r0], nullptr, nq, sm_m, sm_l, sm_o);
+    for (int e = tid; e < NCOL * HD; e += 256) {
+      const int c = e / HD, d = e % HD;
+      if (c / GQA >= nr) continue;
+      float M, num, den;
+      waves_merged<HD, NCOL>(sm_m, sm_l, sm_o, c, d, M, num, den);
+      float* pp = part_p + ((size_t)(r0 + c / GQA) * nq + kh * GQA + c % GQA) * W;
+      st_dev(pp + d, num);
+      if (d == 0) {
+        st_dev(pp + HD, M);
+        st_dev(pp + HD + 1, den);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);                 // the partial is stored before it is counted
+    __syncthreads();
+    if (tid < nr) {
+      const int r = r0 + tid;
+      sm_last[tid] = row_done[r] ? 0 : __hip_atomic_fetch_add(cnt + (size_t)r * nkv + kh, 1, __ATOMIC_RELAXED,
+                                                              __HIP_MEMORY_SCOPE_AGENT) == 1;
+    }
+    __syncthreads();
+    for (int e = tid; e < NCOL * HD; e += 256) {
+      const int c = e / HD, d = e % HD;
+      if (c / GQA >= nr || !sm_last[c / GQA]) continue;
+      float M, num, den;
+      waves_merged<HD, NCOL>(sm_m, sm_l, sm_o, c, d, M, num, den);
+      const int r = r0 + c / GQA;
+      const float* ps = part_s + ((size_t)r * nq + kh * GQA + c % GQA) * W;
+      bf16_t* orow = out + (size_t)r * 2 * nq * HD;
+      split_store(orow, col0 + (c % GQA) * HD + d, merge_partials(M, den, num, ld_dev(ps + HD), ld_dev(ps + HD + 1),
+                                                                  ld_dev(ps + d)));
+    }
+    if (tid < nr && sm_last[tid])
+      __hip_atomic_store(cnt + (size_t)(r0 + tid) * nkv + kh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+
+  const int r = blockIdx.y - n_pfx;
+  bf16_t* orow = out + (size_t)r * 2 * nq * HD;    // split-format activation row
+  if (row_done[r]) {
+    for (int e = tid; e < GQA * HD; e += 256) split_store(orow, col0 + e, 0.f);
+    return;
+  }
+  const int lo = row_lo[r];
+  attend_block<HD, GQA, GQA, false>(q, kc, vc, ctx_stride, slot_stride, row_slot[r], kh, r, 1, lo >> 4,
+                                    row_pos[r] + 1, nullptr, nq, sm_m, sm_l, sm_o);
+  if (lo == 0) {
+    for (int e = tid; e < GQA * HD; e += 256) {
+      float M, num, den;
+      waves_merged<HD, GQA>(sm_m, sm_l, sm_o, e / HD, e % HD, M, num, den);
+      split_store(orow, col0 + e, num / den);
+    }
+    return;
+  }
+  // The prefix workgroups come first in the grid and are short: usually the
+  // prefix partial is there by now (counter 1) and the row merges at once.
+  // Otherwise it publishes its own partial and counts itself; the prefix
+  // workgroup merges if it comes second.
+  int32_t* const cp = cnt + (size_t)r * nkv + kh;
+  if (tid == 0) sm_last[0] = __hip_atomic_load(cp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (!sm_last[0]) {                               // (uniform: every thread read the same flag)
+    for (int e = tid; e < GQA * HD; e += 256) {
+      const int c = e / HD, d = e % HD;
+      float M, num, den;
+      waves_merged<HD, GQA>(sm_m, sm_l, sm_o, c, d, M, num, den);
+      float* ps = part_s + ((size_t)r * nq + kh * GQA + c) * W;
+      st_dev(ps + d, num);
+      if (d == 0) {
+        st_dev(ps + HD, M);
+        st_dev(ps + HD + 1, den);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);                 // the partial is stored before it is counted
+    __syncthreads();
+    if (tid == 0) sm_last[0] = __hip_atomic_fetch_add(cp, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
+    __syncthreads();
+    if (!sm_last[0]) return;
+  }
+  for (int e = tid; e < GQA * HD; e += 256) {
+    const int c = e / HD, d = e % HD;
+    float M, num, den;
+    waves_merged<HD, GQA>(sm_m, sm_l, sm_o, c, d, M, num, den);
+    const float* pp = part_p + ((size_t)r * nq + kh * GQA + c) * W;
+    split_store(orow, col0 + e, merge_partials(ld_dev(pp + HD), ld_dev(pp + HD + 1), ld_dev(pp + d), M, den, num));
+  }
+  if (tid == 0) __hip_atomic_store(cp, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <typename KT, bool SPLIT>
@@ -394,22 +534,23 @@ hipError_t run_mfma(const AttnArgs& a, hipStream_t st) {
   if (ROWS > 1 && a.grp_row0) {         // prompt rows
     hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, RB>), dim3(a.nkv, a.n_groups * (16 / RB)), dim3(256), 0, st, a.q,
                        kc, vc, a.cache.ctx_stride, a.cache.slot_stride, a.row_slot, a.row_pos, a.row_done, a.grp_row0,
-                       a.grp_n, 16 / RB, (const int32_t*)nullptr, (float*)nullptr, (bf16_t*)a.out, a.nq);
+                       a.grp_n, 16 / RB, (bf16_t*)a.out, a.nq);
     return hipGetLastError();
   }
-  if (a.part) {                         // decode rows with a shared prompt prefix: the prefix pass first
-    if (ROWS == 1) return hipErrorInvalidValue;
+  if (a.part) {                         // decode rows with a shared prompt prefix
+    if (ROWS == 1 || !a.row_done || a.pfx_rows < 1 || a.pfx_rows > 16) return hipErrorInvalidValue;
     const int sub = (a.pfx_rows + RB - 1) / RB;
-    if (a.pfx_groups > 0)
-      hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, RB, true>), dim3(a.nkv, a.pfx_groups * sub), dim3(256), 0, st, a.q,
-                         kc, vc, a.cache.ctx_stride, a.cache.slot_stride, a.pfx_slot, a.pfx_pos,
-                         (const int32_t*)nullptr, a.pfx_row0, a.pfx_n, sub, (const int32_t*)nullptr, a.part,
-                         (bf16_t*)nullptr, a.nq);
+    const int n_pfx = a.pfx_groups * sub;
+    const long W = (long)a.R * a.nq * (a.hd + 2);
+    hipLaunchKernelGGL((attn_shared_kernel<HD, (ROWS > 1 ? GQA : 8)>), dim3(a.nkv, n_pfx + a.R), dim3(256), 0, st,
+                       a.q, kc, vc, a.cache.ctx_stride, a.cache.slot_stride, a.row_slot, a.row_pos, a.row_done,
+                       a.row_lo, a.pfx_row0, a.pfx_n, a.pfx_slot, n_pfx, sub, a.part, a.part + W, a.cnt,
+                       (bf16_t*)a.out, a.nq, a.nkv);
+    return hipGetLastError();
   }
   hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, 1>), dim3(a.nkv, a.R), dim3(256), 0, st, a.q, kc, vc,
                      a.cache.ctx_stride, a.cache.slot_stride, a.row_slot, a.row_pos, a.row_done,
-                     (const int32_t*)nullptr, (const int32_t*)nullptr, 1, a.part ? a.row_lo : nullptr, a.part,
-                     (bf16_t*)a.out, a.nq);
+                     (const int32_t*)nullptr, (const int32_t*)nullptr, 1, (bf16_t*)a.out, a.nq);
   return hipGetLastError();
 }
 

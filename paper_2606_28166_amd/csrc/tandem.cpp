@@ -57,7 +57,8 @@ struct ModelPlan {            // byte offsets / sizes of one model's buffers
   size_t ws_floats;
   size_t kv_half;             // bytes of the K (= V) cache
   size_t off_h, off_xa, off_xf, off_q, off_ws, off_logits, off_rope;
-  size_t off_part;            // prefix partials of the decode attention [max_seqs][n_q][hd + 2]
+  size_t off_part;            // partial softmaxes of the decode attention [2][max_seqs][n_q][hd + 2]
+  size_t off_cnt;             // its (row, kv head) counters [max_seqs][n_kv]
   size_t off_packed, packed_bytes;   // MFMA-ordered copies of the projection and LM-head weights
 };
 
@@ -88,7 +89,7 @@ struct Plan {
   ModelPlan m[2];
   size_t kv_bytes;
   size_t off_state, off_seq_slot, off_rows, off_prompt, off_partials, off_count, off_act, off_drows;
-  size_t off_pfx;             // shared-prefix tables of the decode rows (5 x max_seqs int32)
+  size_t off_pfx;             // shared-prefix tables of the decode rows (4 x max_seqs int32)
   size_t scratch_bytes;
 };
 
@@ -117,6 +118,7 @@ struct Model {
   float* logits;
   float2* rope;
   float* part;
+  int32_t* cnt;
 };
 
 tandem_status fail(std::string* where, tandem_status s, const std::string& msg) {
@@ -207,7 +209,8 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
     m.off_ws = sc; sc = align_up(sc + m.ws_floats * 4, kAlign);
     m.off_logits = sc; sc = align_up(sc + (size_t)cap->max_seqs * c->vocab * 4, kAlign);
     m.off_rope = sc; sc = align_up(sc + (size_t)P.ctx_stride * (c->head_dim / 2) * 8, kAlign);
-    m.off_part = sc; sc = align_up(sc + (size_t)cap->max_seqs * c->n_q_heads * (c->head_dim + 2) * 4, kAlign);
+    m.off_part = sc; sc = align_up(sc + (size_t)2 * cap->max_seqs * c->n_q_heads * (c->head_dim + 2) * 4, kAlign);
+    m.off_cnt = sc; sc = align_up(sc + (size_t)cap->max_seqs * c->n_kv_heads * 4, kAlign);
     m.packed_bytes = 0;
     for (const auto& nk : packed_shapes(c))
       if (packs(c, nk.first, nk.second)) m.packed_bytes += align_up(packed_weight_bytes(nk.first, nk.second), kAlign);
@@ -223,7 +226,7 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
   P.off_count = sc; sc = align_up(sc + 4, kAlign);
   P.off_act = sc; sc = align_up(sc + S * 4, kAlign);
   P.off_drows = sc; sc = align_up(sc + 4 * S * 4, kAlign);
-  P.off_pfx = sc; sc = align_up(sc + 5 * S * 4, kAlign);
+  P.off_pfx = sc; sc = align_up(sc + 4 * S * 4, kAlign);
   P.scratch_bytes = sc;
   return P;
 }
@@ -269,10 +272,10 @@ struct tandem_handle {
   // prompt length - 1 rounded down to 16) once per block of rows from the
   // slot of the prompt's first sequence, and each row's own slot from lo on.
   // The tables depend on the act order only (rebuilt at prefill and at each
-  // compaction): per row lo, prefix slot and lo - 1; then pfx_max groups of
-  // at most pfx_rows consecutive rows with the same prefix (unused: 0 rows).
+  // compaction): per row lo and the prefix slot; then pfx_max groups of at
+  // most pfx_rows consecutive rows with the same prefix (unused: 0 rows).
   bool share = false;
-  int32_t *row_lo, *pfx_slot, *pfx_pos, *pfx_row0, *pfx_n;
+  int32_t *row_lo, *pfx_slot, *pfx_row0, *pfx_n;
   int pfx_max = 0, pfx_rows = 0, G = 1;
   std::vector<int32_t> lo_of_prompt;                 // host, per prompt
   std::vector<int32_t> h_pfx, h_act;                 // host staging (kept until the next rebuild)
@@ -527,9 +530,8 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   aa.row_slot = fr.slot; aa.row_pos = fr.pos; aa.row_done = fr.done; aa.out = m.xa;
   aa.grp_row0 = fr.grp_row0; aa.grp_n = fr.grp_n; aa.n_groups = fr.n_groups;
   if (fr.shared_prefix) {
-    aa.row_lo = h->row_lo; aa.part = m.part;
+    aa.row_lo = h->row_lo; aa.pfx_slot = h->pfx_slot; aa.part = m.part; aa.cnt = m.cnt;
     aa.pfx_row0 = h->pfx_row0; aa.pfx_n = h->pfx_n; aa.pfx_groups = h->pfx_max; aa.pfx_rows = h->pfx_rows;
-    aa.pfx_slot = h->pfx_slot; aa.pfx_pos = h->pfx_pos;
   }
   if (att_wait) HIPCHK(hipStreamWaitEvent(st, att_wait, 0));
   TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
@@ -663,15 +665,14 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
 tandem_status upload_prefix_tables(tandem_handle* h, const int32_t* act_host, int R) {
   const int S = h->cap.max_seqs, G = h->G;
   std::vector<int32_t>& t = h->h_pfx;
-  t.assign(5 * (size_t)S, 0);
-  int32_t *lo = t.data(), *ps = lo + S, *pp = lo + 2 * S, *g0 = lo + 3 * S, *gn = lo + 4 * S;
+  t.assign(4 * (size_t)S, 0);
+  int32_t *lo = t.data(), *ps = lo + S, *g0 = lo + 2 * S, *gn = lo + 3 * S;
   int ng = 0;
   for (int r = 0; r < R; ++r) {
     const int s = act_host[r], j = s / G;
     lo[r] = h->lo_of_prompt[j];
     if (lo[r] == 0) continue;
     ps[r] = j * G;                 // slot of the prompt's first sequence (slots follow sequence ids)
-    pp[r] = lo[r] - 1;
     const bool cont = ng > 0 && g0[ng - 1] + gn[ng - 1] == r && act_host[r - 1] / G == j &&
                       (act_host[r - 1] % G) / 16 == (s % G) / 16;
     if (cont) {
@@ -901,6 +902,7 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     m.logits = (float*)(sc + m.p.off_logits);
     m.rope = (float2*)(sc + m.p.off_rope);
     m.part = (float*)(sc + m.p.off_part);
+    m.cnt = (int32_t*)(sc + m.p.off_cnt);
     m.p_lm = nullptr;
   }
   const size_t S = (size_t)cap->max_seqs;
@@ -920,7 +922,7 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   int32_t* drows = (int32_t*)(sc + P.off_drows);
   h->drow_tok = drows; h->drow_slot = drows + S; h->drow_pos = drows + 2 * S; h->drow_done = drows + 3 * S;
   int32_t* pfx = (int32_t*)(sc + P.off_pfx);
-  h->row_lo = pfx; h->pfx_slot = pfx + S; h->pfx_pos = pfx + 2 * S; h->pfx_row0 = pfx + 3 * S; h->pfx_n = pfx + 4 * S;
+  h->row_lo = pfx; h->pfx_slot = pfx + S; h->pfx_row0 = pfx + 2 * S; h->pfx_n = pfx + 3 * S;
   h->h_count = nullptr;
 
   // --- HIP work from here on
@@ -1009,6 +1011,9 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   if (e != hipSuccess) return bail(e, "seq slots");
   e = hipMemsetAsync(stt, 0, 6 * S * 4, h->stream);
   if (e != hipSuccess) return bail(e, "state");
+  for (int i = 0; i < 2 && e == hipSuccess; ++i)       // the attention counters start (and stay) at zero
+    e = hipMemsetAsync(h->m[i].cnt, 0, S * h->m[i].cfg.n_kv_heads * 4, h->stream);
+  if (e != hipSuccess) return bail(e, "attention counters");
   e = hipStreamSynchronize(h->stream);
   if (e != hipSuccess) return bail(e, "synchronize");
   *out_handle = h;

@@ -9,13 +9,14 @@ step graph, so that the contexts reach the middle of the benchmark's
 per kernel).  Counters are collected for the attention kernels and the copy
 only:
 
-    cd /tmp && rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'attn_mfma|copy' -d <dir> -o fetch \\
+    cd /tmp && rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'attn_shared|copy' -d <dir> -o fetch \\
         --output-format csv -- python3 <repo>/paper_2606_28166_amd/pmc_probe.py
-    cd /tmp && rocprofv3 --pmc WRITE_SIZE --kernel-include-regex 'attn_mfma|copy' -d <dir> -o write \\
+    cd /tmp && rocprofv3 --pmc WRITE_SIZE --kernel-include-regex 'attn_shared|copy' -d <dir> -o write \\
         --output-format csv -- python3 <repo>/paper_2606_28166_amd/pmc_probe.py
 
 Analysis mode: the counters of the last STEPS steps' attention dispatches
-(both models; the shared-prefix pass and the per-row pass of every call) x
+(both models; each reads the shared prompt prefix once per block of rows and
+every row's own positions) x
 (copy bytes / copy counter KiB) against the algorithmic K/V bytes of those
 steps (a shared prompt prefix once per group); prints a JSON summary (the
 ratio traffic / algorithmic bytes is what the benchmark applies to its own
@@ -101,10 +102,10 @@ def analyze(fetch_csv: str, write_csv: str) -> dict:
         if not copies:
             raise SystemExit(f"no copy kernel in {path}")
         cal = max(copies)                        # KiB the counter reports for COPY_BYTES
-        # the measured launches are the last STEPS * (both models' layers) x
-        # (prefix pass + per-row pass) attention dispatches
-        n_dec = STEPS * 2 * (wl.senior.n_layers + wl.junior.n_layers)
-        att = [(k, v) for _, k, v in rows if "attn_mfma_kernel" in k][-n_dec:]
+        # the measured launches are the last STEPS * (both models' layers)
+        # attention dispatches
+        n_dec = STEPS * (wl.senior.n_layers + wl.junior.n_layers)
+        att = [(k, v) for _, k, v in rows if "attn_shared_kernel" in k][-n_dec:]
         res[name] = {"copy_counter_kib": cal, "scale_bytes_per_kib": COPY_BYTES / cal,
                      "attention_dispatches": len(att)}
         res[name]["attention_counter_kib"] = [v for _, v in att]
