@@ -57,7 +57,9 @@ def log(msg: str) -> None:
 
 def run(wl: W.Workload, steps: Optional[int] = None, logits_at: Sequence[int] = (1,),
         max_prefill_tokens: int = 4096, seq_subset: Optional[Sequence[int]] = None,
-        weights=None) -> Parity:
+        weights=None, before=None) -> Parity:
+    """before: called with the engine before this batch's prefill (earlier use of
+    the same handle)."""
     from paper_2606_28166_amd.engine import TandemEngine
     steps = steps or wl.sample.max_new
     ws, wj, prompts, bnd = weights if weights is not None else W.make_all(wl)
@@ -76,6 +78,8 @@ def run(wl: W.Workload, steps: Optional[int] = None, logits_at: Sequence[int] = 
     eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed,
                        max_seqs=n, max_ctx=max_ctx, max_prefill_tokens=max_prefill_tokens,
                        boundary_words=W.boundary_bits(bnd))
+    if before is not None:
+        before(eng)
     eng.prefill(prompts, wl.group)
     sampled = np.full((len(rows), wl.sample.max_new), -1, np.int32)
     margin = np.zeros((len(rows), wl.sample.max_new), np.float32)

@@ -74,6 +74,29 @@ def test_shared_prompt_prefix_edges():
     P.check(p, P.TOL_BF16)
 
 
+def test_second_prefill_on_one_handle():
+    """A handle takes a new batch of another shape: a first batch (2 prompts x
+    G=4) runs 20 graph-replayed steps, then 3 ragged prompts x G=3 are prefilled
+    on the same handle and match the oracle (the shared-prefix tables, the
+    attention counters and the step graph are rebuilt or reused)."""
+    P.log("case second prefill on one handle: small shapes 2+1 layers, 2x4 rows then 3x3 ragged rows")
+    wl = _small_reduced()
+    lengths = [33, 90, 17]
+    wl.n_prompts, wl.group, wl.prompt_len, wl.prompt_len_min = len(lengths), 3, max(lengths), None
+    ws, wj, _, bnd = W.make_all(wl)
+    rng = np.random.default_rng(5)
+    first = [rng.integers(0, wl.senior.vocab, size=n).astype(np.int32) for n in (70, 41)]
+    prompts = [rng.integers(0, wl.senior.vocab, size=n).astype(np.int32) for n in lengths]
+
+    def first_batch(eng):
+        eng.prefill(first, 4)
+        for _ in range(20):
+            eng.step()
+
+    p = P.run(wl, logits_at=(1, 24), weights=(ws, wj, prompts, bnd), before=first_batch)
+    P.check(p, P.TOL_BF16)
+
+
 def test_paper_schedule_redraw_word_boundaries_and_cap():
     P.log("case paper schedule: REDRAW p=0.5, K=3, drawn first owner, 35% boundary bitmap, T=0.6")
     wl = _tiny("bf16")
