@@ -74,6 +74,21 @@ def test_shared_prompt_prefix_edges():
     P.check(p, P.TOL_BF16)
 
 
+@pytest.mark.parametrize("shape", ["small", "qwen"])
+def test_one_sequence_per_prompt_unshared_attention(shape):
+    """G = 1: no prompt prefix to share, so decode attention takes the per-row
+    kernel over each row's whole context (head_dim 64 and 128)."""
+    P.log(f"case G=1 ({shape} shapes): per-row decode attention without a shared prefix")
+    if shape == "small":
+        wl = _small_reduced()
+        wl.n_prompts, wl.group = 5, 1
+    else:
+        wl = _qwen_reduced()
+        wl.n_prompts, wl.group, wl.prompt_len_min = 3, 1, 20
+    p = P.run(wl, logits_at=(1, wl.sample.max_new))
+    P.check(p, P.TOL_BF16)
+
+
 def test_second_prefill_on_one_handle():
     """A handle takes a new batch of another shape: a first batch (2 prompts x
     G=4) runs 20 graph-replayed steps, then 3 ragged prompts x G=3 are prefilled
