@@ -51,6 +51,11 @@ DESCRIPTIONS = {
     "tiny": "2-layer d=128 senior + 1-layer d=64 junior, fp32, 1 prompt x G=4, 32 new tokens",
     "longcot": "small shapes, 32 prompts x G=8 = 256 sequences, ragged prompts 64..512, up to 8192 new tokens, "
                "EOS bias for mean length 4000, ownership switch p=0.3 per 32-token chunk, finished sequences compacted",
+    "paper": "small shapes, 4 prompts x G=8, prompt 64, 128 new tokens, the paper's schedule: word-level REDRAW "
+             "p=0.5, span cap K=32, drawn first owner, T=0.6, 35% boundary bitmap",
+    "qwen-paper": "Qwen3-4B-shaped senior + Qwen3-0.6B-shaped junior, bf16, 16 prompts x G=8, prompt 256, 2048 new "
+                  "tokens, the paper's schedule: word-level REDRAW p=0.5, span cap K=32, drawn first owner, T=0.6, "
+                  "35% boundary bitmap",
 }
 
 
@@ -265,7 +270,7 @@ def main():
     # around every launch on the stream it runs on: one with the two forwards
     # serialized (each launch alone on the GPU: the kernel's own roofline, and
     # the per-class breakdown), one in the production two-stream schedule.
-    traffic_ratio = measured_traffic_ratio() if wl.name == "qwen" else None
+    traffic_ratio = measured_traffic_ratio() if wl.name in ("qwen", "qwen-paper") else None
 
     def roofline_of(att, method):
         ms, nl = att

@@ -122,6 +122,19 @@ def test_paper_schedule_redraw_word_boundaries_and_cap():
     assert p.ref.decided.sum() > 0 and 0 < p.ref.owner.mean() < 1
 
 
+def test_paper_schedule_at_qwen_shapes():
+    """The paper's training schedule (word-level REDRAW, p = 0.5, span cap 32,
+    drawn first owner, T = 0.6, 35% boundary bitmap) on the Qwen shapes."""
+    P.log("case paper schedule at Qwen shapes, 2+2 layers, 40 steps")
+    wl = _qwen_reduced()
+    paper = W.workload("qwen-paper")
+    wl.switch, wl.sample.temperature = paper.switch, paper.sample.temperature
+    wl.sample.max_new = 40
+    p = P.run(wl, logits_at=(1, 40))
+    P.check(p, P.TOL_BF16)
+    assert p.ref.decided.sum() > 0 and 0 < p.ref.owner.mean() < 1
+
+
 def test_eos_stops_sequences():
     P.log("case EOS with logit bias")
     wl = _tiny("f32")

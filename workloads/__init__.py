@@ -151,10 +151,15 @@ def workload(name: str) -> Workload:
         return Workload("paper", sen, jun, 4, 8, 64, None,
                         SwitchSettings(REDRAW, 0.5, 32, "random:0.351", DRAW),
                         SampleSettings(0.6, -1, 0.0, 0.0, 128), 6)
+    if name == "qwen-paper":
+        # The Qwen-shaped batch of "qwen" under the paper's training schedule.
+        w = workload("qwen")
+        return w.replace(name="qwen-paper", switch=SwitchSettings(REDRAW, 0.5, 32, "random:0.351", DRAW),
+                         sample=SampleSettings(0.6, -1, 0.0, 0.0, 2048), seed_base=7)
     raise KeyError(name)
 
 
-NAMES = ("tiny", "small", "qwen", "longcot", "wide", "paper")
+NAMES = ("tiny", "small", "qwen", "longcot", "wide", "paper", "qwen-paper")
 
 
 def scaled(shape: ModelShape, **kw) -> ModelShape:
