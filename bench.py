@@ -56,6 +56,8 @@ DESCRIPTIONS = {
     "qwen-paper": "Qwen3-4B-shaped senior + Qwen3-0.6B-shaped junior, bf16, 16 prompts x G=8, prompt 256, 2048 new "
                   "tokens, the paper's schedule: word-level REDRAW p=0.5, span cap K=32, drawn first owner, T=0.6, "
                   "35% boundary bitmap",
+    "self-paired": "Qwen3-4B-shaped senior + Qwen3-4B-shaped junior, bf16, 16 prompts x G=8, prompt 256, 3000 new "
+                   "tokens, the paper's schedule (REDRAW p=0.5, K=32, drawn first owner, T=0.6, 35% boundary bitmap)",
 }
 
 

@@ -156,10 +156,16 @@ def workload(name: str) -> Workload:
         w = workload("qwen")
         return w.replace(name="qwen-paper", switch=SwitchSettings(REDRAW, 0.5, 32, "random:0.351", DRAW),
                          sample=SampleSettings(0.6, -1, 0.0, 0.0, 2048), seed_base=7)
+    if name == "self-paired":
+        # Two Qwen3-4B-shaped models (the paper's self-paired training pair),
+        # 16 prompts x G=8, 3000 new tokens, the paper's schedule.
+        w = workload("qwen-paper")
+        return w.replace(name="self-paired", junior=copy.deepcopy(w.senior),
+                         sample=SampleSettings(0.6, -1, 0.0, 0.0, 3000), seed_base=8)
     raise KeyError(name)
 
 
-NAMES = ("tiny", "small", "qwen", "longcot", "wide", "paper", "qwen-paper")
+NAMES = ("tiny", "small", "qwen", "longcot", "wide", "paper", "qwen-paper", "self-paired")
 
 
 def scaled(shape: ModelShape, **kw) -> ModelShape:
