@@ -188,6 +188,20 @@ tandem_status tandem_step(tandem_handle* h, int32_t* n_active);
 tandem_status tandem_step_forced(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg,
                                  int32_t* n_active);
 
+/* Dual-distribution scores of the step just taken (teacher-forced or free):
+ * the junior legibility and distribution overlap measures of the paper's
+ * evaluation (junior per-token cross-entropy; overlap alpha = sum_v
+ * min(p_sen(v), p_jun(v))) and the per-position divergence of the senior from
+ * the junior that its KL-regularisation ablation penalises.  Both models'
+ * next-token distributions are taken at temperature 1 with no EOS bias.  For
+ * every sequence s that was not done before the step, scores[3 s .. 3 s + 2]
+ * (device float [max_seqs][3], caller-owned) receive (-log p_jun(y), alpha,
+ * KL(p_sen || p_jun)), y being the token the step appended to s; entries of
+ * other sequences are left untouched.  Asynchronous on the handle's stream.
+ * TANDEM_E_STATE when no step has been taken since the last prefill;
+ * TANDEM_E_ARG when scores is NULL. */
+tandem_status tandem_score_step(tandem_handle* h, float* scores);
+
 /* Copy the per-sequence sampler state to HOST int32 arrays of n_seqs
  * entries (any pointer may be NULL): owner (1 = senior), span counter c,
  * next step t, next position, done flag.  Synchronises the stream. */

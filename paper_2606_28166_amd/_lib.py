@@ -55,7 +55,7 @@ class Debug(C.Structure):
 
 
 EXPORTS = ("tandem_workspace_size", "tandem_init", "tandem_prefill", "tandem_step",
-           "tandem_step_forced", "tandem_get_state", "tandem_timing_enable", "tandem_timing_read",
+           "tandem_step_forced", "tandem_score_step", "tandem_get_state", "tandem_timing_enable", "tandem_timing_read",
            "tandem_last_error", "tandem_status_string", "tandem_destroy")
 K_ATTENTION, K_GEMM, K_SAMPLE, K_OTHER = 0, 1, 2, 3
 TIMING_SERIAL = 1 << 8          # timing flag: run the two forwards one after the other
@@ -84,6 +84,8 @@ def _load():
     lib.tandem_step.restype = st
     lib.tandem_step_forced.argtypes = [P, P, C.POINTER(Debug), C.POINTER(C.c_int32)]
     lib.tandem_step_forced.restype = st
+    lib.tandem_score_step.argtypes = [P, P]
+    lib.tandem_score_step.restype = st
     lib.tandem_get_state.argtypes = [P, P, P, P, P, P]
     lib.tandem_get_state.restype = st
     lib.tandem_timing_enable.argtypes = [P, C.c_int32]
@@ -145,6 +147,10 @@ def tandem_step_forced(h, forced_ptr: int, dbg: Debug = None, want_active: bool 
     check(lib.tandem_step_forced(h, forced_ptr, C.byref(dbg) if dbg is not None else None,
                                  C.byref(n) if want_active else None), h)
     return n.value if want_active else None
+
+
+def tandem_score_step(h, scores_ptr: int) -> None:
+    check(lib.tandem_score_step(h, scores_ptr), h)
 
 
 def tandem_get_state(h, n_seq: int):

@@ -317,6 +317,115 @@ __global__ __launch_bounds__(kNT) void sample_partials_kernel(SampleArgs a) {
   }
 }
 
+// ------------------------------------------------- dual-distribution scores
+// Block-wide merge of (max, sum of e^(x - max)) pairs through the waves.
+__device__ __forceinline__ void block_lse(float& m, float& l, float (*sm)[2]) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, 64), l2 = __shfl_xor(l, o, 64);
+    merge_lse(m, l, m2, l2);
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) { sm[wave][0] = m; sm[wave][1] = l; }
+  __syncthreads();
+  m = sm[0][0]; l = sm[0][1];
+  for (int w = 1; w < kNT / 64; ++w) merge_lse(m, l, sm[w][0], sm[w][1]);
+}
+
+// One more value x in a running (max m, sum l of e^(v - m)).
+__device__ __forceinline__ void lse_add(float& m, float& l, float x) {
+  if (x > m) {
+    l = l * expf(m - x) + 1.f;
+    m = x;
+  } else {
+    l += expf(x - m);
+  }
+}
+
+// Pass 1, per (chunk, row): online log-sum-exp partials of both models' logits.
+__global__ __launch_bounds__(kNT) void score_lse_kernel(ScoreArgs a) {
+  __shared__ float sm[kNT / 64][2];
+  const int ch = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
+  if (a.row_done[r]) return;
+  const int v0 = ch * a.chunk, v1 = min(a.V, v0 + a.chunk);
+  const float* zs = a.z_sen + (size_t)r * a.V;
+  const float* zj = a.z_jun + (size_t)r * a.V;
+  float ms = -INFINITY, ls = 0.f, mj = -INFINITY, lj = 0.f;
+  for (int v = v0 + tid; v < v1; v += kNT) {
+    lse_add(ms, ls, zs[v]);
+    lse_add(mj, lj, zj[v]);
+  }
+  block_lse(ms, ls, sm);
+  block_lse(mj, lj, sm);
+  if (tid == 0) {
+    float* p = a.lse + ((size_t)r * a.n_chunks + ch) * 4;
+    p[0] = ms; p[1] = ls; p[2] = mj; p[3] = lj;
+  }
+}
+
+// The row's log-partition functions (log sum_v e^z) of both models from the
+// pass-1 partials, in a fixed order.
+__device__ __forceinline__ void row_logz(const ScoreArgs& a, int r, float& Ls, float& Lj) {
+  float ms = -INFINITY, ls = 0.f, mj = -INFINITY, lj = 0.f;
+  for (int c = 0; c < a.n_chunks; ++c) {
+    const float* p = a.lse + ((size_t)r * a.n_chunks + c) * 4;
+    merge_lse(ms, ls, p[0], p[1]);
+    merge_lse(mj, lj, p[2], p[3]);
+  }
+  Ls = ms + logf(ls);
+  Lj = mj + logf(lj);
+}
+
+// Pass 2, per (chunk, row): sums of min(p_sen, p_jun) and p_sen (log p_sen - log p_jun).
+__global__ __launch_bounds__(kNT) void score_sum_kernel(ScoreArgs a) {
+  __shared__ float red[kNT / 64];
+  __shared__ float logz[2];
+  const int ch = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
+  if (a.row_done[r]) return;
+  if (tid == 0) row_logz(a, r, logz[0], logz[1]);
+  __syncthreads();
+  const float Ls = logz[0], Lj = logz[1];
+  const int v0 = ch * a.chunk, v1 = min(a.V, v0 + a.chunk);
+  const float* zs = a.z_sen + (size_t)r * a.V;
+  const float* zj = a.z_jun + (size_t)r * a.V;
+  float smin = 0.f, skl = 0.f;
+  for (int v = v0 + tid; v < v1; v += kNT) {
+    const float lps = zs[v] - Ls, lpj = zj[v] - Lj;
+    const float ps = expf(lps), pj = expf(lpj);
+    smin += fminf(ps, pj);
+    skl += ps * (lps - lpj);
+  }
+  smin = block_sum<kNT>(smin, red);
+  __syncthreads();
+  skl = block_sum<kNT>(skl, red);
+  if (tid == 0) {
+    float* p = a.sums + ((size_t)r * a.n_chunks + ch) * 2;
+    p[0] = smin; p[1] = skl;
+  }
+}
+
+// One thread per row: the chunk sums in order and the junior's cross-entropy.
+__global__ void score_finish_kernel(ScoreArgs a) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= a.R || a.row_done[r]) return;
+  float Ls, Lj;
+  row_logz(a, r, Ls, Lj);
+  float smin = 0.f, skl = 0.f;
+  for (int c = 0; c < a.n_chunks; ++c) {
+    const float* p = a.sums + ((size_t)r * a.n_chunks + c) * 2;
+    smin += p[0];
+    skl += p[1];
+  }
+  const int s = a.act[r];
+  int y = a.tok[s];
+  y = y < 0 ? 0 : (y >= a.V ? a.V - 1 : y);
+  float* o = a.out + (size_t)s * 3;
+  o[0] = Lj - a.z_jun[(size_t)r * a.V + y];
+  o[1] = smin;
+  o[2] = skl;
+}
+
 // One wave per row: merge the chunk partials, pick the token, compute the
 // senior log-prob, write the outputs and apply the handoff rule.
 __global__ __launch_bounds__(64) void sample_finish_kernel(FinishArgs a) {
@@ -563,6 +672,15 @@ hipError_t launch_rope_table(float theta, int hd, int n_pos, float2* out, hipStr
 hipError_t launch_sample_partials(const SampleArgs& a, int n_chunks, hipStream_t st) {
   if (a.R <= 0) return hipSuccess;
   hipLaunchKernelGGL(sample_partials_kernel, dim3(n_chunks, a.R), dim3(kNT), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_score(const ScoreArgs& a, hipStream_t st) {
+  if (a.R <= 0) return hipSuccess;
+  if (a.chunk < 1 || a.n_chunks < 1 || (long)a.chunk * a.n_chunks < a.V) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(score_lse_kernel, dim3(a.n_chunks, a.R), dim3(kNT), 0, st, a);
+  hipLaunchKernelGGL(score_sum_kernel, dim3(a.n_chunks, a.R), dim3(kNT), 0, st, a);
+  hipLaunchKernelGGL(score_finish_kernel, dim3((a.R + 63) / 64), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 

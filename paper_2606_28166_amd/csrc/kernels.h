@@ -181,6 +181,20 @@ struct FinishArgs {
 };
 hipError_t launch_sample_finish(const FinishArgs& a, hipStream_t st);
 
+// Dual-distribution scores of the rows of the step just taken, from both
+// models' logits [R][V] (temperature 1, no bias): per sequence act[r] of a
+// row not done before the step (row_done[r] == 0), with y = tok[act[r]]
+// the token the step emitted, out[act[r]][0 .. 2] = (-log p_jun(y),
+// sum_v min(p_sen, p_jun), KL(p_sen || p_jun)).  lse: [R][n_chunks][4],
+// sums: [R][n_chunks][2] of scratch; chunk vocabulary entries per chunk.
+struct ScoreArgs {
+  const float* z_sen; const float* z_jun; int R, V;
+  const int32_t* act; const int32_t* row_done; const int32_t* tok;
+  float* lse; float* sums; int chunk, n_chunks;
+  float* out;
+};
+hipError_t launch_score(const ScoreArgs& a, hipStream_t st);
+
 // Copy positions [p0, n_pos) of slot src into slots dst0 .. dst0 + n_dst - 1
 // for every layer and kv head (K and transposed V); p0 % 16 == 0.
 hipError_t launch_kv_replicate(int dt, void* kc, void* vc, int n_layers, long layer_stride,

@@ -90,6 +90,7 @@ struct Plan {
   size_t kv_bytes;
   size_t off_state, off_seq_slot, off_rows, off_prompt, off_partials, off_count, off_act, off_drows;
   size_t off_pfx;             // shared-prefix tables of the decode rows (4 x max_seqs int32)
+  size_t off_score;           // dual-distribution score partials [max_seqs][n_chunks][6]
   size_t scratch_bytes;
 };
 
@@ -227,6 +228,7 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
   P.off_act = sc; sc = align_up(sc + S * 4, kAlign);
   P.off_drows = sc; sc = align_up(sc + 4 * S * 4, kAlign);
   P.off_pfx = sc; sc = align_up(sc + 4 * S * 4, kAlign);
+  P.off_score = sc; sc = align_up(sc + S * P.n_chunks * 6 * 4, kAlign);
   P.scratch_bytes = sc;
   return P;
 }
@@ -286,6 +288,8 @@ struct tandem_handle {
   int32_t* h_count;           // pinned
   int n_seq = 0;
   bool prefilled = false;
+  bool stepped = false;       // a step has run since the last prefill (its logits are in place)
+  float* score_part = nullptr;  // partials of tandem_score_step
   bool poisoned = false;
   std::string err = "no error";
   std::vector<int32_t> hbuf;  // host staging of prefill metadata
@@ -767,6 +771,7 @@ tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_de
     tandem_status s = record_step(h, forced, dbg);
     if (s != TANDEM_OK) return s;
   }
+  h->stepped = true;
   if (n_active) {
     HIPCHK(launch_count_active(h->done, h->n_seq, h->d_count, st));
     HIPCHK(hipMemcpyAsync(h->h_count, h->d_count, 4, hipMemcpyDeviceToHost, st));
@@ -921,6 +926,7 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   h->act = (int32_t*)(sc + P.off_act);
   int32_t* drows = (int32_t*)(sc + P.off_drows);
   h->drow_tok = drows; h->drow_slot = drows + S; h->drow_pos = drows + 2 * S; h->drow_done = drows + 3 * S;
+  h->score_part = (float*)(sc + P.off_score);
   int32_t* pfx = (int32_t*)(sc + P.off_pfx);
   h->row_lo = pfx; h->pfx_slot = pfx + S; h->pfx_row0 = pfx + 2 * S; h->pfx_n = pfx + 3 * S;
   h->h_count = nullptr;
@@ -1146,6 +1152,7 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
   }
   h->steps_since_compact = 0;
   h->prefilled = true;
+  h->stepped = false;
   return TANDEM_OK;
 }
 
@@ -1155,6 +1162,25 @@ tandem_status tandem_step_forced(tandem_handle* h, const int32_t* forced, const 
                                  int32_t* n_active) {
   if (h && !forced) return fail(&h->err, TANDEM_E_ARG, "tandem_step_forced: forced is NULL");
   return step_impl(h, forced, dbg, n_active);
+}
+
+tandem_status tandem_score_step(tandem_handle* h, float* scores) {
+  if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
+  if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
+  if (!scores) return fail(&h->err, TANDEM_E_ARG, "tandem_score_step: scores is NULL");
+  if (!h->prefilled || !h->stepped)
+    return fail(&h->err, TANDEM_E_STATE, "tandem_score_step before a step of the current batch");
+  // the step's rows: its act order, launched row count, done-at-start flags and
+  // logits are all still in place (compaction runs at the start of a step)
+  ScoreArgs a{};
+  a.z_sen = h->m[0].logits; a.z_jun = h->m[1].logits; a.R = h->R_launch; a.V = h->m[0].cfg.vocab;
+  a.act = h->act; a.row_done = h->drow_done; a.tok = h->pending;
+  a.lse = h->score_part;
+  a.sums = a.lse + (size_t)h->cap.max_seqs * h->plan.n_chunks * 4;
+  a.chunk = kVocabChunk; a.n_chunks = h->plan.n_chunks;
+  a.out = scores;
+  HIPCHK(launch_score(a, h->stream));
+  return TANDEM_OK;
 }
 
 tandem_status tandem_get_state(tandem_handle* h, int32_t* owner, int32_t* c, int32_t* t, int32_t* pos,

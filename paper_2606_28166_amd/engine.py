@@ -128,6 +128,16 @@ class TandemEngine:
         names = {L.K_ATTENTION: "attention", L.K_GEMM: "gemm", L.K_SAMPLE: "sample", L.K_OTHER: "other"}
         return {v: L.tandem_timing_read(self.h, k) for k, v in names.items()}
 
+    def score(self, out=None):
+        """Dual-distribution scores of the step just taken: a device float32
+        tensor [max_seqs][3] of (junior cross-entropy of the appended token,
+        overlap, KL(senior || junior)) by sequence id; rows of sequences that
+        were done before the step keep their previous contents."""
+        if out is None:
+            out = torch.full((self.max_seqs, 3), float("nan"), dtype=torch.float32, device=self.dev)
+        L.tandem_score_step(self.h, out.data_ptr())
+        return out
+
     def state(self):
         owner, c, t, pos, done = L.tandem_get_state(self.h, self.n_seq)
         return dict(owner=np.array(owner), c=np.array(c), t=np.array(t), pos=np.array(pos), done=np.array(done))
