@@ -193,6 +193,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-isolated", action="store_true",
                     help="skip the extra rollout that times every kernel class with the forwards serialized")
+    ap.add_argument("--score", type=int, default=0, metavar="STEPS",
+                    help="also time tandem_score_step after each of STEPS decode steps (reported as 'scoring')")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -298,6 +300,28 @@ def main():
                                                  "from the host, a HIP event pair around every attention launch")
         log(f"[bench] concurrent instrumented rollout: decode {d_con:.1f} ms, attention -> {roof_conc['achieved']:.0f} GB/s")
 
+    scoring = None
+    if args.score > 0:
+        # the dual-distribution scores after each step of a fresh rollout:
+        # HIP events on the library's stream around every scoring call
+        eng.prefill(prompts, wl.group)
+        out = torch.empty((wl.n_seqs, 3), dtype=torch.float32, device=eng.dev)
+        tot, ns = 0.0, min(args.score, L)
+        for _ in range(ns):
+            eng.step()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            eng.score(out)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            tot += e0.elapsed_time(e1)
+        ms = tot / ns
+        nbytes = 4 * n * wl.senior.vocab * 4          # two passes over both models' fp32 logits
+        scoring = {"steps": ns, "ms_per_step": round(ms, 4), "bytes_per_step": nbytes,
+                   "achieved_gbs": round(nbytes / (ms / 1e3) / 1e9, 1),
+                   "frac_of_decode_step": round(ms / (sum(dec) / (L * args.steps)), 4)}
+        log(f"[bench] scoring: {ms * 1e3:.1f} us per step ({scoring['achieved_gbs']:.0f} GB/s)")
+
     cpu = None
     if not args.no_cpu_baseline:
         eng_models = None
@@ -335,6 +359,8 @@ def main():
         "senior_share": round(senior_share, 4),
         "breakdown": breakdown,
     }
+    if scoring is not None:
+        res["scoring"] = scoring
     eng.close()
     print(json.dumps(res), flush=True)
 

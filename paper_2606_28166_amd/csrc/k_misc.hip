@@ -333,13 +333,13 @@ __device__ __forceinline__ void block_lse(float& m, float& l, float (*sm)[2]) {
   for (int w = 1; w < kNT / 64; ++w) merge_lse(m, l, sm[w][0], sm[w][1]);
 }
 
-// One more value x in a running (max m, sum l of e^(v - m)).
+// One more value x in a running (max m, sum l of e^(v - m)) (hardware exp2).
 __device__ __forceinline__ void lse_add(float& m, float& l, float x) {
   if (x > m) {
-    l = l * expf(m - x) + 1.f;
+    l = l * fast_exp(m - x) + 1.f;
     m = x;
   } else {
-    l += expf(x - m);
+    l += fast_exp(x - m);
   }
 }
 
@@ -392,7 +392,7 @@ __global__ __launch_bounds__(kNT) void score_sum_kernel(ScoreArgs a) {
   float smin = 0.f, skl = 0.f;
   for (int v = v0 + tid; v < v1; v += kNT) {
     const float lps = zs[v] - Ls, lpj = zj[v] - Lj;
-    const float ps = expf(lps), pj = expf(lpj);
+    const float ps = fast_exp(lps), pj = fast_exp(lpj);
     smin += fminf(ps, pj);
     skl += ps * (lps - lpj);
   }
@@ -405,18 +405,28 @@ __global__ __launch_bounds__(kNT) void score_sum_kernel(ScoreArgs a) {
   }
 }
 
-// One thread per row: the chunk sums in order and the junior's cross-entropy.
-__global__ void score_finish_kernel(ScoreArgs a) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= a.R || a.row_done[r]) return;
-  float Ls, Lj;
-  row_logz(a, r, Ls, Lj);
-  float smin = 0.f, skl = 0.f;
-  for (int c = 0; c < a.n_chunks; ++c) {
-    const float* p = a.sums + ((size_t)r * a.n_chunks + c) * 2;
-    smin += p[0];
-    skl += p[1];
+// One wave per row: the chunk sums (lane-strided, then a fixed butterfly)
+// and the junior's cross-entropy.
+__global__ __launch_bounds__(64) void score_finish_kernel(ScoreArgs a) {
+  const int r = blockIdx.x, lane = threadIdx.x;
+  if (a.row_done[r]) return;
+  float mj = -INFINITY, lj = 0.f, smin = 0.f, skl = 0.f;
+  for (int c = lane; c < a.n_chunks; c += 64) {
+    const float* p = a.lse + ((size_t)r * a.n_chunks + c) * 4;
+    merge_lse(mj, lj, p[2], p[3]);
+    const float* q = a.sums + ((size_t)r * a.n_chunks + c) * 2;
+    smin += q[0];
+    skl += q[1];
   }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(mj, o, 64), l2 = __shfl_xor(lj, o, 64);
+    merge_lse(mj, lj, m2, l2);
+    smin += __shfl_xor(smin, o, 64);
+    skl += __shfl_xor(skl, o, 64);
+  }
+  if (lane != 0) return;
+  const float Lj = mj + logf(lj);
   const int s = a.act[r];
   int y = a.tok[s];
   y = y < 0 ? 0 : (y >= a.V ? a.V - 1 : y);
@@ -680,7 +690,7 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t st) {
   if (a.chunk < 1 || a.n_chunks < 1 || (long)a.chunk * a.n_chunks < a.V) return hipErrorInvalidValue;
   hipLaunchKernelGGL(score_lse_kernel, dim3(a.n_chunks, a.R), dim3(kNT), 0, st, a);
   hipLaunchKernelGGL(score_sum_kernel, dim3(a.n_chunks, a.R), dim3(kNT), 0, st, a);
-  hipLaunchKernelGGL(score_finish_kernel, dim3((a.R + 63) / 64), dim3(64), 0, st, a);
+  hipLaunchKernelGGL(score_finish_kernel, dim3(a.R), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 
