@@ -2,8 +2,8 @@
 
 The long-CoT workload stops sequences at an EOS token whose logit bias makes
 the stop lengths geometric with mean 4000 tokens, i.e. a per-step EOS
-probability of 1/4000 under each model's own distribution (reading Q14 of
-the design notes; the paper fixes neither the EOS rate nor the bias).  This
+probability of 1/4000 under each model's own distribution (a choice of
+this implementation: the paper fixes neither the EOS rate nor the bias).  This
 script measures, with the float64 oracle, each model's mean EOS probability
 over a seeded calibration batch (the workload's first prompts, free-running
 decode steps) as a function of the bias b, and finds b by bisection:

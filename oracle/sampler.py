@@ -5,11 +5,12 @@
   y = argmax_v (s_v + g_v) with g_v = -log(-log u_v), u_v uniform in (0, 1),
   which draws y ~ softmax(s) exactly.  Only the owner's distribution is
   sampled: the owner a_t is fixed before step t, so keeping y^{a_t} of two
-  independent samples has the same law (reading Q9).  The decision is taken
+  independent samples has the same law.  The decision is taken
   in float32, the GPU kernel's precision.
 * Senior log-probability (the L_TRL equation of Section 3.4): the loss
   needs log pi_sen(y_t | x . y_<t) at senior-owned positions; it is returned
-  at every position, taken from the sampling distribution (reading Q8).
+  at every position, taken from the sampling distribution (the paper does
+  not say at which temperature; the sampling one is what GRPO's pi_old is).
 * Handoff (Algorithm 1's boundary-or-cap block; word-level handoff details
   in the appendix): after y_t is emitted, if y_t is a boundary token or the
   span counter c has reached K, a Bernoulli(p) draw picks the next owner and
@@ -52,7 +53,7 @@ def gumbel_noise(seed: int, s: int, t: int, V: int) -> np.ndarray:
 def gumbel_argmax(s_owner: np.ndarray, g: np.ndarray):
     """Gumbel-max decision in float32: returns (token, margin best - second).
 
-    Ties go to the smallest token id (reading Q17).
+    Ties go to the smallest token id (the paper does not say).
     """
     val = s_owner.astype(np.float32) + g.astype(np.float32)
     y = int(np.argmax(val))                       # first maximum = smallest id

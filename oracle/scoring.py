@@ -1,8 +1,9 @@
 """Oracle of the dual-distribution scores of a token stream — TEST INFRASTRUCTURE ONLY.
 
 At one position, both models' next-token distributions over the shared
-vocabulary (temperature 1, no sampling bias: the models' own distributions,
-reading Q16) and the token y that the stream emits there give:
+vocabulary (temperature 1, no sampling bias: the models' own distributions;
+the paper states no temperature for these measures) and the token y that
+the stream emits there give:
 
 * the junior's cross-entropy of y, -log p_jun(y), in nats (the per-token
   junior legibility measure of the evaluation section on junior legibility);

@@ -113,7 +113,7 @@ def _small_pair(vocab=32000):
 
 
 def workload(name: str) -> Workload:
-    """The synthetic workloads by name (model shapes, batch, schedule; readings Q1-Q15)."""
+    """The synthetic workloads by name (model shapes, batch, schedule)."""
     if name == "tiny":
         sen = ModelShape(2, 128, 4, 2, 32, 512, 512, dtype="f32")
         jun = ModelShape(1, 64, 2, 1, 32, 256, 512, dtype="f32")
@@ -312,3 +312,34 @@ def make_all(wl: Workload):
     ws = make_weights(wl.senior, 1000 + wl.seed_base, wl.gain_jitter)
     wj = make_weights(wl.junior, 2000 + wl.seed_base, wl.gain_jitter)
     return ws, wj, make_prompts(wl), make_boundary(wl)
+
+
+def make_grpo_batch(n_groups: int, G: int, T: int, seed: int, noise: float = 0.15,
+                    senior_share: float = 0.5):
+    """Seeded synthetic inputs of the senior-only GRPO loss over n_groups
+    prompts x G rollouts with arenas of row stride T (the paper's batch is 16
+    prompts x G = 8 with responses of at most 3000 tokens).  The verifier and
+    the dataset are not available, so rewards are binary draws whose success
+    rate is itself drawn per group (uniform), which yields solved, unsolved and
+    mixed groups alike; group 0 is forced all-correct and group 1 (when there
+    is one) all-wrong.  Lengths are uniform in [0, T] with the first rollout at
+    0 and the second at T; authorship is Bernoulli(senior_share) per position;
+    the rollout-time log-probs are -Exponential(1); the current policy's
+    log-probs add N(0, noise) to them, so the ratios fall on both sides of
+    the clip band.  Returns (rewards f32 [S], owner u8 [S][T], length i32 [S],
+    logp_old f32 [S][T], logp_new f32 [S][T]), S = n_groups * G."""
+    rng = np.random.default_rng(seed)
+    S = n_groups * G
+    rate = rng.random(n_groups)
+    rate[0] = 1.0
+    if n_groups > 1:
+        rate[1] = 0.0
+    rewards = (rng.random(S) < np.repeat(rate, G)).astype(np.float32)
+    length = rng.integers(0, T + 1, size=S).astype(np.int32)
+    length[0] = 0
+    if S > 1:
+        length[1] = T
+    owner = (rng.random((S, T)) < senior_share).astype(np.uint8)
+    logp_old = (-rng.exponential(1.0, size=(S, T))).astype(np.float32)
+    logp_new = (logp_old + rng.normal(0.0, noise, size=(S, T))).astype(np.float32)
+    return rewards, owner, length, logp_old, logp_new
