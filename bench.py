@@ -195,6 +195,8 @@ def main():
                     help="skip the extra rollout that times every kernel class with the forwards serialized")
     ap.add_argument("--score", type=int, default=0, metavar="STEPS",
                     help="also time tandem_score_step after each of STEPS decode steps (reported as 'scoring')")
+    ap.add_argument("--grpo", type=int, default=0, metavar="REPS",
+                    help="also time tandem_grpo_loss REPS times over the last rollout's arenas (reported as 'grpo')")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -322,6 +324,55 @@ def main():
                    "frac_of_decode_step": round(ms / (sum(dec) / (L * args.steps)), 4)}
         log(f"[bench] scoring: {ms * 1e3:.1f} us per step ({scoring['achieved_gbs']:.0f} GB/s)")
 
+    grpo = None
+    if args.grpo > 0:
+        # the senior-only GRPO loss pieces over the last rollout's arenas (its
+        # authorship, log-prob and length arenas as tandem_step left them),
+        # seeded binary rewards and the recorded log-probs plus seeded offsets
+        # as the current policy's: HIP events on the stream the call runs on
+        from paper_2606_28166_amd.engine import grpo_loss
+        g = torch.Generator(device="cpu").manual_seed(41)
+        rewards = (torch.rand(n, generator=g) < 0.5).float().to(eng.dev)
+        lp_new = eng.logprob[:n] + (0.15 * torch.randn(eng.logprob[:n].shape, generator=g)).to(eng.dev)
+        ws = torch.empty(LIB.tandem_grpo_workspace_size(LIB.GrpoCfg(n // wl.group, wl.group, eng.max_new, 0.2)),
+                         dtype=torch.uint8, device=eng.dev)
+        args_g = (rewards, eng.owner[:n], eng.length[:n], eng.logprob[:n], lp_new, wl.group)
+        ref_g = grpo_loss(*args_g, workspace=ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.grpo):
+            grpo_loss(*args_g, workspace=ws)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_eager = e0.elapsed_time(e1) / args.grpo
+        # the three launches of one call captured in a HIP graph and replayed:
+        # device time without the host's per-call marshalling
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            cap_g = grpo_loss(*args_g, workspace=ws)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.grpo):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.grpo
+        same = all(torch.equal(ref_g[k], cap_g[k]) for k in ("advantages", "loss", "n_masked", "grad"))
+        lens = eng.length[:n].cpu().numpy().astype(np.int64)
+        # per position t < length: authorship byte + two log-probs read; every
+        # position of the [S][T] arena: gradient written; per rollout: reward,
+        # length, advantage
+        nbytes = int(9 * lens.sum() + 4 * n * eng.max_new + 12 * n)
+        grpo = {"calls": args.grpo, "us_per_call": round(ms * 1e3, 2), "timing": "HIP graph replays",
+                "us_per_call_eager": round(ms_eager * 1e3, 2), "replays_match_eager": same,
+                "rollouts": n, "stride": eng.max_new,
+                "positions": int(lens.sum()), "bytes_per_call": nbytes,
+                "achieved_gbs": round(nbytes / (ms / 1e3) / 1e9, 1),
+                "frac_of_8tbs": round(nbytes / (ms / 1e3) / 8e12, 4)}
+        log(f"[bench] grpo loss: {ms * 1e3:.1f} us per call replayed ({ms_eager * 1e3:.1f} us eager; "
+            f"{grpo['achieved_gbs']:.0f} GB/s over {grpo['positions']} positions; replays match: {same})")
+
     cpu = None
     if not args.no_cpu_baseline:
         eng_models = None
@@ -361,6 +412,8 @@ def main():
     }
     if scoring is not None:
         res["scoring"] = scoring
+    if grpo is not None:
+        res["grpo"] = grpo
     eng.close()
     print(json.dumps(res), flush=True)
 

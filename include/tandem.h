@@ -202,6 +202,46 @@ tandem_status tandem_step_forced(tandem_handle* h, const int32_t* forced, const 
  * TANDEM_E_ARG when scores is NULL. */
 tandem_status tandem_score_step(tandem_handle* h, float* scores);
 
+/* Senior-only GRPO loss pieces of a batch of tandem rollouts (Section 3.4, the
+ * L_TRL equation; Algorithm 1's update half; the hyperparameter table's
+ * group-relative, std-normalised advantage and clip ratio).  Handle-free:
+ * it reads the rollout arenas tandem_step wrote (or any arrays of that
+ * layout) and runs on the given stream (hipStream_t as void*, NULL = the null
+ * stream), asynchronously.  S = n_groups * group_size rollouts, s = j * G + i.
+ *   advantage  A_s = (r_s - mean_j) / (std_j + 1e-6), std_j the sample
+ *              standard deviation (divisor G - 1; 0 when G = 1) of group j's
+ *              rewards; every position of rollout s shares A_s.
+ *   mask       position t of rollout s is counted iff t < length[s] and
+ *              owner[s][t] != 0 (the senior emitted it); N = masked count.
+ *   loss       L = -(1/N) sum_masked min(rho A_s, clip(rho, 1 - eps, 1 + eps) A_s),
+ *              rho = exp(logp_new - logp_old); L = 0 when N = 0.
+ *   gradient   dL/dlogp_new[s][t] = -rho A_s / N where the unclipped term is
+ *              the minimum, 0 elsewhere (every unmasked position included).
+ * All pointers are caller-owned device memory:
+ *   rewards    float [S]; owner uint8 [S][T]; length int32 [S] (clamped to
+ *              [0, T]); logp_old float [S][T] (the rollout's senior log-probs,
+ *              pi_old); logp_new float [S][T] or NULL (= logp_old: rho = 1)
+ *   advantages float [S] out; grad float [S][T] out or NULL; loss float [1]
+ *              out; n_masked int32 [1] out
+ *   workspace  >= tandem_grpo_workspace_size bytes, 256-byte aligned; its
+ *              contents need no initialisation and are overwritten.
+ * T is the arenas' row stride (max_new_tokens).  TANDEM_E_ARG for a NULL
+ * required pointer, eps outside [0, 1) or a short workspace; TANDEM_E_SHAPE
+ * for sizes < 1 or S * T >= 2^24 (masked counts are summed exactly in fp32).
+ * Errors are reported through tandem_last_error(NULL). */
+typedef struct {
+  int32_t n_groups;                /* prompts j */
+  int32_t group_size;              /* G >= 1 */
+  int32_t max_new_tokens;          /* T, row stride of the [S][T] arrays */
+  float clip_eps;                  /* PPO clip ratio eps (0.2 in the paper) */
+} tandem_grpo_cfg;
+
+tandem_status tandem_grpo_workspace_size(const tandem_grpo_cfg* cfg, size_t* bytes);
+tandem_status tandem_grpo_loss(const tandem_grpo_cfg* cfg, const float* rewards, const uint8_t* owner,
+                               const int32_t* length, const float* logp_old, const float* logp_new,
+                               float* advantages, float* grad, float* loss, int32_t* n_masked,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
 /* Copy the per-sequence sampler state to HOST int32 arrays of n_seqs
  * entries (any pointer may be NULL): owner (1 = senior), span counter c,
  * next step t, next position, done flag.  Synchronises the stream. */

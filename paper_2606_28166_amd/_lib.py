@@ -54,9 +54,15 @@ class Debug(C.Structure):
                 ("logits_junior", C.c_void_p)]
 
 
+class GrpoCfg(C.Structure):
+    _fields_ = [("n_groups", C.c_int32), ("group_size", C.c_int32), ("max_new_tokens", C.c_int32),
+                ("clip_eps", C.c_float)]
+
+
 EXPORTS = ("tandem_workspace_size", "tandem_init", "tandem_prefill", "tandem_step",
            "tandem_step_forced", "tandem_score_step", "tandem_get_state", "tandem_timing_enable", "tandem_timing_read",
-           "tandem_last_error", "tandem_status_string", "tandem_destroy")
+           "tandem_last_error", "tandem_status_string", "tandem_destroy", "tandem_grpo_workspace_size",
+           "tandem_grpo_loss")
 K_ATTENTION, K_GEMM, K_SAMPLE, K_OTHER = 0, 1, 2, 3
 TIMING_SERIAL = 1 << 8          # timing flag: run the two forwards one after the other
 TIMING_EAGER = 1 << 9           # timing flag: launch every kernel from the host (no step graph)
@@ -98,6 +104,10 @@ def _load():
     lib.tandem_status_string.restype = C.c_char_p
     lib.tandem_destroy.argtypes = [P]
     lib.tandem_destroy.restype = None
+    lib.tandem_grpo_workspace_size.argtypes = [C.POINTER(GrpoCfg), C.POINTER(C.c_size_t)]
+    lib.tandem_grpo_workspace_size.restype = st
+    lib.tandem_grpo_loss.argtypes = [C.POINTER(GrpoCfg), P, P, P, P, P, P, P, P, P, P, C.c_size_t, P]
+    lib.tandem_grpo_loss.restype = st
     return lib
 
 
@@ -171,3 +181,16 @@ def tandem_timing_read(h, kernel_class: int):
 
 def tandem_destroy(h) -> None:
     lib.tandem_destroy(h)
+
+
+def tandem_grpo_workspace_size(cfg: GrpoCfg) -> int:
+    n = C.c_size_t()
+    check(lib.tandem_grpo_workspace_size(C.byref(cfg), C.byref(n)))
+    return n.value
+
+
+def tandem_grpo_loss(cfg: GrpoCfg, rewards: int, owner: int, length: int, logp_old: int, logp_new,
+                     advantages: int, grad, loss: int, n_masked: int, workspace: int, workspace_bytes: int,
+                     stream: int) -> None:
+    check(lib.tandem_grpo_loss(C.byref(cfg), rewards, owner, length, logp_old, logp_new, advantages, grad,
+                               loss, n_masked, workspace, workspace_bytes, stream))

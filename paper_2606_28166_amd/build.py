@@ -20,7 +20,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtandem.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["tandem.cpp", "k_gemm.hip", "k_stream.hip", "k_attn.hip", "k_misc.hip"]
+SOURCES = ["tandem.cpp", "k_gemm.hip", "k_stream.hip", "k_attn.hip", "k_misc.hip", "k_grpo.hip"]
 
 
 def hip_runtime_dir() -> str:

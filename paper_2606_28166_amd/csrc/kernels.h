@@ -195,6 +195,20 @@ struct ScoreArgs {
 };
 hipError_t launch_score(const ScoreArgs& a, hipStream_t st);
 
+// Senior-only GRPO loss pieces over S = n_groups * G rollouts with arenas of
+// row stride T: advantages adv[S], masked counts cnt[S] (scratch), per-(row,
+// chunk) partial sums part[S][n_chunks] (scratch, n_chunks = ceil(T /
+// kGrpoChunk)), gradient grad[S][T] (may be NULL), loss[1], n_masked[1].
+// logp_new NULL means logp_new = logp_old.
+constexpr int kGrpoChunk = 1024;
+struct GrpoArgs {
+  int S, G, T, n_chunks; float eps;
+  const float* rewards; const uint8_t* owner; const int32_t* length;
+  const float* logp_old; const float* logp_new;
+  float* adv; int32_t* cnt; float* part; float* grad; float* loss; int32_t* n_masked;
+};
+hipError_t launch_grpo(const GrpoArgs& a, hipStream_t st);
+
 // Copy positions [p0, n_pos) of slot src into slots dst0 .. dst0 + n_dst - 1
 // for every layer and kv head (K and transposed V); p0 % 16 == 0.
 hipError_t launch_kv_replicate(int dt, void* kc, void* vc, int n_layers, long layer_stride,

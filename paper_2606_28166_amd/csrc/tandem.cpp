@@ -783,6 +783,25 @@ tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_de
 
 }  // namespace
 
+namespace {
+tandem_status grpo_check(const tandem_grpo_cfg* c, size_t* bytes, GrpoArgs* a) {
+  if (!c) return fail(nullptr, TANDEM_E_ARG, "tandem_grpo: cfg is NULL");
+  if (c->n_groups < 1 || c->group_size < 1 || c->max_new_tokens < 1)
+    return fail(nullptr, TANDEM_E_SHAPE, "tandem_grpo: n_groups, group_size and max_new_tokens must be >= 1");
+  const long long S = (long long)c->n_groups * c->group_size;
+  if (S * c->max_new_tokens >= (1LL << 24))
+    return fail(nullptr, TANDEM_E_SHAPE, "tandem_grpo: S * max_new_tokens must be below 2^24");
+  if (!(c->clip_eps >= 0.f && c->clip_eps < 1.f))
+    return fail(nullptr, TANDEM_E_ARG, "tandem_grpo: clip_eps must lie in [0, 1)");
+  a->S = (int)S; a->G = c->group_size; a->T = c->max_new_tokens; a->eps = c->clip_eps;
+  a->n_chunks = (a->T + kGrpoChunk - 1) / kGrpoChunk;
+  // counts [S] int32, then partial sums [S][n_chunks] float, each 256-aligned
+  const size_t cnt_b = ((size_t)S * 4 + 255) / 256 * 256;
+  *bytes = cnt_b + ((size_t)S * a->n_chunks * 4 + 255) / 256 * 256;
+  return TANDEM_OK;
+}
+}  // namespace
+
 extern "C" {
 
 const char* tandem_status_string(tandem_status s) {
@@ -1242,4 +1261,34 @@ void tandem_destroy(tandem_handle* h) {
   delete h;
 }
 
+
+tandem_status tandem_grpo_workspace_size(const tandem_grpo_cfg* cfg, size_t* bytes) {
+  if (!bytes) return fail(nullptr, TANDEM_E_ARG, "tandem_grpo_workspace_size: bytes is NULL");
+  GrpoArgs a{};
+  return grpo_check(cfg, bytes, &a);
+}
+
+tandem_status tandem_grpo_loss(const tandem_grpo_cfg* cfg, const float* rewards, const uint8_t* owner,
+                               const int32_t* length, const float* logp_old, const float* logp_new,
+                               float* advantages, float* grad, float* loss, int32_t* n_masked,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  GrpoArgs a{};
+  size_t need = 0;
+  const tandem_status st = grpo_check(cfg, &need, &a);
+  if (st != TANDEM_OK) return st;
+  if (!rewards || !owner || !length || !logp_old || !advantages || !loss || !n_masked || !workspace)
+    return fail(nullptr, TANDEM_E_ARG, "tandem_grpo_loss: a required pointer is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+    return fail(nullptr, TANDEM_E_ARG, "tandem_grpo_loss: workspace must be 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(nullptr, TANDEM_E_ARG, "tandem_grpo_loss: workspace is smaller than tandem_grpo_workspace_size");
+  a.rewards = rewards; a.owner = owner; a.length = length; a.logp_old = logp_old; a.logp_new = logp_new;
+  a.adv = advantages; a.grad = grad; a.loss = loss; a.n_masked = n_masked;
+  a.cnt = static_cast<int32_t*>(workspace);
+  a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + ((size_t)a.S * 4 + 255) / 256 * 256);
+  const hipError_t e = launch_grpo(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess)
+    return fail(nullptr, TANDEM_E_HIP, std::string("tandem_grpo_loss: ") + hipGetErrorString(e));
+  return TANDEM_OK;
+}
 }  // extern "C"

@@ -115,3 +115,26 @@ def test_null_handle_calls():
     assert L.lib.tandem_get_state(None, None, None, None, None, None) == L.E_ARG
     L.lib.tandem_destroy(None)
     assert L.lib.tandem_status_string(L.E_CAPACITY) == b"TANDEM_E_CAPACITY"
+
+
+def test_grpo_workspace_size_and_argument_checks():
+    cfg = L.GrpoCfg(16, 8, 3000, 0.2)
+    # counts [128] int32 and partials [128][ceil(3000 / 1024)] float, each 256-aligned
+    assert L.tandem_grpo_workspace_size(cfg) == 512 + 1536
+    for bad, code in ((L.GrpoCfg(0, 8, 3000, 0.2), L.E_SHAPE), (L.GrpoCfg(16, 0, 3000, 0.2), L.E_SHAPE),
+                      (L.GrpoCfg(16, 8, 0, 0.2), L.E_SHAPE), (L.GrpoCfg(1024, 8, 3000, 0.2), L.E_SHAPE),
+                      (L.GrpoCfg(16, 8, 3000, 1.0), L.E_ARG), (L.GrpoCfg(16, 8, 3000, -0.1), L.E_ARG)):
+        n = C.c_size_t()
+        assert L.lib.tandem_grpo_workspace_size(C.byref(bad), C.byref(n)) == code
+        assert L.lib.tandem_last_error(None)
+    assert L.lib.tandem_grpo_workspace_size(C.byref(cfg), None) == L.E_ARG
+    # every check fires before any HIP call: fake, never dereferenced addresses
+    fake = 1 << 20
+    ws = L.tandem_grpo_workspace_size(cfg)
+    call = L.lib.tandem_grpo_loss
+    assert call(None, fake, fake, fake, fake, None, fake, None, fake, fake, fake, ws, None) == L.E_ARG
+    assert call(C.byref(cfg), None, fake, fake, fake, None, fake, None, fake, fake, fake, ws, None) == L.E_ARG
+    assert call(C.byref(cfg), fake, fake, fake, fake, None, fake, None, None, fake, fake, ws, None) == L.E_ARG
+    assert call(C.byref(cfg), fake, fake, fake, fake, None, fake, None, fake, fake, fake, ws - 1, None) == L.E_ARG
+    assert call(C.byref(cfg), fake, fake, fake, fake, None, fake, None, fake, fake, fake + 16, ws, None) == L.E_ARG
+    assert b"aligned" in L.lib.tandem_last_error(None)
