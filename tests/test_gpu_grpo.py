@@ -82,6 +82,22 @@ def test_grpo_ratio_one_no_gradient_and_empty_mask():
     assert np.all(got["grad"] == 0.0)
 
 
+def test_grpo_zero_clip_band_and_out_of_range_lengths():
+    """eps = 0 (the band collapses to ratio 1: a term keeps its gradient only
+    on the side the sign of A allows) and lengths outside [0, T] (clamped:
+    a negative length masks nothing, one beyond T masks the whole row)."""
+    global EPS
+    P.log("case grpo loss: eps 0, lengths -5 and T + 100")
+    r, o, l, lo, ln = W.make_grpo_batch(4, 4, 700, seed=7)
+    l[2], l[3] = -5, 800
+    saved, EPS = EPS, 0.0
+    try:
+        _check(_gpu(r, o, l, lo, ln, 4), r, o, l, lo, ln, 4)
+    finally:
+        EPS = saved
+    _check(_gpu(r, o, l, lo, ln, 4), r, o, l, lo, ln, 4)
+
+
 def test_grpo_workspace_reused_across_batches():
     """One workspace serves a large batch and then a smaller one: the counts
     and partial sums left by the first call do not leak into the second."""
