@@ -57,32 +57,29 @@ __device__ __forceinline__ void split4(const float* x, s16x4_t& hi, s16x4_t& lo)
 // One 16-position chunk of a kv head's keys and values in MFMA operand
 // layout (the cache's tiled order): k[dc] = K[pos c16][32dc + 8g .. +7];
 // v[j] = V[pos 4g .. +3][32j + c16] then V[pos 4g .. +3][32j + 16 + c16].
+// Half a 16-position chunk: its K or its V tile (16 positions x HD, bf16)
+// in the lane order the MFMAs consume, 16 bytes per lane per 32 dims.
 template <int HD>
-struct KV16 {
-  u32x4_t k[HD / 32];
-  u32x4_t v[HD / 32];
+struct Half {
+  u32x4_t r[HD / 32];
 };
 
 template <int HD>
-__device__ __forceinline__ void load_chunk(KV16<HD>& c, __amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int chunk,
-                                           int lane) {
+__device__ __forceinline__ void load_half(Half<HD>& h, __amdgpu_buffer_rsrc_t rs, int chunk, int lane) {
   const int base = chunk * 32 * HD + lane * 16;   // bytes: 16 positions x HD x 2
 #pragma unroll
-  for (int j = 0; j < HD / 32; ++j) c.k[j] = buf_load16_nt(kr, base + j * 1024, 0);
-#pragma unroll
-  for (int j = 0; j < HD / 32; ++j) c.v[j] = buf_load16_nt(vr, base + j * 1024, 0);
+  for (int j = 0; j < HD / 32; ++j) h.r[j] = buf_load16_nt(rs, base + j * 1024, 0);
 }
 
-// Orders the loads issued so far before everything that reads chunk c: the
-// empty asm "modifies" every register of c and clobbers memory, so earlier
-// loads cannot sink below it, the arithmetic on c cannot rise above it, and
-// the only wait the compiler places here is for c's own loads.
+// Orders the loads issued so far before everything that follows and ties h
+// to this point: the empty asm "modifies" every register of h and clobbers
+// memory, so earlier loads cannot sink below it, later loads cannot rise
+// above it, arithmetic on h cannot cross it, and the only wait the compiler
+// places here is for h's own loads.
 template <int HD>
-__device__ __forceinline__ void pin_chunk(KV16<HD>& c) {
+__device__ __forceinline__ void pin_half(Half<HD>& h) {
 #pragma unroll
-  for (int j = 0; j < HD / 32; ++j) asm volatile("" : "+v"(c.k[j]) : : "memory");
-#pragma unroll
-  for (int j = 0; j < HD / 32; ++j) asm volatile("" : "+v"(c.v[j]) : : "memory");
+  for (int j = 0; j < HD / 32; ++j) asm volatile("" : "+v"(h.r[j]) : : "memory");
 }
 
 template <int HD>
@@ -95,14 +92,18 @@ struct AttnState {
 // >= ctx_max hold stale cache contents.  GUARD: a column may see a chunk with
 // no position it attends before any it does (several query rows per
 // workgroup); its running max then stays -inf and nothing is added.
+// First half of a chunk: scores of its 16 positions from the K tile, the
+// online-softmax update and the rescaling of the accumulator; returns the
+// probabilities as split bf16 operands of the value product.
 template <int HD, bool GUARD>
-__device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, const bf16x8_t* qh, const bf16x8_t* ql,
-                                             int p0, int ctx, int ctx_max, float scale, int g) {
+__device__ __forceinline__ void attend_scores(AttnState<HD>& st, const Half<HD>& k, const bf16x8_t* qh,
+                                              const bf16x8_t* ql, int p0, int ctx, float scale, int g, s16x4_t& ph,
+                                              s16x4_t& pl) {
   constexpr int DC = HD / 32, DB = HD / 16;
   f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int dc = 0; dc < DC; ++dc) {
-    const bf16x8_t kk = __builtin_bit_cast(bf16x8_t, c.k[dc]);
+    const bf16x8_t kk = __builtin_bit_cast(bf16x8_t, k.r[dc]);
     acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qh[dc], acc0, 0, 0, 0);
     acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, ql[dc], acc1, 0, 0, 0);
   }
@@ -122,7 +123,6 @@ __device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, con
   for (int i = 0; i < 4; ++i) pr[i] = none ? 0.f : exp2f(s[i] - m_new);
   st.l_run = st.l_run * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
   st.m_run = m_new;
-  s16x4_t ph, pl;
   split4(pr, ph, pl);
   // rescale the accumulator rows (heads 4g + i) only when some head's max moved
   if (__ballot(alpha != 1.f)) {
@@ -134,6 +134,14 @@ __device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, con
 #pragma unroll
       for (int i = 0; i < 4; ++i) st.o[db][i] *= ai[i];
   }
+}
+
+// Second half of a chunk: the probabilities times its V tile.
+template <int HD>
+__device__ __forceinline__ void attend_values(AttnState<HD>& st, Half<HD>& v, s16x4_t ph, s16x4_t pl, int p0,
+                                              int ctx_max, int g) {
+  constexpr int DC = HD / 32, DB = HD / 16;
+  const int pg = p0 + 4 * g;
   // positions at or past the context hold stale cache contents: zero them so
   // that 0 * (stale) cannot produce NaN
   if (p0 + 16 > ctx_max) {
@@ -142,19 +150,19 @@ __device__ __forceinline__ void attend_chunk(AttnState<HD>& st, KV16<HD>& c, con
     const uint64_t keep = nv == 4 ? ~0ull : (1ull << (16 * nv)) - 1ull;
     const uint32_t klo = (uint32_t)keep, khi = (uint32_t)(keep >> 32);
 #pragma unroll
-    for (int j = 0; j < DC; ++j) c.v[j] &= u32x4_t{klo, khi, klo, khi};
+    for (int j = 0; j < DC; ++j) v.r[j] &= u32x4_t{klo, khi, klo, khi};
   }
   // hi parts over all dim blocks, then lo parts (independent consecutive MFMAs)
 #pragma unroll
   for (int db = 0; db < DB; ++db) {
-    const u32x4_t v = c.v[db >> 1];
-    const s16x4_t vv = __builtin_bit_cast(s16x4_t, (db & 1) ? make_uint2(v.z, v.w) : make_uint2(v.x, v.y));
+    const u32x4_t w = v.r[db >> 1];
+    const s16x4_t vv = __builtin_bit_cast(s16x4_t, (db & 1) ? make_uint2(w.z, w.w) : make_uint2(w.x, w.y));
     st.o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ph, vv, st.o[db], 0, 0, 0);
   }
 #pragma unroll
   for (int db = 0; db < DB; ++db) {
-    const u32x4_t v = c.v[db >> 1];
-    const s16x4_t vv = __builtin_bit_cast(s16x4_t, (db & 1) ? make_uint2(v.z, v.w) : make_uint2(v.x, v.y));
+    const u32x4_t w = v.r[db >> 1];
+    const s16x4_t vv = __builtin_bit_cast(s16x4_t, (db & 1) ? make_uint2(w.z, w.w) : make_uint2(w.x, w.y));
     st.o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pl, vv, st.o[db], 0, 0, 0);
   }
 }
@@ -177,7 +185,8 @@ __device__ __forceinline__ void attend_block(const float* __restrict__ q, const 
   constexpr int DC = HD / 32;     // k-steps of the S product
   constexpr int DB = HD / 16;     // 16-dim blocks of the O product
   static_assert(NCOL <= 16, "16 query columns per workgroup");
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: the chunk branches stay scalar
   const int g = lane >> 4, c16 = lane & 15;
   const int ri = c16 / GQA, hq = c16 % GQA;           // this lane's query column
   const bool valid = c16 < NCOL && ri < nr;
@@ -193,8 +202,23 @@ __device__ __forceinline__ void attend_block(const float* __restrict__ q, const 
   const int nchunk = ((ctx_max + 15) >> 4) - c0;
   const int nmine = nchunk > wave ? (nchunk - wave + 3) >> 2 : 0;
   auto chunk_at = [&](int i) { return c0 + wave + 4 * min(i, nmine - 1); };
-  KV16<HD> ca, cb;
-  if (nmine > 0) load_chunk<HD>(ca, kr, vr, chunk_at(0), lane);
+  // Five half-chunk slots: the K and V tiles of the wave's chunks enter them
+  // in stream order (K of chunk i is half 2i, its V half 2i + 1, half h goes
+  // to slot h % 5), so while a chunk is consumed the next one and a half to
+  // two chunks are in flight.  A slot is refilled as soon as its tile is
+  // consumed; the slot pattern repeats every five chunks.  Loads are issued
+  // without branches: a chunk past the wave's last one is read at an offset
+  // beyond the buffer's size, which the buffer range check turns into zeros
+  // without a memory access (branches around the loads would make the
+  // compiler wait for every load in flight at each join).
+  const int past = ctx_stride / 16 + 1;            // a chunk index outside the plane
+  auto src = [&](int j) { return j < nmine ? chunk_at(j) : past; };
+  Half<HD> h0, h1, h2, h3, h4;
+  load_half<HD>(h0, kr, src(0), lane);
+  load_half<HD>(h1, vr, src(0), lane);
+  load_half<HD>(h2, kr, src(1), lane);
+  load_half<HD>(h3, vr, src(1), lane);
+  load_half<HD>(h4, kr, src(2), lane);
 
   // Q^T operand: column c16, k = dims 32dc + 8g .. +7 (zero for unused columns)
   bf16x8_t qh[DC], ql[DC];
@@ -217,20 +241,39 @@ __device__ __forceinline__ void attend_block(const float* __restrict__ q, const 
 #pragma unroll
   for (int db = 0; db < DB; ++db) st.o[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // Two register buffers: the next chunk of this wave is in flight while the
-  // current one is consumed.  The loop walks the wave's chunks in pairs and
-  // loads only chunks that exist (uniform branches: a re-read of a streamed
-  // chunk would come from HBM again).  pin_chunk keeps the next chunk's loads
-  // ahead of the current chunk's arithmetic (left alone, the compiler sinks
-  // the loads to their first use and the prefetch disappears).
-  for (int i = 0; i < nmine; i += 2) {
-    if (i + 1 < nmine) load_chunk<HD>(cb, kr, vr, chunk_at(i + 1), lane);
-    pin_chunk<HD>(ca);
-    attend_chunk<HD, GUARD>(st, ca, qh, ql, 16 * chunk_at(i), ctx, ctx_max, scale, g);
-    if (i + 2 < nmine) load_chunk<HD>(ca, kr, vr, chunk_at(i + 2), lane);
+  // Chunk j of the wave with its K tile in slot ks and its V tile in vs.
+  // The pins keep each refill behind the arithmetic that frees its slot and
+  // every wait down to the one tile about to be read (left alone, the
+  // compiler sinks loads to their first use and the prefetch disappears).
+  auto step = [&](int j, Half<HD>& ks, Half<HD>& vs) {
+    const int p0 = 16 * chunk_at(j);
+    s16x4_t ph, pl;
+    pin_half<HD>(ks);
+    attend_scores<HD, GUARD>(st, ks, qh, ql, p0, ctx, scale, g, ph, pl);
+    pin_half<HD>(ks);
+    load_half<HD>(ks, vr, src(j + 2), lane);
+    pin_half<HD>(vs);
+    attend_values<HD>(st, vs, ph, pl, p0, ctx_max, g);
+    pin_half<HD>(vs);
+    load_half<HD>(vs, kr, src(j + 3), lane);
+  };
+  // whole groups of five chunks as straight-line code, then the last < 5
+  int i = 0;
+  for (; i + 5 <= nmine; i += 5) {
+    step(i, h0, h1);
+    step(i + 1, h2, h3);
+    step(i + 2, h4, h0);
+    step(i + 3, h1, h2);
+    step(i + 4, h3, h4);
+  }
+  if (i < nmine) {
+    step(i, h0, h1);
     if (i + 1 < nmine) {
-      pin_chunk<HD>(cb);
-      attend_chunk<HD, GUARD>(st, cb, qh, ql, 16 * chunk_at(i + 1), ctx, ctx_max, scale, g);
+      step(i + 1, h2, h3);
+      if (i + 2 < nmine) {
+        step(i + 2, h4, h0);
+        if (i + 3 < nmine) step(i + 3, h1, h2);
+      }
     }
   }
 
@@ -279,7 +322,7 @@ __device__ __forceinline__ void waves_merged(const float (*sm_m)[16], const floa
 // once per row.  Row groups of at most 16 rows are split over sub_per_grp
 // workgroups of ROWS rows.
 template <int HD, int GQA, int ROWS>
-__global__ __launch_bounds__(256) void attn_mfma_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_mfma_kernel(
     const float* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     int ctx_stride, long slot_stride, const int32_t* __restrict__ row_slot,
     const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
@@ -353,7 +396,7 @@ __device__ __forceinline__ float merge_partials(float mp, float lp, float np, fl
 // next launch.  No workgroup waits for another.  Done rows take no part
 // (zero output).
 template <int HD, int GQA>
-__global__ __launch_bounds__(256) void attn_shared_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_shared_kernel(
     const float* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     int ctx_stride, long slot_stride, const int32_t* __restrict__ row_slot,
     const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
