@@ -197,42 +197,48 @@ __device__ __forceinline__ void attend_block(const float* __restrict__ q, const 
   const __amdgpu_buffer_rsrc_t vr = buf_rsrc(vc + plane, (uint32_t)ctx_stride * HD * 2);
   const float scale = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
 
-  // Wave w owns chunks c0 + w, c0 + w + 4, ... of the stream; its first
-  // chunk is requested before the query is read.
+  // Wave w owns chunks c0 + w, c0 + w + 4, ... of the stream.  The query is
+  // requested first and its first three chunks right after, behind a
+  // compiler barrier, so that waiting for the query (the wait counter is in
+  // issue order) leaves the chunks in flight.
+  const float* qp = q + ((size_t)rr * nq + kh * GQA + (valid ? hq : 0)) * HD + 8 * g;
+  float4 qa[DC], qb[DC];
+#pragma unroll
+  for (int dc = 0; dc < DC; ++dc) {
+    qa[dc] = *reinterpret_cast<const float4*>(qp + 32 * dc);
+    qb[dc] = *reinterpret_cast<const float4*>(qp + 32 * dc + 4);
+  }
+  asm volatile("" : : : "memory");
   const int nchunk = ((ctx_max + 15) >> 4) - c0;
   const int nmine = nchunk > wave ? (nchunk - wave + 3) >> 2 : 0;
   auto chunk_at = [&](int i) { return c0 + wave + 4 * min(i, nmine - 1); };
-  // Five half-chunk slots: the K and V tiles of the wave's chunks enter them
-  // in stream order (K of chunk i is half 2i, its V half 2i + 1, half h goes
-  // to slot h % 5), so while a chunk is consumed the next one and a half to
-  // two chunks are in flight.  A slot is refilled as soon as its tile is
-  // consumed; the slot pattern repeats every five chunks.  Loads are issued
+  // Six half-chunk slots, three chunks: the K and V tiles of chunk i live in
+  // slots 2 (i % 3) and 2 (i % 3) + 1, and each is refilled with the same
+  // tile of chunk i + 3 as soon as it is consumed, so while a chunk is
+  // consumed the next two to two and a half chunks are in flight.  Loads are issued
   // without branches: a chunk past the wave's last one is read at an offset
   // beyond the buffer's size, which the buffer range check turns into zeros
   // without a memory access (branches around the loads would make the
   // compiler wait for every load in flight at each join).
   const int past = ctx_stride / 16 + 1;            // a chunk index outside the plane
   auto src = [&](int j) { return j < nmine ? chunk_at(j) : past; };
-  Half<HD> h0, h1, h2, h3, h4;
+  Half<HD> h0, h1, h2, h3, h4, h5;
   load_half<HD>(h0, kr, src(0), lane);
   load_half<HD>(h1, vr, src(0), lane);
   load_half<HD>(h2, kr, src(1), lane);
   load_half<HD>(h3, vr, src(1), lane);
   load_half<HD>(h4, kr, src(2), lane);
+  load_half<HD>(h5, vr, src(2), lane);
 
   // Q^T operand: column c16, k = dims 32dc + 8g .. +7 (zero for unused columns)
   bf16x8_t qh[DC], ql[DC];
-  {
-    const float* qp = q + ((size_t)rr * nq + kh * GQA + (valid ? hq : 0)) * HD + 8 * g;
 #pragma unroll
-    for (int dc = 0; dc < DC; ++dc) {
-      const float4 a = *reinterpret_cast<const float4*>(qp + 32 * dc);
-      const float4 b = *reinterpret_cast<const float4*>(qp + 32 * dc + 4);
-      float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  for (int dc = 0; dc < DC; ++dc) {
+    const float4 a = qa[dc], b = qb[dc];
+    float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = valid ? x[e] : 0.f;
-      split8(x, qh[dc], ql[dc]);
-    }
+    for (int e = 0; e < 8; ++e) x[e] = valid ? x[e] : 0.f;
+    split8(x, qh[dc], ql[dc]);
   }
 
   AttnState<HD> st;
@@ -251,30 +257,22 @@ __device__ __forceinline__ void attend_block(const float* __restrict__ q, const 
     pin_half<HD>(ks);
     attend_scores<HD, GUARD>(st, ks, qh, ql, p0, ctx, scale, g, ph, pl);
     pin_half<HD>(ks);
-    load_half<HD>(ks, vr, src(j + 2), lane);
+    load_half<HD>(ks, kr, src(j + 3), lane);
     pin_half<HD>(vs);
     attend_values<HD>(st, vs, ph, pl, p0, ctx_max, g);
     pin_half<HD>(vs);
-    load_half<HD>(vs, kr, src(j + 3), lane);
+    load_half<HD>(vs, vr, src(j + 3), lane);
   };
-  // whole groups of five chunks as straight-line code, then the last < 5
+  // whole groups of three chunks as straight-line code, then the last < 3
   int i = 0;
-  for (; i + 5 <= nmine; i += 5) {
+  for (; i + 3 <= nmine; i += 3) {
     step(i, h0, h1);
     step(i + 1, h2, h3);
-    step(i + 2, h4, h0);
-    step(i + 3, h1, h2);
-    step(i + 4, h3, h4);
+    step(i + 2, h4, h5);
   }
   if (i < nmine) {
     step(i, h0, h1);
-    if (i + 1 < nmine) {
-      step(i + 1, h2, h3);
-      if (i + 2 < nmine) {
-        step(i + 2, h4, h0);
-        if (i + 3 < nmine) step(i + 3, h1, h2);
-      }
-    }
+    if (i + 1 < nmine) step(i + 1, h2, h3);
   }
 
   float l_run = st.l_run;
