@@ -224,7 +224,8 @@ tandem_status tandem_score_step(tandem_handle* h, float* scores);
  *   advantages float [S] out; grad float [S][T] out or NULL; loss float [1]
  *              out; n_masked int32 [1] out
  *   workspace  >= tandem_grpo_workspace_size bytes, 256-byte aligned; its
- *              contents need no initialisation and are overwritten.
+ *              contents need no initialisation and are overwritten; calls
+ *              that may overlap (other streams) must not share one.
  * T is the arenas' row stride (max_new_tokens).  TANDEM_E_ARG for a NULL
  * required pointer, eps outside [0, 1) or a short workspace; TANDEM_E_SHAPE
  * for sizes < 1 or S * T >= 2^24 (masked counts are summed exactly in fp32).

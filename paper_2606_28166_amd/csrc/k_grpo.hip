@@ -11,10 +11,12 @@
 // and 0 elsewhere (junior positions, positions past the length, clipped
 // terms).
 //
-// Three launches, all HBM-streaming over the [S][T] arenas: per-rollout
-// advantage and masked count; per-(chunk, rollout) terms, gradient and a
-// partial sum; a one-workgroup finish in double that sums the partials in a
-// fixed order, so the loss is deterministic.
+// Two launches, HBM-streaming over the [S][T] arenas: per-rollout advantage
+// and masked count; per-(chunk, rollout) terms, gradient and a partial sum.
+// The workgroup that counts itself last on a ticket sums the partials in
+// double in a fixed order (index order, whoever is last), so the loss is
+// deterministic.  Partials are exchanged through agent-scope stores and
+// loads, which are coherent across the chips' separate L2 caches.
 #include "common.h"
 #include "kernels.h"
 
@@ -22,6 +24,13 @@ namespace tandem {
 namespace {
 
 constexpr int kGrpoNT = 256;
+
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 __global__ __launch_bounds__(kGrpoNT) void grpo_adv_kernel(GrpoArgs a) {
   __shared__ float red[kGrpoNT / kWave];
@@ -45,6 +54,7 @@ __global__ __launch_bounds__(kGrpoNT) void grpo_adv_kernel(GrpoArgs a) {
   if (tid == 0) {
     a.adv[s] = (a.rewards[s] - mean) / (sd + 1e-6f);
     a.cnt[s] = (int32_t)c;
+    if (s == 0) __hip_atomic_store(a.ticket, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -77,19 +87,19 @@ __global__ __launch_bounds__(kGrpoNT) void grpo_loss_kernel(GrpoArgs a) {
     if (a.grad) a.grad[row + t] = g;
   }
   acc = block_sum<kGrpoNT>(acc, red);
-  if (tid == 0) a.part[(size_t)s * a.n_chunks + chunk] = acc;
-}
-
-__global__ __launch_bounds__(kGrpoNT) void grpo_finish_kernel(GrpoArgs a) {
-  __shared__ double dred[kGrpoNT];
-  __shared__ float red[kGrpoNT / kWave];
-  const int tid = threadIdx.x;
   const int np = a.S * a.n_chunks;
+  __shared__ int last;
+  if (tid == 0) {
+    st_dev(a.part + (size_t)s * a.n_chunks + chunk, acc);
+    __builtin_amdgcn_s_waitcnt(0);           // the partial is stored before it is counted
+    last = __hip_atomic_fetch_add(a.ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == np - 1;
+  }
+  __syncthreads();
+  if (!last) return;
+  // the last workgroup: every partial has been stored
+  __shared__ double dred[kGrpoNT];
   double sum = 0.0;
-  for (int i = tid; i < np; i += kGrpoNT) sum += (double)a.part[i];
-  float n = 0.f;
-  for (int i = tid; i < a.S; i += kGrpoNT) n += (float)a.cnt[i];
-  n = block_sum<kGrpoNT>(n, red);
+  for (int i = tid; i < np; i += kGrpoNT) sum += (double)ld_dev(a.part + i);
   dred[tid] = sum;
   __syncthreads();
   for (int w = kGrpoNT / 2; w > 0; w >>= 1) {
@@ -99,6 +109,7 @@ __global__ __launch_bounds__(kGrpoNT) void grpo_finish_kernel(GrpoArgs a) {
   if (tid == 0) {
     a.loss[0] = n > 0.f ? (float)(-dred[0] / (double)n) : 0.f;
     a.n_masked[0] = (int32_t)n;
+    __hip_atomic_store(a.ticket, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -109,9 +120,6 @@ hipError_t launch_grpo(const GrpoArgs& a, hipStream_t st) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   grpo_loss_kernel<<<dim3(a.n_chunks, a.S), kGrpoNT, 0, st>>>(a);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  grpo_finish_kernel<<<1, kGrpoNT, 0, st>>>(a);
   return hipGetLastError();
 }
 

@@ -198,14 +198,15 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t st);
 // Senior-only GRPO loss pieces over S = n_groups * G rollouts with arenas of
 // row stride T: advantages adv[S], masked counts cnt[S] (scratch), per-(row,
 // chunk) partial sums part[S][n_chunks] (scratch, n_chunks = ceil(T /
-// kGrpoChunk)), gradient grad[S][T] (may be NULL), loss[1], n_masked[1].
+// kGrpoChunk)), a completion ticket (scratch, zeroed by the first launch),
+// gradient grad[S][T] (may be NULL), loss[1], n_masked[1].
 // logp_new NULL means logp_new = logp_old.
 constexpr int kGrpoChunk = 1024;
 struct GrpoArgs {
   int S, G, T, n_chunks; float eps;
   const float* rewards; const uint8_t* owner; const int32_t* length;
   const float* logp_old; const float* logp_new;
-  float* adv; int32_t* cnt; float* part; float* grad; float* loss; int32_t* n_masked;
+  float* adv; int32_t* cnt; float* part; int32_t* ticket; float* grad; float* loss; int32_t* n_masked;
 };
 hipError_t launch_grpo(const GrpoArgs& a, hipStream_t st);
 

@@ -795,9 +795,9 @@ tandem_status grpo_check(const tandem_grpo_cfg* c, size_t* bytes, GrpoArgs* a) {
     return fail(nullptr, TANDEM_E_ARG, "tandem_grpo: clip_eps must lie in [0, 1)");
   a->S = (int)S; a->G = c->group_size; a->T = c->max_new_tokens; a->eps = c->clip_eps;
   a->n_chunks = (a->T + kGrpoChunk - 1) / kGrpoChunk;
-  // counts [S] int32, then partial sums [S][n_chunks] float, each 256-aligned
+  // counts [S] int32, partial sums [S][n_chunks] float, a ticket int32, each 256-aligned
   const size_t cnt_b = ((size_t)S * 4 + 255) / 256 * 256;
-  *bytes = cnt_b + ((size_t)S * a->n_chunks * 4 + 255) / 256 * 256;
+  *bytes = cnt_b + ((size_t)S * a->n_chunks * 4 + 255) / 256 * 256 + 256;
   return TANDEM_OK;
 }
 }  // namespace
@@ -1286,6 +1286,7 @@ tandem_status tandem_grpo_loss(const tandem_grpo_cfg* cfg, const float* rewards,
   a.adv = advantages; a.grad = grad; a.loss = loss; a.n_masked = n_masked;
   a.cnt = static_cast<int32_t*>(workspace);
   a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + ((size_t)a.S * 4 + 255) / 256 * 256);
+  a.ticket = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + need - 256);
   const hipError_t e = launch_grpo(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess)
     return fail(nullptr, TANDEM_E_HIP, std::string("tandem_grpo_loss: ") + hipGetErrorString(e));

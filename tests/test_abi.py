@@ -119,8 +119,8 @@ def test_null_handle_calls():
 
 def test_grpo_workspace_size_and_argument_checks():
     cfg = L.GrpoCfg(16, 8, 3000, 0.2)
-    # counts [128] int32 and partials [128][ceil(3000 / 1024)] float, each 256-aligned
-    assert L.tandem_grpo_workspace_size(cfg) == 512 + 1536
+    # counts [128] int32, partials [128][ceil(3000 / 1024)] float and a ticket, each 256-aligned
+    assert L.tandem_grpo_workspace_size(cfg) == 512 + 1536 + 256
     for bad, code in ((L.GrpoCfg(0, 8, 3000, 0.2), L.E_SHAPE), (L.GrpoCfg(16, 0, 3000, 0.2), L.E_SHAPE),
                       (L.GrpoCfg(16, 8, 0, 0.2), L.E_SHAPE), (L.GrpoCfg(1024, 8, 3000, 0.2), L.E_SHAPE),
                       (L.GrpoCfg(16, 8, 3000, 1.0), L.E_ARG), (L.GrpoCfg(16, 8, 3000, -0.1), L.E_ARG)):
