@@ -6,6 +6,15 @@ prefill of both models on every prompt, then max_new tandem decode steps
 (dual forward, owner sampling, senior log-probs, handoff rule).  Inputs
 (weights, prompts, KV arena) are resident in HBM before the timed region.
 
+A rollout of the Qwen-shaped workload takes about 22 s, so the run keeps a
+wall-clock budget (--budget-s, counted from process start): the warmup runs
+one rollout (more only when they fit a short warm budget), the timed region
+covers at least one whole rollout and at most as many as fit --timed-s, and
+the optional legs (the instrumented rollouts, the CPU oracle) run only
+while the budget lasts.  `steps` and `warmup` in the line are the rollouts
+actually run (`steps_requested`, `warmup_requested` the flags), and
+ms_per_step x steps is the timed wall time.
+
 Prints ONE JSON line:
   value            co-generated tokens / s over the whole job (prefill + decode)
   roofline         decode attention (the dominant kernel): algorithmic K/V
@@ -21,9 +30,15 @@ Prints ONE JSON line:
                    (the junior's forward overlapping the senior's)
   (the timed region replays the captured step graph; graph-captured event
    records carry no launch times, so both roofline rollouts launch from the host)
-  cpu_baseline     the CPU oracle timed on a bounded sample of the same
-                   workload on this host's cores
+  cpu_baseline     the CPU oracle (float64 NumPy) timed on a bounded sample of
+                   the same workload on this host's cores
   decode_*         decode-only tokens/s and whole-decode-step HBM fraction
+
+Counter mode (HBM traffic per kernel class, rocprofv3 FETCH_SIZE and
+WRITE_SIZE, each in a run of its own):
+    rocprofv3 --pmc FETCH_SIZE -d <dir> -o fetch --output-format csv -- python3 bench.py --pmc-run
+    rocprofv3 --pmc WRITE_SIZE -d <dir> -o write --output-format csv -- python3 bench.py --pmc-run
+    python3 bench.py --pmc-analyze <fetch csv> <write csv>
 """
 from __future__ import annotations
 
@@ -35,6 +50,7 @@ import time
 
 import numpy as np
 
+T_START = time.perf_counter()
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -140,7 +156,28 @@ def prefill_flops(wl: W.Workload, plens) -> float:
     return f
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_attention_traffic_qwen.txt")
+
+
+# ------------------------------------------------------- HBM traffic counters
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic_qwen_by_kernel.txt")
+CSRC = os.path.join(ROOT, "paper_2606_28166_amd", "csrc")
+PMC_COPY_BYTES = 1 << 30
+PMC_WARM = 1000          # graph-replayed steps first: contexts ~1255 .. 1279 in the measured steps
+PMC_STEPS = 24
+# kernel classes of the decode step: (name, kernel-name substring, source file)
+PMC_CLASSES = (("attention", "attn_shared_kernel", "k_attn.hip"),
+               ("projections", "gemm_stream_kernel", "k_stream.hip"),
+               ("resid_norm", "resid_norm_kernel", "k_misc.hip"),
+               ("qkv_post", "qkv_post_kernel", "k_misc.hip"),
+               ("swiglu_finish", "swiglu_finish_kernel", "k_misc.hip"),
+               ("sample_partials", "sample_partials_kernel", "k_misc.hip"))
+PMC_REGEX = "attn_shared|gemm_stream|resid_norm|qkv_post|swiglu_finish|sample_partials|copy|elementwise"
+
+
+def source_digest(name: str) -> str:
+    import hashlib
+    with open(os.path.join(CSRC, name), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
 def measured_traffic_ratio():
@@ -148,22 +185,111 @@ def measured_traffic_ratio():
     algorithmic K/V byte of the decode attention kernel, from the committed
     rocprofv3 counter summary; None when that summary is missing or was taken
     on a different version of the kernel source."""
-    import hashlib
     try:
         txt = open(TRAFFIC_FILE).read()
         d = json.loads(txt[txt.index("\n{") + 1:])
-        src = os.path.join(ROOT, "paper_2606_28166_amd", "csrc", "k_attn.hip")
-        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-        if d["kernel_source_sha256_16"] != digest:
+        att = d["classes"]["attention"]
+        if att["source_sha256_16"] != source_digest("k_attn.hip"):
             return None
-        return float(d["traffic_over_algorithmic"])
+        return float(att["traffic_over_algorithmic"])
     except (OSError, IndexError, KeyError, ValueError):
         return None
 
 
+def pmc_run() -> None:
+    """The program the counter passes profile: a 1 GiB device copy (what
+    FETCH_SIZE / WRITE_SIZE report for exactly that many bytes read and
+    written), PMC_WARM decode steps of the Qwen-shaped rollout replayed from
+    the step graph (the contexts reach the middle of the 2048-token rollout),
+    a second, 4 MiB copy that marks where the measured steps begin, then
+    PMC_STEPS decode steps launched from the host (one dispatch per kernel)."""
+    import torch
+    from paper_2606_28166_amd import _lib as L
+    from paper_2606_28166_amd.engine import TandemEngine
+
+    dev = torch.device("cuda:0")
+    x = torch.ones(PMC_COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    del x, y
+    wl = W.workload("qwen")
+    wl.sample.max_new = PMC_WARM + PMC_STEPS
+    ws, wj, prompts, bnd = W.make_all(wl)
+    eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed,
+                       max_seqs=wl.n_seqs, max_ctx=max(len(p) for p in prompts) - 1 + wl.sample.max_new,
+                       max_prefill_tokens=4096, boundary_words=W.boundary_bits(bnd))
+    eng.prefill(prompts, wl.group)
+    for t in range(PMC_WARM):
+        eng.step()
+        if (t + 1) % 250 == 0:
+            torch.cuda.synchronize()
+            print(f"pmc: {t + 1} graph steps", flush=True)
+    torch.cuda.synchronize()
+    m = torch.ones(1 << 20, dtype=torch.float32, device=dev)
+    m2 = torch.empty_like(m)
+    m2.copy_(m)                                  # marker: the measured steps follow
+    torch.cuda.synchronize()
+    eng.timing(L.TIMING_EAGER)
+    for _ in range(PMC_STEPS):
+        eng.step()
+    torch.cuda.synchronize()
+    eng.close()
+    print("pmc run done", flush=True)
+
+
+def pmc_analyze(fetch_csv: str, write_csv: str) -> dict:
+    """Per kernel class, the HBM bytes of the measured steps' dispatches
+    (counter KiB x copy bytes / copy counter KiB) against the algorithmic
+    bytes of that class: the K/V context for decode attention (a shared
+    prompt prefix once per group), both models' weights for the projections
+    and LM heads, both models' fp32 logits for the sampling pass; the split-K
+    reductions have none of their own (their bytes are reported per step and
+    as a fraction of the weight bytes)."""
+    import csv
+    wl = W.workload("qwen")
+    plens = [wl.prompt_len] * wl.n_prompts
+    res = {"copy_bytes": PMC_COPY_BYTES, "prompt_len": wl.prompt_len,
+           "decode_steps": [PMC_WARM + 1, PMC_WARM + PMC_STEPS], "classes": {}}
+    per = {}
+    for name, path in (("fetch", fetch_csv), ("write", write_csv)):
+        rows = sorted((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"]))
+                      for r in csv.DictReader(open(path)))
+        copies = [(i, v) for i, k, v in rows if "copy" in k.lower() or "elementwise" in k.lower()]
+        if len(copies) < 2:
+            raise SystemExit(f"{path}: expected the calibration copy and the marker copy")
+        cal = max(v for _, v in copies)
+        marker = copies[-1][0]
+        scale = PMC_COPY_BYTES / cal
+        res[name] = {"copy_counter_kib": cal, "scale_bytes_per_kib": scale}
+        for cname, sub, _ in PMC_CLASSES:
+            vals = [v * scale for i, k, v in rows if i > marker and sub in k]
+            per.setdefault(cname, {})[name] = (sum(vals), len(vals))
+    kv = kv_bytes_per_token(wl.senior) + kv_bytes_per_token(wl.junior)
+    t0, t1 = PMC_WARM + 1, PMC_WARM + PMC_STEPS
+    alg = {"attention": sum(kv * _context_positions(wl, plens, t)[1] for t in range(t0, t1 + 1)),
+           "projections": PMC_STEPS * (weight_bytes(wl.senior) + weight_bytes(wl.junior)),
+           "sample_partials": PMC_STEPS * 2 * wl.n_seqs * wl.senior.vocab * 4}
+    wbytes = PMC_STEPS * (weight_bytes(wl.senior) + weight_bytes(wl.junior))
+    for cname, sub, srcf in PMC_CLASSES:
+        (fb, fn), (wb, wn) = per[cname]["fetch"], per[cname]["write"]
+        if fn != wn:
+            raise SystemExit(f"{cname}: {fn} fetch dispatches against {wn} write dispatches")
+        c = {"kernel": sub, "source_sha256_16": source_digest(srcf), "dispatches": fn,
+             "dispatches_per_step": fn / PMC_STEPS, "fetch_bytes": fb, "write_bytes": wb,
+             "bytes_per_step": (fb + wb) / PMC_STEPS, "over_weight_bytes": (fb + wb) / wbytes}
+        if cname in alg:
+            c["algorithmic_bytes"] = alg[cname]
+            c["traffic_over_algorithmic"] = (fb + wb) / alg[cname]
+        res["classes"][cname] = c
+    return res
+
+
 # ------------------------------------------------------------------ CPU oracle
 def cpu_baseline(wl: W.Workload, ws, wj, prompts, steps: int):
-    """The oracle (float64 NumPy) on prompt 0's G rows: its prefill plus `steps` decode steps."""
+    """The oracle (float64 NumPy, as it stands) on prompt 0's G rows: its
+    prefill plus `steps` decode steps, timed after the float64 weight copies
+    are built."""
     from oracle.rollout import rollout, build_models
     try:
         from threadpoolctl import threadpool_info
@@ -175,9 +301,11 @@ def cpu_baseline(wl: W.Workload, ws, wj, prompts, steps: int):
     rollout(sen, jun, prompts, wl.group, wl.switch, wl.sample, wl.philox_seed, W.make_boundary(wl),
             seq_subset=list(range(wl.group)), max_steps=steps)
     dt = time.perf_counter() - t0
-    return {"value": wl.group * steps / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+    return {"value": round(wl.group * steps / dt, 3), "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "precision": "f64",
             "sample": f"prompt 0 x G={wl.group} rows: prefill of {len(prompts[0]) - 1} prompt tokens + "
-                      f"{steps} decode steps ({wl.group * steps} co-generated tokens) in {dt:.1f} s",
+                      f"{steps} decode steps ({wl.group * steps} co-generated tokens) in {dt:.1f} s, "
+                      f"float64 NumPy on the same bf16-valued weights",
             "host_cpus": os.cpu_count(), "affinity": len(os.sched_getaffinity(0))}
 
 
@@ -185,28 +313,52 @@ def cpu_baseline(wl: W.Workload, ws, wj, prompts, steps: int):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1, help="timed rollouts requested (capped by --timed-s)")
+    ap.add_argument("--warmup", type=int, default=1, help="warmup rollouts requested (the first always runs)")
     ap.add_argument("--workload", default="qwen", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--max-new", type=int, default=None, help="shorter rollouts (development only)")
-    ap.add_argument("--cpu-steps", type=int, default=4, help="decode steps of the CPU-oracle sample")
+    ap.add_argument("--budget-s", type=float, default=420.0,
+                    help="wall-clock budget of the whole run, counted from process start: optional legs are "
+                         "skipped when what is left would not cover them")
+    ap.add_argument("--timed-s", type=float, default=75.0,
+                    help="the timed region runs as many requested rollouts as fit this many seconds (at least one)")
+    ap.add_argument("--warm-s", type=float, default=30.0,
+                    help="warmup rollouts after the first run only while they fit this many seconds")
+    ap.add_argument("--cpu-steps", type=int, default=16, help="decode steps of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-isolated", action="store_true",
                     help="skip the extra rollout that times every kernel class with the forwards serialized")
+    ap.add_argument("--no-concurrent", action="store_true",
+                    help="skip the extra rollout that times the attention launches in the two-stream schedule")
     ap.add_argument("--score", type=int, default=0, metavar="STEPS",
                     help="also time tandem_score_step after each of STEPS decode steps (reported as 'scoring')")
     ap.add_argument("--grpo", type=int, default=0, metavar="REPS",
                     help="also time tandem_grpo_loss REPS times over the last rollout's arenas (reported as 'grpo')")
+    ap.add_argument("--pmc-run", action="store_true", help="counter mode: the program rocprofv3 --pmc profiles")
+    ap.add_argument("--pmc-analyze", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="counter mode: per-class HBM traffic from the two counter passes (JSON)")
     args = ap.parse_args()
 
+    if args.pmc_analyze:
+        print(json.dumps(pmc_analyze(*args.pmc_analyze), indent=1))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
         print(json.dumps({"error": "this build runs on one GPU only: the tandem rollout shards over prompt "
                                    "groups with no per-step exchange, and no multi-GPU path is built"}))
         sys.exit(2)
+    if args.pmc_run:
+        pmc_run()
+        return
 
+    def left() -> float:
+        return args.budget_s - (time.perf_counter() - T_START)
+
+    log(f"[bench] {args.workload}: importing torch")
     import torch
-    from paper_2606_28166_amd.engine import TandemEngine
+    from paper_2606_28166_amd import _lib as LIB
+    from paper_2606_28166_amd.engine import TandemEngine, grpo_loss
+    log(f"[bench] torch ready ({time.perf_counter() - T_START:.0f}s since start)")
 
     wl = W.workload(args.workload)
     if args.max_new:
@@ -214,7 +366,7 @@ def main():
     t0 = time.time()
     ws, wj, prompts, bnd = W.make_all(wl)
     plens = [len(p) for p in prompts]
-    log(f"[bench] weights generated in {time.time() - t0:.1f}s")
+    log(f"[bench] weights generated in {time.time() - t0:.1f}s ({time.perf_counter() - T_START:.0f}s since start)")
     max_ctx = max(plens) - 1 + wl.sample.max_new
     eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed,
                        max_seqs=wl.n_seqs, max_ctx=max_ctx, max_prefill_tokens=4096,
@@ -223,12 +375,13 @@ def main():
     stream = eng.stream
     L = wl.sample.max_new
     n = wl.n_seqs
-
-    from paper_2606_28166_amd import _lib as LIB
+    skipped = []
 
     def rollout_once(timing=0):
-        """Prefill + L decode steps; timing = the library's class mask (0: step-graph replays)."""
+        """Prefill + L decode steps; timing = the library's class mask (0: step-graph replays).
+        Returns (prefill ms, decode ms, per-class timing or None, wall s)."""
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        w0 = time.perf_counter()
         ev[0].record(stream)
         eng.prefill(prompts, wl.group)
         ev[1].record(stream)
@@ -239,34 +392,45 @@ def main():
         torch.cuda.synchronize()
         tr = eng.timing_read() if timing & 0b1111 else None
         eng.timing(0)
-        return ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), tr
+        return ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), tr, time.perf_counter() - w0
 
-    for i in range(args.warmup):
-        p_ms, d_ms, _ = rollout_once()
-        log(f"[bench] warmup {i}: prefill {p_ms:.1f} ms, decode {d_ms:.1f} ms")
+    # ---- warmup: the first rollout captures the step graph and sets the
+    # estimate of one rollout's duration
+    n_warm, warm_wall, est = 0, 0.0, None
+    while n_warm < max(1, args.warmup):
+        if n_warm > 0 and (warm_wall + est > args.warm_s or left() < 3 * est):
+            break
+        p_ms, d_ms, _, w = rollout_once()
+        n_warm += 1
+        warm_wall += w
+        est = w
+        log(f"[bench] warmup {n_warm - 1}: prefill {p_ms:.1f} ms, decode {d_ms:.1f} ms ({w:.1f} s)")
 
     # ---- timed region: whole rollouts, decode steps replayed from the step graph
+    n_timed = max(1, min(args.steps, int(args.timed_s // est), int((left() - 2.0 * est) // est)))
+    log(f"[bench] timing {n_timed} rollout(s) of {args.steps} requested ({left():.0f}s of budget left)")
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     pre, dec = [], []
-    for i in range(args.steps):
-        p_ms, d_ms, _ = rollout_once()
+    for i in range(n_timed):
+        p_ms, d_ms, _, _ = rollout_once()
         pre.append(p_ms)
         dec.append(d_ms)
         log(f"[bench] step {i}: prefill {p_ms:.1f} ms, decode {d_ms:.1f} ms")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
+    est = wall / n_timed
 
     out = eng.outputs()
     lengths = out["length"].tolist() if wl.sample.eos_id >= 0 else None     # every run of this batch is identical
     gen = int(out["length"].sum())
     mask = np.arange(L)[None, :] < out["length"][:, None]
     senior_share = float(out["owner"][:, :L][mask].mean())
-    toks = gen * args.steps
-    ms_per_step = wall * 1e3 / args.steps
+    toks = gen * n_timed
+    ms_per_step = wall * 1e3 / n_timed
     value = toks / wall
     dec_s = sum(dec) / 1e3
-    dec_bytes = sum(decode_step_bytes(wl, plens, t, lengths) for t in range(1, L + 1)) * args.steps
+    dec_bytes = sum(decode_step_bytes(wl, plens, t, lengths) for t in range(1, L + 1)) * n_timed
     pf = prefill_flops(wl, plens)
     pre_ms = float(np.mean(pre))
 
@@ -283,37 +447,62 @@ def main():
         nbytes = attention_bytes(wl, plens, L, lengths)
         gbs = nbytes / (ms / 1e3) / 1e9
         per = nbytes / max(nl, 1)
-        return {"bound": "hbm", "kernel": "decode attention (both models; shared prompt prefix)" if shares_prefix(wl) else "decode attention (both models)", "achieved": round(gbs, 1),
+        return {"bound": "hbm", "kernel": "decode attention (both models; shared prompt prefix)" if shares_prefix(wl)
+                else "decode attention (both models)", "achieved": round(gbs, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                 "traffic": None if traffic_ratio is None else int(per * traffic_ratio),
                 "launches": nl, "avg_launch_us": round(ms * 1e3 / max(nl, 1), 2),
                 "bytes_per_launch": int(per), "method": method}
 
     roof, roof_conc, breakdown = None, None, None
-    if not args.no_isolated:
-        _, d_ser, tr = rollout_once(0b1111 | LIB.TIMING_SERIAL)
+    if args.no_isolated:
+        skipped.append("serialized rollout (--no-isolated)")
+    elif left() < 1.8 * est:
+        skipped.append(f"serialized rollout (budget: {left():.0f}s left)")
+    else:
+        _, d_ser, tr, _ = rollout_once(0b1111 | LIB.TIMING_SERIAL)
         breakdown = {k: {"ms": round(v[0], 3), "launches": v[1]} for k, v in tr.items()}
         roof = roofline_of(tr["attention"], "one rollout's decode steps, the two forwards serialized and launched "
                                             "from the host, a HIP event pair around every attention launch")
         log(f"[bench] serialized rollout: decode {d_ser:.1f} ms, attention {tr['attention'][0]:.1f} ms / "
-            f"{tr['attention'][1]} launches -> {roof['achieved']:.0f} GB/s")
-        _, d_con, tr = rollout_once(1 << LIB.K_ATTENTION)
+            f"{tr['attention'][1]} launches -> {roof['achieved']:.0f} GB/s ({left():.0f}s of budget left)")
+
+    cpu = None
+    if args.no_cpu_baseline:
+        skipped.append("cpu baseline (--no-cpu-baseline)")
+    elif left() < 120:
+        skipped.append(f"cpu baseline (budget: {left():.0f}s left)")
+    else:
+        log("[bench] timing the CPU oracle sample")
+        try:
+            cpu = cpu_baseline(wl, ws, wj, prompts, args.cpu_steps)
+            log(f"[bench] cpu oracle: {cpu['sample']} ({left():.0f}s of budget left)")
+        except MemoryError as e:                  # the float64 copies of the weights do not fit this host
+            skipped.append(f"cpu baseline ({e!r})")
+
+    if args.no_concurrent:
+        skipped.append("concurrent instrumented rollout (--no-concurrent)")
+    elif args.no_isolated or left() < 1.5 * est + 20:
+        skipped.append(f"concurrent instrumented rollout (budget: {left():.0f}s left)")
+    else:
+        _, d_con, tr, _ = rollout_once(1 << LIB.K_ATTENTION)
         roof_conc = roofline_of(tr["attention"], "one rollout's decode steps in the two-stream schedule, launched "
                                                  "from the host, a HIP event pair around every attention launch")
-        log(f"[bench] concurrent instrumented rollout: decode {d_con:.1f} ms, attention -> {roof_conc['achieved']:.0f} GB/s")
+        log(f"[bench] concurrent instrumented rollout: decode {d_con:.1f} ms, attention -> "
+            f"{roof_conc['achieved']:.0f} GB/s")
 
     scoring = None
     if args.score > 0:
         # the dual-distribution scores after each step of a fresh rollout:
         # HIP events on the library's stream around every scoring call
         eng.prefill(prompts, wl.group)
-        out = torch.empty((wl.n_seqs, 3), dtype=torch.float32, device=eng.dev)
+        sc_out = torch.empty((wl.n_seqs, 3), dtype=torch.float32, device=eng.dev)
         tot, ns = 0.0, min(args.score, L)
         for _ in range(ns):
             eng.step()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            eng.score(out)
+            eng.score(sc_out)
             e1.record(stream)
             torch.cuda.synchronize()
             tot += e0.elapsed_time(e1)
@@ -321,7 +510,7 @@ def main():
         nbytes = 4 * n * wl.senior.vocab * 4          # two passes over both models' fp32 logits
         scoring = {"steps": ns, "ms_per_step": round(ms, 4), "bytes_per_step": nbytes,
                    "achieved_gbs": round(nbytes / (ms / 1e3) / 1e9, 1),
-                   "frac_of_decode_step": round(ms / (sum(dec) / (L * args.steps)), 4)}
+                   "frac_of_decode_step": round(ms / (sum(dec) / (L * n_timed)), 4)}
         log(f"[bench] scoring: {ms * 1e3:.1f} us per step ({scoring['achieved_gbs']:.0f} GB/s)")
 
     grpo = None
@@ -330,27 +519,26 @@ def main():
         # authorship, log-prob and length arenas as tandem_step left them),
         # seeded binary rewards and the recorded log-probs plus seeded offsets
         # as the current policy's: HIP events on the stream the call runs on
-        from paper_2606_28166_amd.engine import grpo_loss
         g = torch.Generator(device="cpu").manual_seed(41)
         rewards = (torch.rand(n, generator=g) < 0.5).float().to(eng.dev)
         lp_new = eng.logprob[:n] + (0.15 * torch.randn(eng.logprob[:n].shape, generator=g)).to(eng.dev)
-        ws = torch.empty(LIB.tandem_grpo_workspace_size(LIB.GrpoCfg(n // wl.group, wl.group, eng.max_new, 0.2)),
-                         dtype=torch.uint8, device=eng.dev)
+        grpo_ws = torch.empty(LIB.tandem_grpo_workspace_size(LIB.GrpoCfg(n // wl.group, wl.group, eng.max_new, 0.2)),
+                              dtype=torch.uint8, device=eng.dev)
         args_g = (rewards, eng.owner[:n], eng.length[:n], eng.logprob[:n], lp_new, wl.group)
-        ref_g = grpo_loss(*args_g, workspace=ws)
+        ref_g = grpo_loss(*args_g, workspace=grpo_ws)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for _ in range(args.grpo):
-            grpo_loss(*args_g, workspace=ws)
+            grpo_loss(*args_g, workspace=grpo_ws)
         e1.record(stream)
         torch.cuda.synchronize()
         ms_eager = e0.elapsed_time(e1) / args.grpo
-        # the three launches of one call captured in a HIP graph and replayed:
+        # the launches of one call captured in a HIP graph and replayed:
         # device time without the host's per-call marshalling
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
-            cap_g = grpo_loss(*args_g, workspace=ws)
+            cap_g = grpo_loss(*args_g, workspace=grpo_ws)
         torch.cuda.synchronize()
         e0.record(stream)
         for _ in range(args.grpo):
@@ -373,24 +561,27 @@ def main():
         log(f"[bench] grpo loss: {ms * 1e3:.1f} us per call replayed ({ms_eager * 1e3:.1f} us eager; "
             f"{grpo['achieved_gbs']:.0f} GB/s over {grpo['positions']} positions; replays match: {same})")
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        eng_models = None
-        log("[bench] timing the CPU oracle sample")
-        cpu = cpu_baseline(wl, ws, wj, prompts, args.cpu_steps)
-
+    bf16 = wl.senior.dtype == "bf16"
     res = {
         "metric": METRIC,
         "value": round(value, 2),
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": n_timed,
+        "warmup": n_warm,
+        "steps_requested": args.steps,
+        "warmup_requested": args.warmup,
+        "step_unit": "one whole rollout: prefill of every prompt + %d tandem decode steps over %d rows" % (L, n),
         "ms_per_step": round(ms_per_step, 3),
+        "timed_wall_s": round(wall, 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if wl.senior.dtype == "bf16" else "f32",
+        "dtype": "bf16+fp16" if bf16 else "f32",
+        "dtype_detail": ("bf16 weights and K/V cache, fp32 accumulation and residual; QKV and O products on bf16 "
+                         "hi+lo split activations (two bf16 MFMAs), FFN and LM-head products fp16 x fp16 MFMA on "
+                         "fp16 copies of the bf16 weights; attention bf16 K/V with hi+lo q and P; fp32 sampling")
+                        if bf16 else "fp32 weights, activations and K/V",
         "data": "synthetic",
         "config": {"workload": DESCRIPTIONS[wl.name], "name": wl.name, "rows": n,
                    "prompt_len": plens[0] if min(plens) == max(plens) else [min(plens), max(plens)],
@@ -399,9 +590,9 @@ def main():
         "roofline": roof,
         "roofline_concurrent": roof_conc,
         "cpu_baseline": cpu,
-        "decode_tokens_per_s": round(gen * args.steps / dec_s, 2),
+        "decode_tokens_per_s": round(gen * n_timed / dec_s, 2),
         "generated_tokens": gen,
-        "decode_ms_per_token_step": round(sum(dec) / (L * args.steps), 4),
+        "decode_ms_per_token_step": round(sum(dec) / (L * n_timed), 4),
         "decode_hbm_gbs": round(dec_bytes / dec_s / 1e9, 1),
         "decode_hbm_frac": round(dec_bytes / dec_s / 1e9 / HBM_PEAK_GBS, 4),
         "prefill_ms": round(pre_ms, 3),
@@ -409,6 +600,8 @@ def main():
         "prefill_mfma_frac": round(pf / (pre_ms / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
         "senior_share": round(senior_share, 4),
         "breakdown": breakdown,
+        "skipped": skipped,
+        "run_wall_s": round(time.perf_counter() - T_START, 1),
     }
     if scoring is not None:
         res["scoring"] = scoring

@@ -250,14 +250,16 @@ def make_weights(shape: ModelShape, seed: int, gain_jitter: float = 0.0,
 
 
 def weights_as_float(shape: ModelShape, w: Dict[str, np.ndarray], dtype=np.float64) -> Dict[str, np.ndarray]:
-    """Convert generated weights to a float dtype (exact for bf16 inputs)."""
-    out = {}
-    for k, v in w.items():
+    """Convert generated weights to a float dtype (exact for bf16 inputs),
+    one tensor per thread (NumPy's conversions release the GIL)."""
+    def conv(kv):
+        k, v = kv
         if v.dtype == np.uint16:
-            out[k] = bf16_bits_to_f32(v).astype(dtype)
-        else:
-            out[k] = v.astype(dtype)
-    return out
+            return k, bf16_bits_to_f32(v).astype(dtype)
+        return k, v.astype(dtype)
+
+    with ThreadPoolExecutor(_threads()) as ex:
+        return dict(ex.map(conv, list(w.items())))
 
 
 def make_prompts(wl: Workload) -> List[np.ndarray]:
