@@ -16,7 +16,9 @@
 // The workgroup that counts itself last on a ticket sums the partials in
 // double in a fixed order (index order, whoever is last), so the loss is
 // deterministic.  Partials are exchanged through agent-scope stores and
-// loads, which are coherent across the chips' separate L2 caches.
+// loads, which are coherent across the chips' separate L2 caches; the ticket
+// is counted with release-acquire ordering at agent scope, so the last
+// workgroup reads every partial after its store.
 #include "common.h"
 #include "kernels.h"
 
@@ -91,12 +93,15 @@ __global__ __launch_bounds__(kGrpoNT) void grpo_loss_kernel(GrpoArgs a) {
   __shared__ int last;
   if (tid == 0) {
     st_dev(a.part + (size_t)s * a.n_chunks + chunk, acc);
-    __builtin_amdgcn_s_waitcnt(0);           // the partial is stored before it is counted
-    last = __hip_atomic_fetch_add(a.ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == np - 1;
+    // release: the partial is visible before the count; acquire: the last
+    // one to count sees every other workgroup's partial
+    last = __hip_atomic_fetch_add(a.ticket, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == np - 1;
   }
   __syncthreads();
   if (!last) return;
-  // the last workgroup: every partial has been stored
+  // the last workgroup: every partial has been stored; the fence orders this
+  // workgroup's loads after the acquire of its first thread
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __shared__ double dred[kGrpoNT];
   double sum = 0.0;
   for (int i = tid; i < np; i += kGrpoNT) sum += (double)ld_dev(a.part + i);
