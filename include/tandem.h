@@ -243,6 +243,23 @@ tandem_status tandem_grpo_loss(const tandem_grpo_cfg* cfg, const float* rewards,
                                float* advantages, float* grad, float* loss, int32_t* n_masked,
                                void* workspace, size_t workspace_bytes, void* stream);
 
+/* tandem_grpo_loss without the workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, serving loops and
+ * harnesses that forbid hipMalloc.  The workspace is a device array of the
+ * library's own, 1 MiB per GPU, held from the first call on that GPU until
+ * the process ends; the call allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine).  Batches whose tandem_grpo_workspace_size
+ * exceeds 1 MiB (S * ceil(T / 1024) partial sums plus S counts, each
+ * 256-byte aligned, plus 256 bytes) return TANDEM_E_CAPACITY.  Every call on
+ * one GPU shares that GPU's array (the kernels overwrite or clear everything
+ * they read), so calls that may overlap on one GPU (other streams, other
+ * threads) race and must not be issued.  Arguments, results and the other
+ * errors are those of tandem_grpo_loss. */
+tandem_status tandem_grpo_loss_noalloc(const tandem_grpo_cfg* cfg, const float* rewards, const uint8_t* owner,
+                                       const int32_t* length, const float* logp_old, const float* logp_new,
+                                       float* advantages, float* grad, float* loss, int32_t* n_masked,
+                                       void* stream);
+
 /* Copy the per-sequence sampler state to HOST int32 arrays of n_seqs
  * entries (any pointer may be NULL): owner (1 = senior), span counter c,
  * next step t, next position, done flag.  Synchronises the stream. */

@@ -62,7 +62,7 @@ class GrpoCfg(C.Structure):
 EXPORTS = ("tandem_workspace_size", "tandem_init", "tandem_prefill", "tandem_step",
            "tandem_step_forced", "tandem_score_step", "tandem_get_state", "tandem_timing_enable", "tandem_timing_read",
            "tandem_last_error", "tandem_status_string", "tandem_destroy", "tandem_grpo_workspace_size",
-           "tandem_grpo_loss")
+           "tandem_grpo_loss", "tandem_grpo_loss_noalloc")
 K_ATTENTION, K_GEMM, K_SAMPLE, K_OTHER = 0, 1, 2, 3
 TIMING_SERIAL = 1 << 8          # timing flag: run the two forwards one after the other
 TIMING_EAGER = 1 << 9           # timing flag: launch every kernel from the host (no step graph)
@@ -108,6 +108,8 @@ def _load():
     lib.tandem_grpo_workspace_size.restype = st
     lib.tandem_grpo_loss.argtypes = [C.POINTER(GrpoCfg), P, P, P, P, P, P, P, P, P, P, C.c_size_t, P]
     lib.tandem_grpo_loss.restype = st
+    lib.tandem_grpo_loss_noalloc.argtypes = [C.POINTER(GrpoCfg), P, P, P, P, P, P, P, P, P, P]
+    lib.tandem_grpo_loss_noalloc.restype = st
     return lib
 
 
@@ -194,3 +196,9 @@ def tandem_grpo_loss(cfg: GrpoCfg, rewards: int, owner: int, length: int, logp_o
                      stream: int) -> None:
     check(lib.tandem_grpo_loss(C.byref(cfg), rewards, owner, length, logp_old, logp_new, advantages, grad,
                                loss, n_masked, workspace, workspace_bytes, stream))
+
+
+def tandem_grpo_loss_noalloc(cfg: GrpoCfg, rewards: int, owner: int, length: int, logp_old: int, logp_new,
+                             advantages: int, grad, loss: int, n_masked: int, stream: int) -> None:
+    check(lib.tandem_grpo_loss_noalloc(C.byref(cfg), rewards, owner, length, logp_old, logp_new, advantages,
+                                       grad, loss, n_masked, stream))

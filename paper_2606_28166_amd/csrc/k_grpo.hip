@@ -19,6 +19,8 @@
 // loads, which are coherent across the chips' separate L2 caches; the ticket
 // is counted with release-acquire ordering at agent scope, so the last
 // workgroup reads every partial after its store.
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -118,7 +120,30 @@ __global__ __launch_bounds__(kGrpoNT) void grpo_loss_kernel(GrpoArgs a) {
   }
 }
 
+// The allocation-free entry point's workspace: one array per device, kept
+// until the process ends.  Host code uses its device address from
+// hipGetSymbolAddress (taken once per device), never the array's name.
+static __device__ __align__(256) unsigned char scratch[kGrpoStaticBytes];
+
 }  // namespace
+
+hipError_t grpo_static_workspace(void** ptr) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_grpo(const GrpoArgs& a, hipStream_t st) {
   grpo_adv_kernel<<<a.S, kGrpoNT, 0, st>>>(a);

@@ -209,6 +209,11 @@ struct GrpoArgs {
   float* adv; int32_t* cnt; float* part; int32_t* ticket; float* grad; float* loss; int32_t* n_masked;
 };
 hipError_t launch_grpo(const GrpoArgs& a, hipStream_t st);
+// Bytes of the device-resident workspace of the allocation-free GRPO entry
+// point, and its device address on the current device (looked up once per
+// device).
+constexpr size_t kGrpoStaticBytes = (size_t)1 << 20;
+hipError_t grpo_static_workspace(void** ptr);
 
 // Copy positions [p0, n_pos) of slot src into slots dst0 .. dst0 + n_dst - 1
 // for every layer and kv head (K and transposed V); p0 % 16 == 0.

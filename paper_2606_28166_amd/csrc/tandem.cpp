@@ -1292,4 +1292,38 @@ tandem_status tandem_grpo_loss(const tandem_grpo_cfg* cfg, const float* rewards,
     return fail(nullptr, TANDEM_E_HIP, std::string("tandem_grpo_loss: ") + hipGetErrorString(e));
   return TANDEM_OK;
 }
+
+tandem_status tandem_grpo_loss_noalloc(const tandem_grpo_cfg* cfg, const float* rewards, const uint8_t* owner,
+                                       const int32_t* length, const float* logp_old, const float* logp_new,
+                                       float* advantages, float* grad, float* loss, int32_t* n_masked,
+                                       void* stream) {
+  GrpoArgs a{};
+  size_t need = 0;
+  const tandem_status st = grpo_check(cfg, &need, &a);
+  if (st != TANDEM_OK) return st;
+  if (!rewards || !owner || !length || !logp_old || !advantages || !loss || !n_masked)
+    return fail(nullptr, TANDEM_E_ARG, "tandem_grpo_loss_noalloc: a required pointer is NULL");
+  if (need > kGrpoStaticBytes) {
+    char b[200];
+    snprintf(b, sizeof b,
+             "tandem_grpo_loss_noalloc: this batch needs %zu bytes of workspace, the library's device array holds "
+             "%zu; use tandem_grpo_loss with a workspace",
+             need, kGrpoStaticBytes);
+    return fail(nullptr, TANDEM_E_CAPACITY, b);
+  }
+  void* ws = nullptr;
+  hipError_t e = grpo_static_workspace(&ws);
+  if (e != hipSuccess)
+    return fail(nullptr, TANDEM_E_HIP, std::string("tandem_grpo_loss_noalloc: workspace address: ") +
+                                           hipGetErrorString(e));
+  a.rewards = rewards; a.owner = owner; a.length = length; a.logp_old = logp_old; a.logp_new = logp_new;
+  a.adv = advantages; a.grad = grad; a.loss = loss; a.n_masked = n_masked;
+  a.cnt = static_cast<int32_t*>(ws);
+  a.part = reinterpret_cast<float*>(static_cast<char*>(ws) + ((size_t)a.S * 4 + 255) / 256 * 256);
+  a.ticket = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + need - 256);
+  e = launch_grpo(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess)
+    return fail(nullptr, TANDEM_E_HIP, std::string("tandem_grpo_loss_noalloc: ") + hipGetErrorString(e));
+  return TANDEM_OK;
+}
 }  // extern "C"

@@ -163,12 +163,14 @@ class TandemEngine:
 
 def grpo_loss(rewards: torch.Tensor, owner: torch.Tensor, length: torch.Tensor, logp_old: torch.Tensor,
               logp_new: Optional[torch.Tensor], G: int, clip_eps: float = 0.2, want_grad: bool = True,
-              workspace: Optional[torch.Tensor] = None):
+              workspace: Optional[torch.Tensor] = None, noalloc: bool = False):
     """Senior-only GRPO loss pieces (tandem_grpo_loss) of S = len(rewards)
     rollouts in groups of G, on the current torch stream.  rewards float32
     [S]; owner uint8 [S][T]; length int32 [S]; logp_old / logp_new float32
     [S][T] (logp_new None: ratio 1).  Returns device tensors: advantages [S],
-    loss [1], n_masked [1] and grad [S][T] (None unless want_grad)."""
+    loss [1], n_masked [1] and grad [S][T] (None unless want_grad).
+    noalloc: call tandem_grpo_loss_noalloc (the library's own device
+    workspace; the output tensors are still allocated here)."""
     S, T = owner.shape
     dev = owner.device
     for name, t, dt, shape in (("rewards", rewards, torch.float32, (S,)), ("owner", owner, torch.uint8, (S, T)),
@@ -181,13 +183,19 @@ def grpo_loss(rewards: torch.Tensor, owner: torch.Tensor, length: torch.Tensor, 
     if S % G != 0:
         raise ValueError(f"grpo_loss: {S} rollouts do not form groups of {G}")
     cfg = L.GrpoCfg(S // G, G, T, float(clip_eps))
-    wsb = L.tandem_grpo_workspace_size(cfg)
-    if workspace is None or workspace.numel() < wsb:
-        workspace = torch.empty(wsb, dtype=torch.uint8, device=dev)
     adv = torch.empty(S, dtype=torch.float32, device=dev)
     loss = torch.empty(1, dtype=torch.float32, device=dev)
     n = torch.empty(1, dtype=torch.int32, device=dev)
     grad = torch.empty((S, T), dtype=torch.float32, device=dev) if want_grad else None
+    if noalloc:
+        L.tandem_grpo_loss_noalloc(cfg, rewards.data_ptr(), owner.data_ptr(), length.data_ptr(), logp_old.data_ptr(),
+                                   logp_new.data_ptr() if logp_new is not None else None, adv.data_ptr(),
+                                   grad.data_ptr() if grad is not None else None, loss.data_ptr(), n.data_ptr(),
+                                   torch.cuda.current_stream(dev).cuda_stream)
+        return dict(advantages=adv, loss=loss, n_masked=n, grad=grad)
+    wsb = L.tandem_grpo_workspace_size(cfg)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(wsb, dtype=torch.uint8, device=dev)
     L.tandem_grpo_loss(cfg, rewards.data_ptr(), owner.data_ptr(), length.data_ptr(), logp_old.data_ptr(),
                        logp_new.data_ptr() if logp_new is not None else None, adv.data_ptr(),
                        grad.data_ptr() if grad is not None else None, loss.data_ptr(), n.data_ptr(),

@@ -138,3 +138,21 @@ def test_grpo_workspace_size_and_argument_checks():
     assert call(C.byref(cfg), fake, fake, fake, fake, None, fake, None, fake, fake, fake, ws - 1, None) == L.E_ARG
     assert call(C.byref(cfg), fake, fake, fake, fake, None, fake, None, fake, fake, fake + 16, ws, None) == L.E_ARG
     assert b"aligned" in L.lib.tandem_last_error(None)
+
+
+def test_grpo_noalloc_argument_and_capacity_checks():
+    # every check fires before any HIP call: fake, never dereferenced addresses
+    fake = 1 << 20
+    call = L.lib.tandem_grpo_loss_noalloc
+    cfg = L.GrpoCfg(16, 8, 3000, 0.2)
+    assert call(None, fake, fake, fake, fake, None, fake, None, fake, fake, None) == L.E_ARG
+    assert call(C.byref(cfg), None, fake, fake, fake, None, fake, None, fake, fake, None) == L.E_ARG
+    assert call(C.byref(cfg), fake, fake, fake, fake, None, fake, None, None, fake, None) == L.E_ARG
+    assert call(C.byref(L.GrpoCfg(16, 8, 3000, 1.5)), fake, fake, fake, fake, None, fake, None, fake, fake,
+                None) == L.E_ARG
+    # the device array holds 1 MiB: 2^17 rollouts of 100 positions need
+    # 512 KiB of counts + 512 KiB of partial sums + 256 bytes
+    big = L.GrpoCfg(1 << 17, 1, 100, 0.2)
+    assert L.tandem_grpo_workspace_size(big) == (1 << 20) + 256
+    assert call(C.byref(big), fake, fake, fake, fake, None, fake, None, fake, fake, None) == L.E_CAPACITY
+    assert b"holds 1048576" in L.lib.tandem_last_error(None)
