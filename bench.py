@@ -96,12 +96,15 @@ def weight_bytes(s: W.ModelShape) -> int:
 
 
 def shares_prefix(wl: W.Workload) -> bool:
-    """Whether decode attention reads a prompt's K/V prefix once per group of
-    its G sequences (bf16 models, head_dim 64 or 128, at most 8 query heads per
-    kv head, G > 1), as the library decides at prefill."""
+    """Whether the G sequences of a prompt share its K/V prefix (bf16 models,
+    head_dim 64 or 128, at most 16 query heads per kv head, G > 1), as the
+    library decides at prefill: decode attention then reads the prefix from
+    the prompt's first slot for every row of the group, and the group's rows
+    run side by side on one XCD, so HBM delivers the prefix about once per
+    group (the rest comes from L2)."""
     def ok(s):
         g = s.n_q_heads // s.n_kv_heads
-        return s.dtype == "bf16" and s.head_dim in (64, 128) and g in (1, 2, 4, 8) and s.n_q_heads % s.n_kv_heads == 0
+        return s.dtype == "bf16" and s.head_dim in (64, 128) and g in (1, 2, 4, 8, 16) and s.n_q_heads % s.n_kv_heads == 0
     return wl.group > 1 and ok(wl.senior) and ok(wl.junior)
 
 

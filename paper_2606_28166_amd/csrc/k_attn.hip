@@ -21,6 +21,7 @@
 #include "common.h"
 #include "kernels.h"
 
+
 namespace tandem {
 
 namespace {
@@ -64,11 +65,11 @@ struct Half {
   u32x4_t r[HD / 32];
 };
 
-template <int HD>
+template <int HD, bool NT = true>
 __device__ __forceinline__ void load_half(Half<HD>& h, __amdgpu_buffer_rsrc_t rs, int chunk, int lane) {
   const int base = chunk * 32 * HD + lane * 16;   // bytes: 16 positions x HD x 2
 #pragma unroll
-  for (int j = 0; j < HD / 32; ++j) h.r[j] = buf_load16_nt(rs, base + j * 1024, 0);
+  for (int j = 0; j < HD / 32; ++j) h.r[j] = NT ? buf_load16_nt(rs, base + j * 1024, 0) : buf_load16(rs, base + j * 1024, 0);
 }
 
 // Orders the loads issued so far before everything that follows and ties h
@@ -176,12 +177,12 @@ __device__ __forceinline__ void attend_values(AttnState<HD>& st, Half<HD>& v, s1
 // in LDS: sm_m[w][c] (running max, log2 units), sm_l[w][c] (sum of
 // exponentials), sm_o[(w NCOL + c) HD + d] (unnormalised weighted sums).
 // GUARD: some column may see a chunk with no position it attends.
-template <int HD, int GQA, int NCOL, bool GUARD>
+template <int HD, int GQA, int NCOL, bool GUARD, bool NT = true>
 __device__ __forceinline__ void attend_block(const float* __restrict__ q, const bf16_t* __restrict__ kc,
                                              const bf16_t* __restrict__ vc, int ctx_stride, long slot_stride,
                                              int slot, int kh, int r0, int nr, int c0, int ctx_max,
                                              const int32_t* __restrict__ row_pos_col, int nq, float (*sm_m)[16],
-                                             float (*sm_l)[16], float* sm_o) {
+                                             float (*sm_l)[16], float* sm_o, int pslot = 0, int lo16 = 0) {
   constexpr int DC = HD / 32;     // k-steps of the S product
   constexpr int DB = HD / 16;     // 16-dim blocks of the O product
   static_assert(NCOL <= 16, "16 query columns per workgroup");
@@ -193,8 +194,14 @@ __device__ __forceinline__ void attend_block(const float* __restrict__ q, const 
   const int rr = r0 + (valid ? ri : 0);
   const int ctx = (valid && row_pos_col) ? row_pos_col[rr] + 1 : ctx_max;   // positions the column attends
   const size_t plane = (size_t)slot * slot_stride + (size_t)kh * ctx_stride * HD;
-  const __amdgpu_buffer_rsrc_t kr = buf_rsrc(kc + plane, (uint32_t)ctx_stride * HD * 2);
-  const __amdgpu_buffer_rsrc_t vr = buf_rsrc(vc + plane, (uint32_t)ctx_stride * HD * 2);
+  const __amdgpu_buffer_rsrc_t kr_o = buf_rsrc(kc + plane, (uint32_t)ctx_stride * HD * 2);
+  const __amdgpu_buffer_rsrc_t vr_o = buf_rsrc(vc + plane, (uint32_t)ctx_stride * HD * 2);
+  // chunks below lo16 come from the prefix plane (slot pslot), the rest from
+  // the row's own plane; the chunk index is wave-uniform, so the choice is a
+  // scalar select of the buffer descriptor
+  const size_t pplane = (size_t)pslot * slot_stride + (size_t)kh * ctx_stride * HD;
+  const __amdgpu_buffer_rsrc_t kr_p = buf_rsrc(kc + pplane, (uint32_t)ctx_stride * HD * 2);
+  const __amdgpu_buffer_rsrc_t vr_p = buf_rsrc(vc + pplane, (uint32_t)ctx_stride * HD * 2);
   const float scale = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
 
   // Wave w owns chunks c0 + w, c0 + w + 4, ... of the stream.  The query is
@@ -222,13 +229,15 @@ __device__ __forceinline__ void attend_block(const float* __restrict__ q, const 
   // compiler wait for every load in flight at each join).
   const int past = ctx_stride / 16 + 1;            // a chunk index outside the plane
   auto src = [&](int j) { return j < nmine ? chunk_at(j) : past; };
+  auto kr = [&](int c) { return c < lo16 ? kr_p : kr_o; };
+  auto vr = [&](int c) { return c < lo16 ? vr_p : vr_o; };
   Half<HD> h0, h1, h2, h3, h4, h5;
-  load_half<HD>(h0, kr, src(0), lane);
-  load_half<HD>(h1, vr, src(0), lane);
-  load_half<HD>(h2, kr, src(1), lane);
-  load_half<HD>(h3, vr, src(1), lane);
-  load_half<HD>(h4, kr, src(2), lane);
-  load_half<HD>(h5, vr, src(2), lane);
+  load_half<HD, NT>(h0, kr(src(0)), src(0), lane);
+  load_half<HD, NT>(h1, vr(src(0)), src(0), lane);
+  load_half<HD, NT>(h2, kr(src(1)), src(1), lane);
+  load_half<HD, NT>(h3, vr(src(1)), src(1), lane);
+  load_half<HD, NT>(h4, kr(src(2)), src(2), lane);
+  load_half<HD, NT>(h5, vr(src(2)), src(2), lane);
 
   // Q^T operand: column c16, k = dims 32dc + 8g .. +7 (zero for unused columns)
   bf16x8_t qh[DC], ql[DC];
@@ -257,11 +266,11 @@ __device__ __forceinline__ void attend_block(const float* __restrict__ q, const 
     pin_half<HD>(ks);
     attend_scores<HD, GUARD>(st, ks, qh, ql, p0, ctx, scale, g, ph, pl);
     pin_half<HD>(ks);
-    load_half<HD>(ks, kr, src(j + 3), lane);
+    load_half<HD, NT>(ks, kr(src(j + 3)), src(j + 3), lane);
     pin_half<HD>(vs);
     attend_values<HD>(st, vs, ph, pl, p0, ctx_max, g);
     pin_half<HD>(vs);
-    load_half<HD>(vs, vr, src(j + 3), lane);
+    load_half<HD, NT>(vs, vr(src(j + 3)), src(j + 3), lane);
   };
   // whole groups of three chunks as straight-line code, then the last < 3
   int i = 0;
@@ -358,153 +367,36 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   }
 }
 
-// Device-coherent (agent scope) accesses of the partial-softmax exchange:
-// they bypass the per-XCD L2 caches, so a partial written by a workgroup on
-// one XCD is what a workgroup on another reads once the counter says so.
-__device__ __forceinline__ void st_dev(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_dev(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Both partial softmaxes of a column merged (prefix first, then the row's
-// own part: the same arithmetic whichever workgroup does it).
-__device__ __forceinline__ float merge_partials(float mp, float lp, float np, float ms, float ls, float ns) {
-  const float M = fmaxf(mp, ms);
-  const float fp = exp2f(mp - M), fs = exp2f(ms - M);
-  return (np * fp + ns * fs) / (lp * fp + ls * fs);
-}
-
-// Decode rows whose prompt prefix is shared by the G sequences of the prompt.
-// The softmax over positions [0, n) splits exactly into partial softmaxes over
-// [0, lo) and [lo, n), each carried as (running max M, sum of exponentials,
-// unnormalised weighted sum of V) and merged by rescaling both to the larger
-// max.  One launch holds two kinds of workgroups:
-//   * y < n_pfx (prefix): rows r0 .. r0 + nr - 1 of a prefix group (16 / GQA
-//     rows, query column c = (row c / GQA, head c % GQA)) over positions
-//     [0, lo) of the group's source slot, read once for all of them;
-//   * y = n_pfx + r (row r): positions [lo, pos] of the row's own slot
-//     (lo = row_lo[r], a multiple of 16; 0: no shared prefix, the row's
-//     output directly).
-// The first of the two to finish writes its partial ([row][head][HD + 2]:
-// the weighted sums, M, the sum; part_p and part_s), waits for the stores
-// to complete, and counts itself on the (row, kv head) counter; the second
-// merges both partials into the output row and clears the counter for the
-// next launch.  No workgroup waits for another.  Done rows take no part
-// (zero output).
-template <int HD, int GQA>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_shared_kernel(
+// Decode rows whose prompt prefix is shared, one workgroup per (kv head,
+// row) and no exchange between workgroups: the row streams positions [0, lo)
+// from the plane of the prompt's first sequence (pfx_slot) and [lo, pos] from
+// its own.  The G rows of a prompt are consecutive in the grid, so for each
+// kv head they run side by side on one XCD and read the prefix through its L2.
+template <int HD, int GQA, bool NT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_rows_kernel(
     const float* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     int ctx_stride, long slot_stride, const int32_t* __restrict__ row_slot,
     const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_done,
-    const int32_t* __restrict__ row_lo, const int32_t* __restrict__ pfx_row0, const int32_t* __restrict__ pfx_n,
-    const int32_t* __restrict__ pfx_slot, int n_pfx, int sub_per_grp, float* __restrict__ part_p,
-    float* __restrict__ part_s, int32_t* __restrict__ cnt, bf16_t* __restrict__ out, int nq, int nkv) {
-  constexpr int RP = 16 / GQA;                     // rows of a prefix workgroup
-  constexpr int W = HD + 2;                        // floats of one column's partial
-  static_assert(RP > 1, "the prefix pass serves several rows");
+    const int32_t* __restrict__ row_lo, const int32_t* __restrict__ pfx_slot, bf16_t* __restrict__ out, int nq) {
   __shared__ float sm_m[4][16];
   __shared__ float sm_l[4][16];
-  __shared__ float sm_o[4 * 16 * HD];
-  __shared__ int sm_last[RP];
-
-  const int kh = blockIdx.x, tid = threadIdx.x;
+  __shared__ float sm_o[4 * GQA * HD];
+  const int kh = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
   const int col0 = kh * GQA * HD;
-  if ((int)blockIdx.y < n_pfx) {
-    const int grp = blockIdx.y / sub_per_grp, sub = blockIdx.y % sub_per_grp;
-    const int r0 = pfx_row0[grp] + sub * RP;
-    const int nr = min(RP, pfx_n[grp] - sub * RP);
-    if (nr <= 0) return;
-    constexpr int NCOL = GQA * RP;
-    attend_block<HD, GQA, NCOL, false>(q, kc, vc, ctx_stride, slot_stride, pfx_slot[r0], kh, r0, nr, 0,
-                                       row_lo[r0], nullptr, nq, sm_m, sm_l, sm_o);
-    for (int e = tid; e < NCOL * HD; e += 256) {
-      const int c = e / HD, d = e % HD;
-      if (c / GQA >= nr) continue;
-      float M, num, den;
-      waves_merged<HD, NCOL>(sm_m, sm_l, sm_o, c, d, M, num, den);
-      float* pp = part_p + ((size_t)(r0 + c / GQA) * nq + kh * GQA + c % GQA) * W;
-      st_dev(pp + d, num);
-      if (d == 0) {
-        st_dev(pp + HD, M);
-        st_dev(pp + HD + 1, den);
-      }
-    }
-    __builtin_amdgcn_s_waitcnt(0);                 // the partial is stored before it is counted
-    __syncthreads();
-    if (tid < nr) {
-      const int r = r0 + tid;
-      sm_last[tid] = row_done[r] ? 0 : __hip_atomic_fetch_add(cnt + (size_t)r * nkv + kh, 1, __ATOMIC_RELAXED,
-                                                              __HIP_MEMORY_SCOPE_AGENT) == 1;
-    }
-    __syncthreads();
-    for (int e = tid; e < NCOL * HD; e += 256) {
-      const int c = e / HD, d = e % HD;
-      if (c / GQA >= nr || !sm_last[c / GQA]) continue;
-      float M, num, den;
-      waves_merged<HD, NCOL>(sm_m, sm_l, sm_o, c, d, M, num, den);
-      const int r = r0 + c / GQA;
-      const float* ps = part_s + ((size_t)r * nq + kh * GQA + c % GQA) * W;
-      bf16_t* orow = out + (size_t)r * 2 * nq * HD;
-      split_store(orow, col0 + (c % GQA) * HD + d, merge_partials(M, den, num, ld_dev(ps + HD), ld_dev(ps + HD + 1),
-                                                                  ld_dev(ps + d)));
-    }
-    if (tid < nr && sm_last[tid])
-      __hip_atomic_store(cnt + (size_t)(r0 + tid) * nkv + kh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return;
-  }
-
-  const int r = blockIdx.y - n_pfx;
   bf16_t* orow = out + (size_t)r * 2 * nq * HD;    // split-format activation row
   if (row_done[r]) {
     for (int e = tid; e < GQA * HD; e += 256) split_store(orow, col0 + e, 0.f);
     return;
   }
   const int lo = row_lo[r];
-  attend_block<HD, GQA, GQA, false>(q, kc, vc, ctx_stride, slot_stride, row_slot[r], kh, r, 1, lo >> 4,
-                                    row_pos[r] + 1, nullptr, nq, sm_m, sm_l, sm_o);
-  if (lo == 0) {
-    for (int e = tid; e < GQA * HD; e += 256) {
-      float M, num, den;
-      waves_merged<HD, GQA>(sm_m, sm_l, sm_o, e / HD, e % HD, M, num, den);
-      split_store(orow, col0 + e, num / den);
-    }
-    return;
-  }
-  // The prefix workgroups come first in the grid and are short: usually the
-  // prefix partial is there by now (counter 1) and the row merges at once.
-  // Otherwise it publishes its own partial and counts itself; the prefix
-  // workgroup merges if it comes second.
-  int32_t* const cp = cnt + (size_t)r * nkv + kh;
-  if (tid == 0) sm_last[0] = __hip_atomic_load(cp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  if (!sm_last[0]) {                               // (uniform: every thread read the same flag)
-    for (int e = tid; e < GQA * HD; e += 256) {
-      const int c = e / HD, d = e % HD;
-      float M, num, den;
-      waves_merged<HD, GQA>(sm_m, sm_l, sm_o, c, d, M, num, den);
-      float* ps = part_s + ((size_t)r * nq + kh * GQA + c) * W;
-      st_dev(ps + d, num);
-      if (d == 0) {
-        st_dev(ps + HD, M);
-        st_dev(ps + HD + 1, den);
-      }
-    }
-    __builtin_amdgcn_s_waitcnt(0);                 // the partial is stored before it is counted
-    __syncthreads();
-    if (tid == 0) sm_last[0] = __hip_atomic_fetch_add(cp, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
-    __syncthreads();
-    if (!sm_last[0]) return;
-  }
+  attend_block<HD, GQA, GQA, false, NT>(q, kc, vc, ctx_stride, slot_stride, row_slot[r], kh, r, 1, 0,
+                                        row_pos[r] + 1, nullptr, nq, sm_m, sm_l, sm_o, lo > 0 ? pfx_slot[r] : 0,
+                                        lo >> 4);
   for (int e = tid; e < GQA * HD; e += 256) {
-    const int c = e / HD, d = e % HD;
     float M, num, den;
-    waves_merged<HD, GQA>(sm_m, sm_l, sm_o, c, d, M, num, den);
-    const float* pp = part_p + ((size_t)r * nq + kh * GQA + c) * W;
-    split_store(orow, col0 + e, merge_partials(ld_dev(pp + HD), ld_dev(pp + HD + 1), ld_dev(pp + d), M, den, num));
+    waves_merged<HD, GQA>(sm_m, sm_l, sm_o, e / HD, e % HD, M, num, den);
+    split_store(orow, col0 + e, num / den);
   }
-  if (tid == 0) __hip_atomic_store(cp, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <typename KT, bool SPLIT>
@@ -578,15 +470,11 @@ hipError_t run_mfma(const AttnArgs& a, hipStream_t st) {
                        a.grp_n, 16 / RB, (bf16_t*)a.out, a.nq);
     return hipGetLastError();
   }
-  if (a.part) {                         // decode rows with a shared prompt prefix
-    if (ROWS == 1 || !a.row_done || a.pfx_rows < 1 || a.pfx_rows > 16) return hipErrorInvalidValue;
-    const int sub = (a.pfx_rows + RB - 1) / RB;
-    const int n_pfx = a.pfx_groups * sub;
-    const long W = (long)a.R * a.nq * (a.hd + 2);
-    hipLaunchKernelGGL((attn_shared_kernel<HD, (ROWS > 1 ? GQA : 8)>), dim3(a.nkv, n_pfx + a.R), dim3(256), 0, st,
-                       a.q, kc, vc, a.cache.ctx_stride, a.cache.slot_stride, a.row_slot, a.row_pos, a.row_done,
-                       a.row_lo, a.pfx_row0, a.pfx_n, a.pfx_slot, n_pfx, sub, a.part, a.part + W, a.cnt,
-                       (bf16_t*)a.out, a.nq, a.nkv);
+  if (a.row_lo) {                       // decode rows with a shared prompt prefix
+    if (!a.row_done || !a.pfx_slot) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((attn_rows_kernel<HD, GQA, true>), dim3(a.nkv, a.R), dim3(256), 0, st, a.q, kc, vc,
+                       a.cache.ctx_stride, a.cache.slot_stride, a.row_slot, a.row_pos, a.row_done, a.row_lo,
+                       a.pfx_slot, (bf16_t*)a.out, a.nq);
     return hipGetLastError();
   }
   hipLaunchKernelGGL((attn_mfma_kernel<HD, GQA, 1>), dim3(a.nkv, a.R), dim3(256), 0, st, a.q, kc, vc,
@@ -613,7 +501,7 @@ bool attention_has_mfma(int dt, int hd, int gqa) {
   return dt == DT_BF16 && (hd == 64 || hd == 128) && (gqa == 1 || gqa == 2 || gqa == 4 || gqa == 8 || gqa == 16);
 }
 
-bool attention_shares_prefix(int dt, int hd, int gqa) { return attention_has_mfma(dt, hd, gqa) && gqa <= 8; }
+bool attention_shares_prefix(int dt, int hd, int gqa) { return attention_has_mfma(dt, hd, gqa); }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st) {
   if (a.R <= 0) return hipSuccess;

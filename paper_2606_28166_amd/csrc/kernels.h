@@ -134,17 +134,11 @@ struct AttnArgs {
   // rows of one prompt, rows grp_row0[g] .. + grp_n[g] - 1 in increasing
   // position order; NULL: one workgroup per row
   const int32_t* grp_row0; const int32_t* grp_n; int n_groups;
-  // Decode rows whose prompt prefix is shared (part != NULL; needs row_done):
-  // row r attends positions [0, row_lo[r]) in slot pfx_slot[r] and
-  // [row_lo[r], row_pos[r]] in its own slot; row_lo is a multiple of 16 (0: no
-  // shared prefix).  pfx_groups groups of at most pfx_rows (<= 16) consecutive
-  // rows with the same prefix (pfx_row0, pfx_n; a group with pfx_n = 0 is
-  // skipped) cover every row with row_lo > 0, each row once.  part: 2 R nq
-  // (hd + 2) floats of partial softmaxes; cnt: R nkv counters, all zero
-  // between launches (each launch leaves them so).  Both are the model's own:
-  // the two models' attentions may run at the same time.
-  const int32_t* row_lo; const int32_t* pfx_slot; float* part; int32_t* cnt;
-  const int32_t* pfx_row0; const int32_t* pfx_n; int pfx_groups; int pfx_rows;
+  // Decode rows whose prompt prefix is shared (row_lo != NULL; needs
+  // row_done): row r attends positions [0, row_lo[r]) in slot pfx_slot[r]
+  // and [row_lo[r], row_pos[r]] in its own slot; row_lo is a multiple of 16
+  // (0: the whole context in the row's own slot).
+  const int32_t* row_lo; const int32_t* pfx_slot;
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
 

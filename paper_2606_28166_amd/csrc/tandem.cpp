@@ -57,8 +57,6 @@ struct ModelPlan {            // byte offsets / sizes of one model's buffers
   size_t ws_floats;
   size_t kv_half;             // bytes of the K (= V) cache
   size_t off_h, off_xa, off_xf, off_q, off_ws, off_logits, off_rope;
-  size_t off_part;            // partial softmaxes of the decode attention [2][max_seqs][n_q][hd + 2]
-  size_t off_cnt;             // its (row, kv head) counters [max_seqs][n_kv]
   size_t off_packed, packed_bytes;   // MFMA-ordered copies of the projection and LM-head weights
 };
 
@@ -89,7 +87,7 @@ struct Plan {
   ModelPlan m[2];
   size_t kv_bytes;
   size_t off_state, off_seq_slot, off_rows, off_prompt, off_partials, off_count, off_act, off_drows;
-  size_t off_pfx;             // shared-prefix tables of the decode rows (4 x max_seqs int32)
+  size_t off_pfx;             // shared-prefix tables of the decode rows (2 x max_seqs int32)
   size_t off_score;           // dual-distribution score partials [max_seqs][n_chunks][6]
   size_t scratch_bytes;
 };
@@ -118,8 +116,6 @@ struct Model {
   float* ws;
   float* logits;
   float2* rope;
-  float* part;
-  int32_t* cnt;
 };
 
 tandem_status fail(std::string* where, tandem_status s, const std::string& msg) {
@@ -210,8 +206,6 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
     m.off_ws = sc; sc = align_up(sc + m.ws_floats * 4, kAlign);
     m.off_logits = sc; sc = align_up(sc + (size_t)cap->max_seqs * c->vocab * 4, kAlign);
     m.off_rope = sc; sc = align_up(sc + (size_t)P.ctx_stride * (c->head_dim / 2) * 8, kAlign);
-    m.off_part = sc; sc = align_up(sc + (size_t)2 * cap->max_seqs * c->n_q_heads * (c->head_dim + 2) * 4, kAlign);
-    m.off_cnt = sc; sc = align_up(sc + (size_t)cap->max_seqs * c->n_kv_heads * 4, kAlign);
     m.packed_bytes = 0;
     for (const auto& nk : packed_shapes(c))
       if (packs(c, nk.first, nk.second)) m.packed_bytes += align_up(packed_weight_bytes(nk.first, nk.second), kAlign);
@@ -227,7 +221,7 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
   P.off_count = sc; sc = align_up(sc + 4, kAlign);
   P.off_act = sc; sc = align_up(sc + S * 4, kAlign);
   P.off_drows = sc; sc = align_up(sc + 4 * S * 4, kAlign);
-  P.off_pfx = sc; sc = align_up(sc + 4 * S * 4, kAlign);
+  P.off_pfx = sc; sc = align_up(sc + 2 * S * 4, kAlign);
   P.off_score = sc; sc = align_up(sc + S * P.n_chunks * 6 * 4, kAlign);
   P.scratch_bytes = sc;
   return P;
@@ -271,14 +265,13 @@ struct tandem_handle {
   int R_launch = 0;
   // Shared prompt prefix.  The G sequences of a prompt hold the same K/V at
   // the prompt positions: decode attention reads positions [0, lo) (lo = the
-  // prompt length - 1 rounded down to 16) once per block of rows from the
-  // slot of the prompt's first sequence, and each row's own slot from lo on.
-  // The tables depend on the act order only (rebuilt at prefill and at each
-  // compaction): per row lo and the prefix slot; then pfx_max groups of at
-  // most pfx_rows consecutive rows with the same prefix (unused: 0 rows).
+  // prompt length - 1 rounded down to 16) from the slot of the prompt's first
+  // sequence and each row's own slot from lo on.  The per-row tables (lo,
+  // prefix slot) follow the act order (rebuilt at prefill and at each
+  // compaction).
   bool share = false;
-  int32_t *row_lo, *pfx_slot, *pfx_row0, *pfx_n;
-  int pfx_max = 0, pfx_rows = 0, G = 1;
+  int32_t *row_lo, *pfx_slot;
+  int G = 1;
   std::vector<int32_t> lo_of_prompt;                 // host, per prompt
   std::vector<int32_t> h_pfx, h_act;                 // host staging (kept until the next rebuild)
   int steps_since_compact = 0;
@@ -534,8 +527,7 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   aa.row_slot = fr.slot; aa.row_pos = fr.pos; aa.row_done = fr.done; aa.out = m.xa;
   aa.grp_row0 = fr.grp_row0; aa.grp_n = fr.grp_n; aa.n_groups = fr.n_groups;
   if (fr.shared_prefix) {
-    aa.row_lo = h->row_lo; aa.pfx_slot = h->pfx_slot; aa.part = m.part; aa.cnt = m.cnt;
-    aa.pfx_row0 = h->pfx_row0; aa.pfx_n = h->pfx_n; aa.pfx_groups = h->pfx_max; aa.pfx_rows = h->pfx_rows;
+    aa.row_lo = h->row_lo; aa.pfx_slot = h->pfx_slot;
   }
   if (att_wait) HIPCHK(hipStreamWaitEvent(st, att_wait, 0));
   TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
@@ -661,32 +653,17 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
 }
 
 // Shared-prefix tables of decode rows 0 .. R-1 in the act order act_host
-// (see tandem_handle::share), copied to the device on the handle's stream.
-// Rows of one prompt are consecutive in any act order (sequence ids grow
-// within each part of the partition), so a group is a run of rows with the
-// same prompt and the same 16-block of sequence index within the prompt:
-// at most 16 rows, and at most two runs per (prompt, block).
+// (see tandem_handle::share), copied to the device on the handle's stream:
+// per row its prompt's lo and the slot of the prompt's first sequence.
 tandem_status upload_prefix_tables(tandem_handle* h, const int32_t* act_host, int R) {
   const int S = h->cap.max_seqs, G = h->G;
   std::vector<int32_t>& t = h->h_pfx;
-  t.assign(4 * (size_t)S, 0);
-  int32_t *lo = t.data(), *ps = lo + S, *g0 = lo + 2 * S, *gn = lo + 3 * S;
-  int ng = 0;
+  t.assign(2 * (size_t)S, 0);
+  int32_t *lo = t.data(), *ps = lo + S;
   for (int r = 0; r < R; ++r) {
-    const int s = act_host[r], j = s / G;
+    const int j = act_host[r] / G;
     lo[r] = h->lo_of_prompt[j];
-    if (lo[r] == 0) continue;
-    ps[r] = j * G;                 // slot of the prompt's first sequence (slots follow sequence ids)
-    const bool cont = ng > 0 && g0[ng - 1] + gn[ng - 1] == r && act_host[r - 1] / G == j &&
-                      (act_host[r - 1] % G) / 16 == (s % G) / 16;
-    if (cont) {
-      ++gn[ng - 1];
-      continue;
-    }
-    if (ng == h->pfx_max) return fail(&h->err, TANDEM_E_STATE, "shared-prefix table overflow");
-    g0[ng] = r;
-    gn[ng] = 1;
-    ++ng;
+    ps[r] = j * G;                 // slots follow sequence ids
   }
   HIPCHK(hipMemcpyAsync(h->row_lo, t.data(), t.size() * 4, hipMemcpyHostToDevice, h->stream));
   return TANDEM_OK;
@@ -925,8 +902,6 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     m.ws = (float*)(sc + m.p.off_ws);
     m.logits = (float*)(sc + m.p.off_logits);
     m.rope = (float2*)(sc + m.p.off_rope);
-    m.part = (float*)(sc + m.p.off_part);
-    m.cnt = (int32_t*)(sc + m.p.off_cnt);
     m.p_lm = nullptr;
   }
   const size_t S = (size_t)cap->max_seqs;
@@ -947,7 +922,7 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   h->drow_tok = drows; h->drow_slot = drows + S; h->drow_pos = drows + 2 * S; h->drow_done = drows + 3 * S;
   h->score_part = (float*)(sc + P.off_score);
   int32_t* pfx = (int32_t*)(sc + P.off_pfx);
-  h->row_lo = pfx; h->pfx_slot = pfx + S; h->pfx_row0 = pfx + 2 * S; h->pfx_n = pfx + 3 * S;
+  h->row_lo = pfx; h->pfx_slot = pfx + S;
   h->h_count = nullptr;
 
   // --- HIP work from here on
@@ -1036,9 +1011,6 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   if (e != hipSuccess) return bail(e, "seq slots");
   e = hipMemsetAsync(stt, 0, 6 * S * 4, h->stream);
   if (e != hipSuccess) return bail(e, "state");
-  for (int i = 0; i < 2 && e == hipSuccess; ++i)       // the attention counters start (and stay) at zero
-    e = hipMemsetAsync(h->m[i].cnt, 0, S * h->m[i].cfg.n_kv_heads * 4, h->stream);
-  if (e != hipSuccess) return bail(e, "attention counters");
   e = hipStreamSynchronize(h->stream);
   if (e != hipSuccess) return bail(e, "synchronize");
   *out_handle = h;
@@ -1098,8 +1070,6 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
     h->lo_of_prompt.assign((size_t)n_prompts, 0);
     if (share)
       for (int j = 0; j < n_prompts; ++j) h->lo_of_prompt[j] = (prompt_offsets[j + 1] - prompt_offsets[j] - 1) / 16 * 16;
-    h->pfx_rows = std::min(G, 16);
-    h->pfx_max = (int)std::min<long>((long)2 * n_prompts * ((G + 15) / 16), h->cap.max_seqs);
   }
   // chunks of whole prompts whose (P - 1) rows fit max_prefill_tokens
   int j0 = 0;
