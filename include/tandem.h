@@ -23,7 +23,9 @@
  *
  * Streams: every call enqueues its work on the stream given to tandem_init
  * (a hipStream_t passed as void*) and returns without synchronising, except
- * when a host result is requested (n_active, tandem_get_state).
+ * where a call below says otherwise: a host result is requested (n_active,
+ * tandem_get_state, tandem_timing_read), a batch with an EOS token compacts
+ * its rows (once every 32 steps), tandem_timing_enable and tandem_destroy.
  *
  * Errors: every call returns a tandem_status; tandem_last_error(handle) (or
  * tandem_last_error(NULL) for calls that failed before a handle existed)
@@ -149,31 +151,52 @@ tandem_status tandem_workspace_size(const tandem_model_cfg* senior, const tandem
                                     const tandem_capacity* cap, size_t* kv_bytes,
                                     size_t* scratch_bytes);
 
-/* Validate the pair (shared vocabulary, supported head_dim, ...), bind the
- * weights, arenas and stream, and build per-model tables.  stream is a
- * hipStream_t (NULL = the null stream).  On success *out_handle is set. */
+/* Algorithm 1's inputs: the senior and the junior policies (one shared
+ * vocabulary), the handoff probability p, the boundary set and the span cap K
+ * (the reproducibility appendix's word-level handoff details), plus the
+ * sampling settings and the per-request seed of the appendix's seeded
+ * generator.  Validates the pair (shared vocabulary, supported head_dim, ...),
+ * binds the weights, arenas and stream, and enqueues the per-model tables
+ * (rotary table, MFMA-ordered weight copies in scratch) on the stream; it
+ * does not wait for them (later calls on the same stream are ordered after
+ * them).  stream is a hipStream_t (NULL = the null stream).  On success
+ * *out_handle is set; on failure nothing is left allocated. */
 tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior,
                           const tandem_switch_cfg* sw, const tandem_sample_cfg* smp,
                           const tandem_capacity* cap, void* kv_arena, size_t kv_bytes,
                           void* scratch, size_t scratch_bytes, const tandem_outputs* out,
                           void* stream, tandem_handle** out_handle);
 
-/* Prefill both models on every prompt but its last token, replicate the
- * prompt's KV into its G sequences, and set each sequence's state: pending
- * token = last prompt token, position = P_j - 1, step t = 1, span counter 0,
- * first owner per first_owner.
- *   prompt_tokens  device int32, prompts concatenated
+/* Section 3.3: both models condition on the prompt x before the first token
+ * (the dual-decoder backend of the reproducibility appendix keeps one cache
+ * per model on shared positions).  Prefills both models on every prompt but
+ * its last token, shares the prompt's K/V among its G sequences, and sets each
+ * sequence's state: pending token = last prompt token, position = P_j - 1,
+ * step t = 1, span counter 0, first owner per first_owner (DRAW: Algorithm 1's
+ * Bernoulli(p) first draw).
+ *   prompt_tokens  device int32, prompts concatenated (read on the stream)
  *   prompt_offsets HOST int32 [n_prompts + 1], CSR offsets into prompt_tokens
  * Every prompt needs >= 1 token.  Sequence ids are s = j * G + i.  A new
- * prefill starts a new batch (all previous sequence state is replaced). */
+ * prefill starts a new batch (all previous sequence state is replaced).
+ * Asynchronous: the per-prompt table is uploaded from pinned staging and the
+ * prefill rows are built on the device.  The call waits only if the previous
+ * prefill's table upload is still queued on the stream.  Token ids are
+ * checked on the device: an id outside [0, vocab) is read as 0 and makes the
+ * next synchronising call (tandem_step with n_active, a compaction step,
+ * tandem_get_state) return TANDEM_E_ARG; the batch is then void and steps
+ * return TANDEM_E_STATE until the next prefill. */
 tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens,
                              const int32_t* prompt_offsets, int32_t n_prompts, int32_t G);
 
-/* One tandem decode step for every unfinished sequence: forward the pending
- * token through both models (appending to both caches), sample y_t from the
- * owner, write (y_t, m_t, senior log-prob) to the output arenas, stop at EOS
- * or at t = max_new_tokens, apply the handoff rule.  If n_active is not NULL
- * the call synchronises and stores the number of unfinished sequences.
+/* One pass of Algorithm 1's rollout loop for every unfinished sequence:
+ * forward the pending token through both models (appending to both caches,
+ * Section 3.3), sample y_t from the owner a_t, write (y_t, m_t, senior
+ * log-prob log pi_sen(y_t | .) for Section 3.4's L_TRL) to the output arenas,
+ * stop at EOS or at t = max_new_tokens, apply the handoff block.  If
+ * n_active is not NULL the call synchronises and stores the number of
+ * unfinished sequences.  With an EOS token, every 32nd step first compacts
+ * the batch (unfinished sequences to the front): that step synchronises once
+ * to read the unfinished count.
  * The step's kernels are captured once per batch into a HIP graph (on the
  * first tandem_step after tandem_prefill, or after a timing-mode change)
  * and every step replays it: the per-step state lives in device memory, so
@@ -181,10 +204,12 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens,
  * objects and events owned by the handle. */
 tandem_status tandem_step(tandem_handle* h, int32_t* n_active);
 
-/* As tandem_step, but the appended token of sequence s is forced[s] (device
- * int32 [max_seqs]; entries < 0 keep the library's own sample).  The owner
- * rule and the outputs follow the appended token; dbg (may be NULL) receives
- * the library's own sample, its margin and the raw logits of this step. */
+/* As tandem_step (the same pass of Algorithm 1's loop, launched kernel by
+ * kernel), but the appended token of sequence s is forced[s] (device int32
+ * [max_seqs]; entries < 0 keep the library's own sample): teacher forcing.
+ * The owner rule and the outputs follow the appended token; dbg (may be
+ * NULL) receives the library's own sample, its margin and the raw logits of
+ * this step. */
 tandem_status tandem_step_forced(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg,
                                  int32_t* n_active);
 
@@ -260,9 +285,12 @@ tandem_status tandem_grpo_loss_noalloc(const tandem_grpo_cfg* cfg, const float* 
                                        float* advantages, float* grad, float* loss, int32_t* n_masked,
                                        void* stream);
 
-/* Copy the per-sequence sampler state to HOST int32 arrays of n_seqs
- * entries (any pointer may be NULL): owner (1 = senior), span counter c,
- * next step t, next position, done flag.  Synchronises the stream. */
+/* The per-request sampler state of the reproducibility appendix (current
+ * owner, span counter, step, position, finished), copied to HOST int32
+ * arrays of n_seqs entries (any pointer may be NULL): owner (1 = senior),
+ * span counter c, next step t, next position, done flag.  Synchronises the
+ * stream; reports a token-range error of the batch's prompts (see
+ * tandem_prefill). */
 tandem_status tandem_get_state(tandem_handle* h, int32_t* owner, int32_t* c, int32_t* t,
                                int32_t* pos, int32_t* done);
 
@@ -273,7 +301,8 @@ tandem_status tandem_get_state(tandem_handle* h, int32_t* owner, int32_t* c, int
  * launches may overlap the senior's); tandem_timing_read
  * synchronises and returns the summed device milliseconds and the number of
  * launches of one class since the last tandem_timing_enable.  Every call to
- * tandem_timing_enable resets the sums (mask 0 switches timing off).  Each
+ * tandem_timing_enable waits for the stream's queued work and resets the sums
+ * (mask 0 switches timing off).  Each
  * event pair adds a few microseconds of stream time.  While any class is
  * timed, tandem_step launches its kernels from the host instead of replaying
  * the step graph (event records inside a graph carry no launch times). */

@@ -524,7 +524,12 @@ __global__ void init_state_kernel(InitStateArgs a) {
   if (s >= a.n_seq) return;
   const int j = s / a.G;
   const int P = a.prompt_len[j];
-  a.pending[s] = a.prompt_tokens[a.prompt_end[j] - 1];
+  int tok = a.prompt_tokens[a.prompt_end[j] - 1];
+  if (tok < 0 || tok >= a.V) {
+    __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    tok = 0;
+  }
+  a.pending[s] = tok;
   a.pos[s] = P - 1;
   a.t[s] = 1;
   a.c[s] = 0;
@@ -615,9 +620,43 @@ __global__ void scatter_rows_kernel(const float* __restrict__ src, const int32_t
   for (int v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) dp[v] = sp[v];
 }
 
-__global__ void gather_i32_kernel(const int32_t* src, const int32_t* idx, int n, int32_t* dst) {
+// One workgroup per prompt of the chunk.
+__global__ __launch_bounds__(kNT) void prefill_rows_kernel(PrefillRowsArgs a) {
+  const int j = a.j0 + blockIdx.x;
+  const int P = a.prompt_len[j], start = a.prompt_end[j] - P;
+  const int rb = a.row_base[j], gb = a.grp_base[j];
+  bool bad = false;
+  for (int i = threadIdx.x; i < P - 1; i += kNT) {
+    const int r = rb + i;
+    int tok = a.prompt_tokens[start + i];
+    if (tok < 0 || tok >= a.V) {
+      bad = true;
+      tok = 0;
+    }
+    a.row_slot[r] = j * a.G;
+    a.row_pos[r] = i;
+    a.row_tok[r] = tok;
+    if ((i & 15) == 0) {
+      a.grp_row0[gb + (i >> 4)] = r;
+      a.grp_n[gb + (i >> 4)] = min(16, P - 1 - i);
+    }
+  }
+  if (bad) __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ void iota_kernel(int32_t* __restrict__ dst, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) dst[i] = src[idx[i]];
+  if (i < n) dst[i] = i;
+}
+
+__global__ void prefix_rows_kernel(const int32_t* __restrict__ act, int R, int G,
+                                   const int32_t* __restrict__ prompt_len, int32_t* __restrict__ row_lo,
+                                   int32_t* __restrict__ pfx_slot) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= R) return;
+  const int j = act[r] / G;
+  row_lo[r] = (prompt_len[j] - 1) / 16 * 16;
+  pfx_slot[r] = j * G;                        // slots follow sequence ids
 }
 
 }  // namespace
@@ -744,9 +783,23 @@ hipError_t launch_scatter_rows(const float* src, const int32_t* act, int R, int 
   return hipGetLastError();
 }
 
-hipError_t launch_gather_i32(const int32_t* src, const int32_t* idx, int n, int32_t* dst, hipStream_t st) {
+hipError_t launch_prefill_rows(const PrefillRowsArgs& a, hipStream_t st) {
+  if (a.n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(prefill_rows_kernel, dim3(a.n), dim3(kNT), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_iota(int32_t* dst, int n, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gather_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, st, src, idx, n, dst);
+  hipLaunchKernelGGL(iota_kernel, dim3((n + 255) / 256), dim3(256), 0, st, dst, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefix_rows(const int32_t* act, int R, int G, const int32_t* prompt_len, int32_t* row_lo,
+                              int32_t* pfx_slot, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(prefix_rows_kernel, dim3((R + 255) / 256), dim3(256), 0, st, act, R, G, prompt_len, row_lo,
+                     pfx_slot);
   return hipGetLastError();
 }
 

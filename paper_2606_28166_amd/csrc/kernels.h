@@ -215,15 +215,41 @@ hipError_t launch_kv_replicate(int dt, void* kc, void* vc, int n_layers, long la
                                long slot_stride, int nkv, int hd, int ctx_stride, int src,
                                int dst0, int n_dst, int p0, int n_pos, hipStream_t st);
 
-// Per-sequence state after prefill.
+// Per-sequence state after prefill.  The pending token (a prompt's last
+// token) is range-checked like the prompt rows (see PrefillRowsArgs).
 struct InitStateArgs {
-  int n_seq, G;
+  int n_seq, G, V;
   const int32_t* prompt_tokens; const int32_t* prompt_end;   // device [n_prompts] exclusive ends
   const int32_t* prompt_len;                                 // device [n_prompts]
   uint32_t key0, key1; unsigned long long thr; int first_owner;
   int32_t* owner; int32_t* c; int32_t* t; int32_t* pos; int32_t* pending; int32_t* done;
   int32_t* out_len;
+  int32_t* err;                                              // set to 1 when a token id is outside [0, V)
 };
+
+// Row tables of one prefill chunk, prompts j0 .. j0 + n - 1: prompt j's
+// P_j - 1 rows start at row_base[j] (chunk-relative) with slot j G,
+// positions 0 .. P_j - 2 and tokens prompt_tokens[end_j - P_j + i]; its
+// groups of 16 rows start at grp_base[j].  A token id outside [0, V) is
+// replaced by 0 (so every later read stays in bounds) and sets *err.
+struct PrefillRowsArgs {
+  int j0, n, G, V;
+  const int32_t* prompt_tokens;
+  const int32_t* prompt_end; const int32_t* prompt_len;      // device [n_prompts]
+  const int32_t* row_base; const int32_t* grp_base;          // device [n_prompts]
+  int32_t* row_slot; int32_t* row_pos; int32_t* row_tok; int32_t* grp_row0; int32_t* grp_n;
+  int32_t* err;
+};
+hipError_t launch_prefill_rows(const PrefillRowsArgs& a, hipStream_t st);
+
+// dst[i] = i for i < n.
+hipError_t launch_iota(int32_t* dst, int n, hipStream_t st);
+
+// Shared-prefix tables of decode rows 0 .. R-1: row r of sequence act[r]
+// (prompt j = act[r] / G) reads positions [0, lo) from slot j G, lo =
+// (P_j - 1) rounded down to 16.
+hipError_t launch_prefix_rows(const int32_t* act, int R, int G, const int32_t* prompt_len, int32_t* row_lo,
+                              int32_t* pfx_slot, hipStream_t st);
 hipError_t launch_init_state(const InitStateArgs& a, hipStream_t st);
 
 hipError_t launch_count_active(const int32_t* done, int n, int32_t* out, hipStream_t st);
@@ -244,8 +270,6 @@ hipError_t launch_gather_rows(const GatherRowsArgs& a, hipStream_t st);
 // dst[act[r]][0 .. V) = src[r][0 .. V) for rows 0 .. R-1 (debug logits by sequence).
 hipError_t launch_scatter_rows(const float* src, const int32_t* act, int R, int V, float* dst, hipStream_t st);
 
-// dst[i] = src[idx[i]]
-hipError_t launch_gather_i32(const int32_t* src, const int32_t* idx, int n, int32_t* dst, hipStream_t st);
 
 // true when the MFMA attention kernel covers this (dtype, head_dim, group size)
 bool attention_has_mfma(int dt, int hd, int gqa);

@@ -88,6 +88,7 @@ struct Plan {
   size_t kv_bytes;
   size_t off_state, off_seq_slot, off_rows, off_prompt, off_partials, off_count, off_act, off_drows;
   size_t off_pfx;             // shared-prefix tables of the decode rows (2 x max_seqs int32)
+  size_t off_err;             // the batch's token-range error flag (int32)
   size_t off_score;           // dual-distribution score partials [max_seqs][n_chunks][6]
   size_t scratch_bytes;
 };
@@ -215,8 +216,9 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
   const size_t S = (size_t)cap->max_seqs;
   P.off_state = sc; sc = align_up(sc + 6 * S * 4, kAlign);
   P.off_seq_slot = sc; sc = align_up(sc + S * 4, kAlign);
-  P.off_rows = sc; sc = align_up(sc + 6 * (size_t)cap->max_prefill_tokens * 4, kAlign);
-  P.off_prompt = sc; sc = align_up(sc + 2 * S * 4, kAlign);
+  P.off_rows = sc; sc = align_up(sc + 5 * (size_t)cap->max_prefill_tokens * 4, kAlign);
+  P.off_prompt = sc; sc = align_up(sc + 4 * S * 4, kAlign);
+  P.off_err = sc; sc = align_up(sc + 4, kAlign);
   P.off_partials = sc; sc = align_up(sc + S * P.n_chunks * 5 * 4, kAlign);
   P.off_count = sc; sc = align_up(sc + 4, kAlign);
   P.off_act = sc; sc = align_up(sc + S * 4, kAlign);
@@ -254,7 +256,7 @@ struct tandem_handle {
   int n_cu = 256;             // compute units of the device (split-K sizing)
   int32_t *owner, *c, *t, *pos, *pending, *done;
   int32_t* seq_slot;
-  int32_t *row_slot, *row_pos, *row_tok, *row_src;      // prompt rows
+  int32_t *row_slot, *row_pos, *row_tok;                // prompt rows of one prefill chunk
   int32_t *grp_row0, *grp_n;                            // their 16-row groups (attention)
   // Decode rows: row r carries sequence act[r].  After a prefill act is the
   // identity; with EOS on, a stable partition (unfinished first) runs every
@@ -272,20 +274,24 @@ struct tandem_handle {
   bool share = false;
   int32_t *row_lo, *pfx_slot;
   int G = 1;
-  std::vector<int32_t> lo_of_prompt;                 // host, per prompt
-  std::vector<int32_t> h_pfx, h_act;                 // host staging (kept until the next rebuild)
   int steps_since_compact = 0;
-  int32_t *p_end, *p_len;
+  int32_t *p_end, *p_len, *p_rbase, *p_gbase;         // per prompt (device)
+  // A prompt token id outside [0, vocab) sets this device flag (and is read
+  // as 0); it is reported at the next call that synchronises.
+  int32_t* d_err;
+  // Pinned host staging of the per-prompt table; the next prefill refills it
+  // only once the previous upload has left it (ev_stage).
+  int32_t* h_stage = nullptr;
+  hipEvent_t ev_stage = nullptr;
   float* partials;
   int32_t* d_count;
-  int32_t* h_count;           // pinned
+  int32_t* h_sync = nullptr;  // pinned: [0] a count read back, [1] the error flag
   int n_seq = 0;
   bool prefilled = false;
   bool stepped = false;       // a step has run since the last prefill (its logits are in place)
   float* score_part = nullptr;  // partials of tandem_score_step
   bool poisoned = false;
   std::string err = "no error";
-  std::vector<int32_t> hbuf;  // host staging of prefill metadata
   // instrumentation: event pairs per kernel class
   int timing = 0;             // class mask and flags
   std::vector<hipEvent_t> ev_pool;                   // eager launches
@@ -652,46 +658,51 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
   return TANDEM_OK;
 }
 
-// Shared-prefix tables of decode rows 0 .. R-1 in the act order act_host
-// (see tandem_handle::share), copied to the device on the handle's stream:
-// per row its prompt's lo and the slot of the prompt's first sequence.
-tandem_status upload_prefix_tables(tandem_handle* h, const int32_t* act_host, int R) {
-  const int S = h->cap.max_seqs, G = h->G;
-  std::vector<int32_t>& t = h->h_pfx;
-  t.assign(2 * (size_t)S, 0);
-  int32_t *lo = t.data(), *ps = lo + S;
-  for (int r = 0; r < R; ++r) {
-    const int j = act_host[r] / G;
-    lo[r] = h->lo_of_prompt[j];
-    ps[r] = j * G;                 // slots follow sequence ids
-  }
-  HIPCHK(hipMemcpyAsync(h->row_lo, t.data(), t.size() * 4, hipMemcpyHostToDevice, h->stream));
+// Shared-prefix tables of the launched decode rows in the current act order
+// (see tandem_handle::share), built on the device.
+tandem_status prefix_tables(tandem_handle* h) {
+  if (!h->share) return TANDEM_OK;
+  HIPCHK(launch_prefix_rows(h->act, h->R_launch, h->G, h->p_len, h->row_lo, h->pfx_slot, h->stream));
   return TANDEM_OK;
+}
+
+// After a synchronisation that read the error flag into h_sync[1]: a prompt
+// token id of the current batch was outside the vocabulary.
+tandem_status batch_error(tandem_handle* h) {
+  if (!h->h_sync[1]) return TANDEM_OK;
+  h->prefilled = false;
+  return fail(&h->err, TANDEM_E_ARG,
+              "a prompt token id passed to tandem_prefill was outside [0, vocab): the batch ran with token 0 in its "
+              "place and is void; prefill again");
+}
+
+// Read the batch's error flag along with a count already on its way to
+// h_sync[0], then synchronise the stream.
+tandem_status sync_read(tandem_handle* h, const int32_t* d_count) {
+  hipStream_t st = h->stream;
+  if (d_count) HIPCHK(hipMemcpyAsync(h->h_sync, d_count, 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipMemcpyAsync(h->h_sync + 1, h->d_err, 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipStreamSynchronize(st));
+  return batch_error(h);
 }
 
 // With EOS on, sequences finish at different steps: every kCompactEvery steps
 // partition the batch (unfinished sequences first, stable) and shrink the
-// launched row count.  One host synchronisation per compaction.
+// launched row count.  One host synchronisation per compaction (the launched
+// row count is a host value).
 tandem_status maybe_compact(tandem_handle* h) {
   if (h->smp.eos_id < 0 || ++h->steps_since_compact < kCompactEvery) return TANDEM_OK;
   h->steps_since_compact = 0;
-  hipStream_t st = h->stream;
-  HIPCHK(launch_compact(h->done, h->n_seq, h->act, h->d_count, st));
-  HIPCHK(hipMemcpyAsync(h->h_count, h->d_count, 4, hipMemcpyDeviceToHost, st));
-  HIPCHK(hipStreamSynchronize(st));
-  const int n_act = *h->h_count;
+  HIPCHK(launch_compact(h->done, h->n_seq, h->act, h->d_count, h->stream));
+  CALL(sync_read(h, h->d_count));
+  const int n_act = h->h_sync[0];
   int R = (std::max(n_act, 1) + kCompactBucket - 1) / kCompactBucket * kCompactBucket;
   if (R > h->n_seq) R = h->n_seq;
   if (R < h->R_launch) {
     h->R_launch = R;
     drop_graphs(h);                   // captured for the old row count
   }
-  if (h->share) {                     // the act order changed: new prefix tables (same launch bounds)
-    h->h_act.resize((size_t)h->n_seq);
-    HIPCHK(hipMemcpy(h->h_act.data(), h->act, (size_t)h->n_seq * 4, hipMemcpyDeviceToHost));
-    CALL(upload_prefix_tables(h, h->h_act.data(), h->R_launch));
-  }
-  return TANDEM_OK;
+  return prefix_tables(h);            // the act order changed
 }
 
 // Capture the step into h->graph (the streams return to normal operation
@@ -751,9 +762,8 @@ tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_de
   h->stepped = true;
   if (n_active) {
     HIPCHK(launch_count_active(h->done, h->n_seq, h->d_count, st));
-    HIPCHK(hipMemcpyAsync(h->h_count, h->d_count, 4, hipMemcpyDeviceToHost, st));
-    HIPCHK(hipStreamSynchronize(st));
-    *n_active = *h->h_count;
+    CALL(sync_read(h, h->d_count));
+    *n_active = h->h_sync[0];
   }
   return TANDEM_OK;
 }
@@ -911,10 +921,11 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   h->seq_slot = (int32_t*)(sc + P.off_seq_slot);
   int32_t* rows = (int32_t*)(sc + P.off_rows);
   const size_t PT = (size_t)cap->max_prefill_tokens;
-  h->row_slot = rows; h->row_pos = rows + PT; h->row_tok = rows + 2 * PT; h->row_src = rows + 3 * PT;
-  h->grp_row0 = rows + 4 * PT; h->grp_n = rows + 5 * PT;
+  h->row_slot = rows; h->row_pos = rows + PT; h->row_tok = rows + 2 * PT;
+  h->grp_row0 = rows + 3 * PT; h->grp_n = rows + 4 * PT;
   int32_t* pr = (int32_t*)(sc + P.off_prompt);
-  h->p_end = pr; h->p_len = pr + S;
+  h->p_end = pr; h->p_len = pr + S; h->p_rbase = pr + 2 * S; h->p_gbase = pr + 3 * S;
+  h->d_err = (int32_t*)(sc + P.off_err);
   h->partials = (float*)(sc + P.off_partials);
   h->d_count = (int32_t*)(sc + P.off_count);
   h->act = (int32_t*)(sc + P.off_act);
@@ -923,12 +934,13 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   h->score_part = (float*)(sc + P.off_score);
   int32_t* pfx = (int32_t*)(sc + P.off_pfx);
   h->row_lo = pfx; h->pfx_slot = pfx + S;
-  h->h_count = nullptr;
 
   // --- HIP work from here on
   auto bail = [&](hipError_t e, const char* what) {
     std::string msg = std::string("HIP error in tandem_init (") + what + "): " + hipGetErrorString(e);
-    if (h->h_count) (void)hipHostFree(h->h_count);
+    if (h->h_sync) (void)hipHostFree(h->h_sync);
+    if (h->h_stage) (void)hipHostFree(h->h_stage);
+    if (h->ev_stage) (void)hipEventDestroy(h->ev_stage);
     for (int i = 0; i < 2; ++i)
       for (hipEvent_t ev : h->ev_att[i]) (void)hipEventDestroy(ev);
     if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
@@ -940,8 +952,12 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     delete h;
     return fail(nullptr, TANDEM_E_HIP, msg);
   };
-  hipError_t e = hipHostMalloc((void**)&h->h_count, 4, hipHostMallocDefault);
-  if (e != hipSuccess) { h->h_count = nullptr; return bail(e, "hipHostMalloc"); }
+  hipError_t e = hipHostMalloc((void**)&h->h_sync, 8, hipHostMallocDefault);
+  if (e != hipSuccess) { h->h_sync = nullptr; return bail(e, "hipHostMalloc"); }
+  e = hipHostMalloc((void**)&h->h_stage, 4 * S * 4, hipHostMallocDefault);
+  if (e != hipSuccess) { h->h_stage = nullptr; return bail(e, "hipHostMalloc"); }
+  e = hipEventCreateWithFlags(&h->ev_stage, hipEventDisableTiming);
+  if (e != hipSuccess) { h->ev_stage = nullptr; return bail(e, "staging event"); }
   {
     int dev = 0, ncu = 0;
     e = hipGetDevice(&dev);
@@ -1005,14 +1021,11 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
     if (e == hipSuccess) e = pack(m.lm_head, c.vocab, c.d_model, 0, m.lm16, &m.p_lm);
     if (e != hipSuccess) return bail(e, "weight packing");
   }
-  std::vector<int32_t> ident(S);
-  for (size_t i = 0; i < S; ++i) ident[i] = (int32_t)i;
-  e = hipMemcpyAsync(h->seq_slot, ident.data(), S * 4, hipMemcpyHostToDevice, h->stream);
+  e = launch_iota(h->seq_slot, (int)S, h->stream);       // slots follow sequence ids
   if (e != hipSuccess) return bail(e, "seq slots");
   e = hipMemsetAsync(stt, 0, 6 * S * 4, h->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(h->d_err, 0, 4, h->stream);
   if (e != hipSuccess) return bail(e, "state");
-  e = hipStreamSynchronize(h->stream);
-  if (e != hipSuccess) return bail(e, "synchronize");
   *out_handle = h;
   return TANDEM_OK;
 }
@@ -1038,107 +1051,92 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
   h->prefilled = false;
   drop_graphs(h);      // a new batch: the step graph is captured again on demand
   const int n_seq = n_prompts * G;
-  {
-    // token ids index the embedding tables: check them on the host before any kernel reads them
-    std::vector<int32_t> toks((size_t)prompt_offsets[n_prompts]);
-    HIPCHK(hipStreamSynchronize(st));
-    HIPCHK(hipMemcpy(toks.data(), prompt_tokens, toks.size() * 4, hipMemcpyDeviceToHost));
-    const int V = h->m[0].cfg.vocab;
-    for (int32_t tk : toks)
-      if (tk < 0 || tk >= V) return fail(&h->err, TANDEM_E_ARG, "prefill: a prompt token id is outside [0, vocab)");
-  }
-  // prompt metadata
-  h->hbuf.assign(2 * (size_t)n_prompts, 0);
-  for (int j = 0; j < n_prompts; ++j) {
-    h->hbuf[j] = prompt_offsets[j + 1];
-    h->hbuf[n_prompts + j] = prompt_offsets[j + 1] - prompt_offsets[j];
-  }
-  HIPCHK(hipMemcpyAsync(h->p_end, h->hbuf.data(), (size_t)n_prompts * 4, hipMemcpyHostToDevice, st));
-  HIPCHK(hipMemcpyAsync(h->p_len, h->hbuf.data() + n_prompts, (size_t)n_prompts * 4, hipMemcpyHostToDevice, st));
-  HIPCHK(hipStreamSynchronize(st));
   // the G sequences of a prompt share its prefix in decode attention when
   // both models' attention kernels can (otherwise every slot gets a copy)
-  {
-    bool share = G > 1;
-    for (int i = 0; i < 2; ++i) {
-      const tandem_model_cfg& c = h->m[i].cfg;
-      share = share && attention_shares_prefix(c.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32, c.head_dim,
-                                               c.n_q_heads / c.n_kv_heads);
-    }
-    h->share = share;
-    h->G = G;
-    h->lo_of_prompt.assign((size_t)n_prompts, 0);
-    if (share)
-      for (int j = 0; j < n_prompts; ++j) h->lo_of_prompt[j] = (prompt_offsets[j + 1] - prompt_offsets[j] - 1) / 16 * 16;
+  bool share = G > 1;
+  for (int i = 0; i < 2; ++i) {
+    const tandem_model_cfg& c = h->m[i].cfg;
+    share = share && attention_shares_prefix(c.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32, c.head_dim,
+                                             c.n_q_heads / c.n_kv_heads);
   }
-  // chunks of whole prompts whose (P - 1) rows fit max_prefill_tokens
-  int j0 = 0;
-  std::vector<int32_t> rows;
-  while (j0 < n_prompts) {
-    int j1 = j0, nr = 0;
-    while (j1 < n_prompts) {
-      const int add = prompt_offsets[j1 + 1] - prompt_offsets[j1] - 1;
-      if (nr + add > h->cap.max_prefill_tokens) break;
-      nr += add;
-      ++j1;
+  h->share = share;
+  h->G = G;
+  // per-prompt table (exclusive end, length, first row and first 16-row group
+  // within its chunk of whole prompts whose rows fit max_prefill_tokens),
+  // uploaded once from pinned staging; the staging is refilled only after the
+  // previous prefill's upload has left it
+  std::vector<std::pair<int, int>> chunks;           // [j0, j1) per chunk
+  HIPCHK(hipEventSynchronize(h->ev_stage));
+  {
+    int32_t* t = h->h_stage;
+    int j0 = 0, nr = 0, ng = 0;
+    for (int j = 0; j < n_prompts; ++j) {
+      const int rows = prompt_offsets[j + 1] - prompt_offsets[j] - 1;
+      if (nr + rows > h->cap.max_prefill_tokens) {
+        chunks.push_back({j0, j});
+        j0 = j;
+        nr = ng = 0;
+      }
+      t[j] = prompt_offsets[j + 1];
+      t[n_prompts + j] = rows + 1;
+      t[2 * n_prompts + j] = nr;
+      t[3 * n_prompts + j] = ng;
+      nr += rows;
+      ng += (rows + 15) / 16;
     }
-    if (nr > 0) {
-      rows.assign(5 * (size_t)nr, 0);
-      int r = 0, ng = 0;
-      for (int j = j0; j < j1; ++j) {
-        const int P = prompt_offsets[j + 1] - prompt_offsets[j];
-        for (int i = 0; i < P - 1; ++i, ++r) {
-          rows[r] = j * G;                            // slot of the prompt's first sequence
-          rows[nr + r] = i;                           // position
-          rows[2 * nr + r] = prompt_offsets[j] + i;   // source token index
-          if (i % 16 == 0) {                          // groups of 16 rows within the prompt
-            rows[3 * nr + ng] = r;
-            rows[4 * nr + ng] = std::min(16, P - 1 - i);
-            ++ng;
-          }
-        }
-      }
-      HIPCHK(hipMemcpyAsync(h->row_slot, rows.data(), (size_t)nr * 4, hipMemcpyHostToDevice, st));
-      HIPCHK(hipMemcpyAsync(h->row_pos, rows.data() + nr, (size_t)nr * 4, hipMemcpyHostToDevice, st));
-      HIPCHK(hipMemcpyAsync(h->row_src, rows.data() + 2 * nr, (size_t)nr * 4, hipMemcpyHostToDevice, st));
-      HIPCHK(hipMemcpyAsync(h->grp_row0, rows.data() + 3 * nr, (size_t)ng * 4, hipMemcpyHostToDevice, st));
-      HIPCHK(hipMemcpyAsync(h->grp_n, rows.data() + 4 * nr, (size_t)ng * 4, hipMemcpyHostToDevice, st));
-      TIMED(TANDEM_K_OTHER, launch_gather_i32(prompt_tokens, h->row_src, nr, h->row_tok, st));
-      {
-        FwdRows fr{nr, h->row_tok, h->row_slot, h->row_pos, nullptr};
-        fr.grp_row0 = h->grp_row0; fr.grp_n = h->grp_n; fr.n_groups = ng;
-        tandem_status s = forward_pair(h, fr, false);
-        if (s != TANDEM_OK) return s;
-      }
-      for (int j = j0; j < j1; ++j) {
-        const int P = prompt_offsets[j + 1] - prompt_offsets[j];
-        if (P - 1 <= 0 || G <= 1) continue;
-        for (int i = 0; i < 2; ++i) {
-          Model& m = h->m[i];
-          TIMED(TANDEM_K_OTHER, launch_kv_replicate(m.cfg.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32, m.kc, m.vc,
-                                     m.cfg.n_layers, m.layer_stride, m.slot_stride, m.cfg.n_kv_heads,
-                                     m.cfg.head_dim, h->plan.ctx_stride, j * G, j * G + 1, G - 1,
-                                     h->lo_of_prompt[j], P - 1, st));
-        }
-      }
-      HIPCHK(hipStreamSynchronize(st));   // the host row arrays are reused by the next chunk
+    chunks.push_back({j0, n_prompts});
+  }
+  HIPCHK(hipMemsetAsync(h->d_err, 0, 4, st));
+  HIPCHK(hipMemcpyAsync(h->p_end, h->h_stage, (size_t)n_prompts * 4, hipMemcpyHostToDevice, st));
+  HIPCHK(hipMemcpyAsync(h->p_len, h->h_stage + n_prompts, (size_t)n_prompts * 4, hipMemcpyHostToDevice, st));
+  HIPCHK(hipMemcpyAsync(h->p_rbase, h->h_stage + 2 * n_prompts, (size_t)n_prompts * 4, hipMemcpyHostToDevice, st));
+  HIPCHK(hipMemcpyAsync(h->p_gbase, h->h_stage + 3 * n_prompts, (size_t)n_prompts * 4, hipMemcpyHostToDevice, st));
+  HIPCHK(hipEventRecord(h->ev_stage, st));
+  for (const auto& ch : chunks) {
+    const int j0 = ch.first, j1 = ch.second;
+    int nr = 0, ng = 0;
+    for (int j = j0; j < j1; ++j) {
+      const int rows = prompt_offsets[j + 1] - prompt_offsets[j] - 1;
+      nr += rows;
+      ng += (rows + 15) / 16;
     }
-    j0 = j1;
+    if (nr == 0) continue;
+    PrefillRowsArgs pa{};
+    pa.j0 = j0; pa.n = j1 - j0; pa.G = G; pa.V = h->m[0].cfg.vocab;
+    pa.prompt_tokens = prompt_tokens; pa.prompt_end = h->p_end; pa.prompt_len = h->p_len;
+    pa.row_base = h->p_rbase; pa.grp_base = h->p_gbase;
+    pa.row_slot = h->row_slot; pa.row_pos = h->row_pos; pa.row_tok = h->row_tok;
+    pa.grp_row0 = h->grp_row0; pa.grp_n = h->grp_n; pa.err = h->d_err;
+    TIMED(TANDEM_K_OTHER, launch_prefill_rows(pa, st));
+    {
+      FwdRows fr{nr, h->row_tok, h->row_slot, h->row_pos, nullptr};
+      fr.grp_row0 = h->grp_row0; fr.grp_n = h->grp_n; fr.n_groups = ng;
+      tandem_status s = forward_pair(h, fr, false);
+      if (s != TANDEM_OK) return s;
+    }
+    for (int j = j0; j < j1; ++j) {
+      const int P = prompt_offsets[j + 1] - prompt_offsets[j];
+      if (P - 1 <= 0 || G <= 1) continue;
+      const int lo = share ? (P - 1) / 16 * 16 : 0;    // shared positions stay in the first slot only
+      for (int i = 0; i < 2; ++i) {
+        Model& m = h->m[i];
+        TIMED(TANDEM_K_OTHER, launch_kv_replicate(m.cfg.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32, m.kc, m.vc,
+                                   m.cfg.n_layers, m.layer_stride, m.slot_stride, m.cfg.n_kv_heads,
+                                   m.cfg.head_dim, h->plan.ctx_stride, j * G, j * G + 1, G - 1, lo, P - 1, st));
+      }
+    }
   }
   InitStateArgs is{};
-  is.n_seq = n_seq; is.G = G; is.prompt_tokens = prompt_tokens; is.prompt_end = h->p_end; is.prompt_len = h->p_len;
+  is.n_seq = n_seq; is.G = G; is.V = h->m[0].cfg.vocab;
+  is.prompt_tokens = prompt_tokens; is.prompt_end = h->p_end; is.prompt_len = h->p_len;
   is.key0 = h->key0; is.key1 = h->key1; is.thr = h->thr; is.first_owner = h->sw.first_owner;
   is.owner = h->owner; is.c = h->c; is.t = h->t; is.pos = h->pos; is.pending = h->pending; is.done = h->done;
-  is.out_len = h->out.length;
+  is.out_len = h->out.length; is.err = h->d_err;
   HIPCHK(launch_init_state(is, st));
   HIPCHK(hipMemcpyAsync(h->act, h->seq_slot, (size_t)n_seq * 4, hipMemcpyDeviceToDevice, st));   // identity
   h->n_seq = n_seq;
   h->R_launch = n_seq;
-  if (h->share) {
-    h->h_act.resize((size_t)n_seq);
-    for (int s = 0; s < n_seq; ++s) h->h_act[s] = s;
-    CALL(upload_prefix_tables(h, h->h_act.data(), n_seq));
-  }
+  CALL(prefix_tables(h));
   h->steps_since_compact = 0;
   h->prefilled = true;
   h->stepped = false;
@@ -1178,7 +1176,7 @@ tandem_status tandem_get_state(tandem_handle* h, int32_t* owner, int32_t* c, int
   if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
   if (!h->prefilled) return fail(&h->err, TANDEM_E_STATE, "tandem_get_state before tandem_prefill");
   const size_t n = (size_t)h->n_seq * 4;
-  HIPCHK(hipStreamSynchronize(h->stream));
+  CALL(sync_read(h, nullptr));
   if (owner) HIPCHK(hipMemcpy(owner, h->owner, n, hipMemcpyDeviceToHost));
   if (c) HIPCHK(hipMemcpy(c, h->c, n, hipMemcpyDeviceToHost));
   if (t) HIPCHK(hipMemcpy(t, h->t, n, hipMemcpyDeviceToHost));
@@ -1227,7 +1225,9 @@ void tandem_destroy(tandem_handle* h) {
   if (h->ev_in) (void)hipEventDestroy(h->ev_in);
   if (h->ev_out) (void)hipEventDestroy(h->ev_out);
   if (h->gstream) (void)hipStreamDestroy(h->gstream);
-  if (h->h_count) (void)hipHostFree(h->h_count);
+  if (h->h_sync) (void)hipHostFree(h->h_sync);
+  if (h->h_stage) (void)hipHostFree(h->h_stage);
+  if (h->ev_stage) (void)hipEventDestroy(h->ev_stage);
   delete h;
 }
 

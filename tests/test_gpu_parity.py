@@ -216,13 +216,28 @@ def test_error_paths_on_device():
         eng.prefill([np.arange(40, dtype=np.int32)], 1)          # prompt longer than max_ctx allows
     assert e.value.status == L.E_CAPACITY
     with pytest.raises(L.TandemError) as e:
-        eng.prefill([np.array([1, 2, 9999], dtype=np.int32)], 1)  # token id outside the vocabulary
-    assert e.value.status == L.E_ARG
-    with pytest.raises(L.TandemError) as e:
         eng.prefill(prompts, wl.group + 1)                         # more sequences than max_seqs
     assert e.value.status == L.E_CAPACITY
-    eng.prefill(prompts, wl.group)
+    # token ids are checked on the device: the prefill is queued, the id is
+    # read as 0, and the next synchronising call reports the void batch
+    eng.prefill([np.array([1, 2, 9999], dtype=np.int32), np.array([-3], dtype=np.int32)], 2)
     eng.step()
+    with pytest.raises(L.TandemError) as e:
+        eng.state()
+    assert e.value.status == L.E_ARG
+    with pytest.raises(L.TandemError) as e:
+        eng.step()
+    assert e.value.status == L.E_STATE
+    # the last prompt token alone out of range (the first pending token)
+    eng.prefill([np.array([4, 5, 512], dtype=np.int32)], 1)
+    with pytest.raises(L.TandemError) as e:
+        eng.step(want_active=True)
+    assert e.value.status == L.E_ARG
+    # a valid batch afterwards runs and matches a fresh handle
+    eng.prefill(prompts, wl.group)
+    for _ in range(4):
+        eng.step()
+    assert eng.step(want_active=True) == wl.n_seqs
     eng.close()
 
 
@@ -273,3 +288,81 @@ def test_eos_compaction_shrinks_the_batch():
     # by step 64 (the second compaction) fewer than 64 sequences are alive
     assert (p.ref.length > 64).sum() < 64
     P.check(p, P.TOL_BF16)
+
+
+@pytest.mark.parametrize("name,switch", [
+    ("ALTERNATE at a 20% boundary set, no cap", W.SwitchSettings(W.ALTERNATE, 0.5, -1, "random:0.2", W.SENIOR)),
+    ("ALTERNATE with a span cap of 4, junior first", W.SwitchSettings(W.ALTERNATE, 0.5, 4, "random:0.05", W.JUNIOR)),
+    ("SWITCH p=0 per token (solo senior)", W.SwitchSettings(W.SWITCH, 0.0, -1, "all", W.SENIOR)),
+    ("SWITCH p=1 per token (strict alternation)", W.SwitchSettings(W.SWITCH, 1.0, -1, "all", W.SENIOR)),
+    ("REDRAW p=0.3, junior first, 35% boundary set, K=5", W.SwitchSettings(W.REDRAW, 0.3, 5, "random:0.351", W.JUNIOR)),
+    ("REDRAW p=1 drawn first owner (solo senior)", W.SwitchSettings(W.REDRAW, 1.0, 2, "random:0.351", W.DRAW)),
+    ("REDRAW p=0 drawn first owner (solo junior)", W.SwitchSettings(W.REDRAW, 0.0, 2, "random:0.351", W.DRAW)),
+])
+def test_handoff_branches(name, switch):
+    """Every branch of the handoff block on the GPU: the ALTERNATE flip (with
+    and without the span cap), the coin thresholds 0 and 2^32 (p = 0 and
+    p = 1), the junior as first owner, and the drawn first owner at p in
+    {0, 1}; owner masks, decision state and tokens bit-exact."""
+    P.log(f"case handoff branch: {name} (tiny bf16)")
+    wl = _tiny("bf16")
+    wl.switch = switch
+    p = P.run(wl, logits_at=(7,))
+    P.check(p, P.TOL_BF16)
+    own = p.ref.owner
+    if switch.mode == W.SWITCH and switch.p == 0.0:
+        assert own.all()
+    elif switch.mode == W.SWITCH and switch.p == 1.0:
+        assert (own[:, 1:] != own[:, :-1]).all()
+    elif switch.mode == W.REDRAW and switch.p in (0.0, 1.0):
+        assert (own == int(switch.p)).all()
+    elif switch.mode == W.ALTERNATE:
+        assert p.ref.decided.sum() > 0
+        if switch.first_owner == W.JUNIOR:
+            assert (own[:, 0] == 0).all()
+
+
+@pytest.mark.parametrize("schedule", ["alternate", "stepcoin"])
+def test_reasoning_step_schedules_at_qwen_shapes(schedule):
+    """The evaluation schedules: the owner flips at every reasoning-step
+    boundary (deterministic round-robin) or is redrawn there by a fair coin,
+    with no span cap and T = 0.6, on a sparse synthetic step-boundary set
+    (Qwen shapes, 2+2 layers, 64 steps)."""
+    wl_ref = W.workload("qwen-eval-" + schedule)
+    P.log(f"case reasoning-step schedule {schedule} at Qwen shapes, 2+2 layers, 64 steps")
+    wl = _qwen_reduced()
+    wl.switch, wl.sample.temperature = wl_ref.switch, wl_ref.sample.temperature
+    wl.switch.boundary = "random:0.1"          # denser than the workload's, so 64 steps cross several steps
+    wl.sample.max_new = 64
+    p = P.run(wl, logits_at=(1, 64))
+    P.check(p, P.TOL_BF16)
+    assert p.ref.decided.sum() > 0 and 0 < p.ref.owner.mean() < 1
+
+
+def test_graph_replays_with_compaction_match_oracle_fp32():
+    """Free-running steps replayed from the step graph, with EOS ending most
+    sequences so that compaction shrinks the launched rows and the graph is
+    captured again: the stream equals eager launches bit for bit, and equals
+    the free-running oracle (fp32 models: up to each row's first step whose
+    Gumbel margin is inside the float32 band)."""
+    from paper_2606_28166_amd.engine import TandemEngine
+    from oracle.rollout import rollout, build_models
+    P.log("case graph replays across compactions vs oracle: tiny fp32, 3 prompts x G=32, EOS")
+    wl = _tiny("f32")
+    wl.n_prompts, wl.group = 3, 32
+    wl.sample.max_new = 80
+    wl.sample.eos_id, wl.sample.eos_bias_senior, wl.sample.eos_bias_junior = 7, 3.0, 2.5
+    ws, wj, prompts, bnd = W.make_all(wl)
+    sen, jun = build_models(wl, ws, wj)
+    ref = rollout(sen, jun, prompts, wl.group, wl.switch, wl.sample, wl.philox_seed, bnd)
+    assert (ref.length < 32).sum() >= 32 and (ref.length > 64).sum() > 0, "compaction must shrink the batch"
+    eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed,
+                       max_seqs=wl.n_seqs, max_ctx=wl.prompt_len - 1 + wl.sample.max_new)
+    graph = P.free_run(eng, prompts, wl.group, wl.sample.max_new, eager=False)
+    eager = P.free_run(eng, prompts, wl.group, wl.sample.max_new, eager=True)
+    eng.close()
+    for k in graph:
+        np.testing.assert_array_equal(graph[k], eager[k], err_msg=k)
+    first, full, n = P.first_divergence(graph, ref, np.arange(wl.n_seqs), wl.sample.max_new, band=1e-4)
+    P.log(f"  {full}/{wl.n_seqs} rows identical to the oracle, {n} tokens compared, first divergence {first}")
+    assert full >= wl.n_seqs - 2
