@@ -74,6 +74,13 @@ DESCRIPTIONS = {
                   "35% boundary bitmap",
     "self-paired": "Qwen3-4B-shaped senior + Qwen3-4B-shaped junior, bf16, 16 prompts x G=8, prompt 256, 3000 new "
                    "tokens, the paper's schedule (REDRAW p=0.5, K=32, drawn first owner, T=0.6, 35% boundary bitmap)",
+    "qwen-eval-alternate": "Qwen3-4B-shaped senior + Qwen3-0.6B-shaped junior, bf16, 16 prompts x G=8, prompt 256, "
+                           "2048 new tokens, the evaluation schedule: owner flips at every reasoning-step boundary "
+                           "(1/48-density synthetic boundary set), senior first, no cap, T=0.6",
+    "qwen-eval-stepcoin": "Qwen3-4B-shaped senior + Qwen3-0.6B-shaped junior, bf16, 16 prompts x G=8, prompt 256, "
+                          "2048 new tokens, the stochastic evaluation schedule: fair-coin redraw at every "
+                          "reasoning-step boundary (1/48-density synthetic boundary set), drawn first owner, no cap, "
+                          "T=0.6",
 }
 
 

@@ -51,7 +51,7 @@ def rollout(sen: OracleModel, jun: OracleModel, prompts: Sequence[np.ndarray], G
             switch, sample, seed: int, boundary: Optional[np.ndarray] = None,
             forced: Optional[np.ndarray] = None, keep_logits_at: Sequence[int] = (),
             seq_subset: Optional[Sequence[int]] = None, max_steps: Optional[int] = None,
-            start_state=None, progress=None) -> RolloutResult:
+            progress=None) -> RolloutResult:
     """Run the tandem rollout.
 
     switch: workloads.SwitchSettings; sample: workloads.SampleSettings.

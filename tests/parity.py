@@ -57,9 +57,10 @@ def log(msg: str) -> None:
 
 def run(wl: W.Workload, steps: Optional[int] = None, logits_at: Sequence[int] = (1,),
         max_prefill_tokens: int = 4096, seq_subset: Optional[Sequence[int]] = None,
-        weights=None, before=None) -> Parity:
+        weights=None, before=None, after=None) -> Parity:
     """before: called with the engine before this batch's prefill (earlier use of
-    the same handle)."""
+    the same handle); after: called with (engine, prompts, oracle result)
+    once the teacher-forced steps are read, before the engine is closed."""
     from paper_2606_28166_amd.engine import TandemEngine
     steps = steps or wl.sample.max_new
     ws, wj, prompts, bnd = weights if weights is not None else W.make_all(wl)
@@ -99,8 +100,50 @@ def run(wl: W.Workload, steps: Optional[int] = None, logits_at: Sequence[int] = 
     out = {k: v[rows] for k, v in out.items()}
     st = eng.state()
     st = {k: v[rows] for k, v in st.items()}
+    if after is not None:
+        after(eng, prompts, ref)
     eng.close()
     return Parity(ref, out, sampled, margin, logits, st, steps, rows)
+
+
+def free_run(eng, prompts, G: int, steps: int, eager: bool) -> Dict[str, np.ndarray]:
+    """Prefill and `steps` free-running tandem_step calls on an engine, replayed
+    from the step graph (eager=False) or launched kernel by kernel."""
+    from paper_2606_28166_amd import _lib as L
+    eng.timing(L.TIMING_EAGER if eager else 0)
+    eng.prefill(prompts, G)
+    for _ in range(steps):
+        eng.step()
+    out = eng.outputs()
+    eng.timing(0)
+    return out
+
+
+def first_divergence(gpu: Dict[str, np.ndarray], ref, rows: np.ndarray, steps: int, band: float = MARGIN):
+    """Free-running GPU stream against the free-running oracle, per checked
+    row: the tokens must agree before the row's first step whose oracle Gumbel
+    margin is inside `band` (at that step either token is a correct sample,
+    and the two streams may part), the owner bits through that step (they
+    depend on the earlier tokens only), and rows without such a step must
+    agree in full, length included.  Returns (first divergence step or None,
+    rows compared in full, tokens compared)."""
+    first, full, n = None, 0, 0
+    for i, s in enumerate(rows):
+        L = min(steps, int(ref.length[i]))
+        inband = np.nonzero(ref.margin[i, :L] <= band)[0]
+        upto = int(inband[0]) if inband.size else L
+        np.testing.assert_array_equal(gpu["tokens"][s, :upto], ref.tokens[i, :upto], err_msg=f"row {s}")
+        np.testing.assert_array_equal(gpu["owner"][s, :min(upto + 1, L)], ref.owner[i, :min(upto + 1, L)],
+                                      err_msg=f"row {s}")
+        diff = np.nonzero(gpu["tokens"][s, :L] != ref.tokens[i, :L])[0]
+        if diff.size:
+            first = int(diff[0]) + 1 if first is None else min(first, int(diff[0]) + 1)
+        else:
+            full += 1
+        if not inband.size:
+            assert min(steps, int(gpu["length"][s])) == L, f"row {s}: length"
+        n += upto
+    return first, full, n
 
 
 def check(p: Parity, tol: float) -> None:

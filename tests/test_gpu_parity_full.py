@@ -5,6 +5,7 @@ only on the weights, its prompt, the seed and its id, so a subset is exact);
 the library runs the whole batch with the benchmark's capacity, the other
 sequences sampling freely next to the checked ones.
 """
+import numpy as np
 import pytest
 
 import workloads as W
@@ -14,10 +15,49 @@ pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 
 def test_qwen_full_size_prompt0_first_64_steps():
+    """Teacher-forced steps at the full Qwen shapes, then, on the same handle,
+    64 free-running steps replayed from the captured step graph: bit-equal to
+    the same steps launched eagerly, and equal to the free-running oracle on
+    prompt 0's rows up to each row's first in-band step (the first free-running
+    divergence is reported)."""
     wl = W.workload("qwen")
     P.log("case qwen full size: 36 + 28 layers, V 151936, 128 rows, capacity 2303 positions; "
           "prompt 0's 8 rows, 64 steps")
-    p = P.run(wl, steps=64, logits_at=(1, 32, 64), seq_subset=list(range(wl.group)))
+    rows = list(range(wl.group))
+    seen = {}
+
+    def free(eng, prompts, ref):
+        graph = P.free_run(eng, prompts, wl.group, 64, eager=False)
+        eager = P.free_run(eng, prompts, wl.group, 64, eager=True)
+        for k in graph:
+            np.testing.assert_array_equal(graph[k], eager[k], err_msg=k)
+        seen["div"] = P.first_divergence(graph, ref, np.array(rows), 64)
+
+    p = P.run(wl, steps=64, logits_at=(1, 32, 64), seq_subset=rows, after=free)
+    P.check(p, P.TOL_BF16)
+    first, full, n = seen["div"]
+    P.log(f"  free-running graph replays: {full}/{len(rows)} rows identical to the oracle over 64 steps, "
+          f"{n} tokens compared, first divergence at step {first}")
+
+
+def test_small_full_size_prompt0_all_512_steps():
+    """The small pair at its full shape (8 + 4 layers, V 32000) over the whole
+    64-row batch and all 512 steps; the oracle follows prompt 0's 8 rows."""
+    wl = W.workload("small")
+    P.log("case small full size: 8 + 4 layers, V 32000, 64 rows, 512 steps; prompt 0's 8 rows")
+    p = P.run(wl, logits_at=(1, 256, 512), seq_subset=list(range(wl.group)))
+    P.check(p, P.TOL_BF16)
+
+
+def test_qwen_shapes_context_beyond_2048_positions():
+    """Contexts past 2048 positions: one 2040-token prompt x G = 4 at the Qwen
+    shapes (2+2 layers), 24 decode steps (positions 2039 .. 2062), logits
+    checked at the first and the last step."""
+    wl = W.workload("qwen").replace(n_prompts=1, group=4, prompt_len=2040, gain_jitter=0.05)
+    wl.senior.n_layers, wl.junior.n_layers = 2, 2
+    wl.sample.max_new = 24
+    P.log("case long context: Qwen shapes 2+2 layers, prompt 2040 tokens, G=4, 24 steps")
+    p = P.run(wl, logits_at=(1, 24))
     P.check(p, P.TOL_BF16)
 
 

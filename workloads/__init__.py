@@ -18,6 +18,9 @@ Shapes are the five workloads of the hot-path scope:
   qwen    Qwen3-4B-shaped senior + Qwen3-0.6B-shaped junior, bf16, V=151936
   longcot small shapes, ragged prompts, EOS, 32-token ownership chunks
   wide    small shapes, 1024 concurrent sequences
+plus the paper's own schedules on these shapes: its training schedule
+(paper, qwen-paper, self-paired) and its evaluation schedules at
+reasoning-step boundaries (qwen-eval-alternate, qwen-eval-stepcoin).
 """
 from __future__ import annotations
 
@@ -162,10 +165,24 @@ def workload(name: str) -> Workload:
         w = workload("qwen-paper")
         return w.replace(name="self-paired", junior=copy.deepcopy(w.senior),
                          sample=SampleSettings(0.6, -1, 0.0, 0.0, 3000), seed_base=8)
+    if name in ("qwen-eval-alternate", "qwen-eval-stepcoin"):
+        # The paper's evaluation schedules at inference (T = 0.6): the owner
+        # flips at every reasoning-step boundary (deterministic round-robin,
+        # senior first), or a fair coin redraws it there (drawn first owner);
+        # no span cap.  The step boundary is a sparse synthetic token set of
+        # density 1/48 (reasoning steps of about 48 tokens on average).
+        w = workload("qwen")
+        if name.endswith("alternate"):
+            sw = SwitchSettings(ALTERNATE, 0.5, -1, "random:0.0208", SENIOR)
+        else:
+            sw = SwitchSettings(REDRAW, 0.5, -1, "random:0.0208", DRAW)
+        return w.replace(name=name, switch=sw, sample=SampleSettings(0.6, -1, 0.0, 0.0, 2048),
+                         seed_base=9 if name.endswith("alternate") else 10)
     raise KeyError(name)
 
 
-NAMES = ("tiny", "small", "qwen", "longcot", "wide", "paper", "qwen-paper", "self-paired")
+NAMES = ("tiny", "small", "qwen", "longcot", "wide", "paper", "qwen-paper", "self-paired", "qwen-eval-alternate",
+         "qwen-eval-stepcoin")
 
 
 def scaled(shape: ModelShape, **kw) -> ModelShape:
