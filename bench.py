@@ -340,6 +340,8 @@ def main():
                     help="skip the extra rollout that times every kernel class with the forwards serialized")
     ap.add_argument("--no-concurrent", action="store_true",
                     help="skip the extra rollout that times the attention launches in the two-stream schedule")
+    ap.add_argument("--no-solo", action="store_true",
+                    help="skip the single-model rollout of the senior (the tandem-over-solo step-time ratio)")
     ap.add_argument("--score", type=int, default=0, metavar="STEPS",
                     help="also time tandem_score_step after each of STEPS decode steps (reported as 'scoring')")
     ap.add_argument("--grpo", type=int, default=0, metavar="REPS",
@@ -571,6 +573,49 @@ def main():
         log(f"[bench] grpo loss: {ms * 1e3:.1f} us per call replayed ({ms_eager * 1e3:.1f} us eager; "
             f"{grpo['achieved_gbs']:.0f} GB/s over {grpo['positions']} positions; replays match: {same})")
 
+    # ---- the senior alone through the same kernels (a handle without a
+    # junior): the decode step-time ratio of the tandem rollout over a
+    # single-model rollout of the same batch, which the paper reports as about
+    # 2x latency and 0.5x throughput on its two-GPU layout
+    solo = None
+    tandem_dec_ms = sum(dec) / (L * n_timed)
+    if args.no_solo:
+        skipped.append("solo rollout (--no-solo)")
+    elif left() < 1.0 * est + 30:
+        skipped.append(f"solo rollout (budget: {left():.0f}s left)")
+    else:
+        sen_model = eng.sen
+        eng.close()
+        del eng.kv, eng.scratch
+        torch.cuda.empty_cache()
+        seng = TandemEngine(wl.senior, None, None, None, wl.switch, wl.sample, wl.philox_seed, max_seqs=n,
+                            max_ctx=max_ctx, max_prefill_tokens=4096, models=(sen_model, None))
+        seng.prefill(prompts, wl.group)
+        seng.step()                                  # captures the single-model step graph
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(seng.stream)
+        seng.prefill(prompts, wl.group)
+        ev[1].record(seng.stream)
+        for _ in range(L):
+            seng.step()
+        ev[2].record(seng.stream)
+        torch.cuda.synchronize()
+        s_pre, s_dec = ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])
+        seng.close()
+        solo_ms = s_dec / L
+        solo = {"solo_decode_ms_per_step": round(solo_ms, 4), "tandem_decode_ms_per_step": round(tandem_dec_ms, 4),
+                "step_time_ratio": round(tandem_dec_ms / solo_ms, 4),
+                "throughput_ratio": round(solo_ms / tandem_dec_ms, 4),
+                "solo_prefill_ms": round(s_pre, 3), "tandem_prefill_ms": round(pre_ms, 3),
+                "solo_tokens_per_s": round(gen / ((s_pre + s_dec) / 1e3), 2),
+                "method": "one rollout of the same batch with a handle that has no junior (the senior emits every "
+                          "token, same kernels, step graph), HIP events around prefill and decode",
+                "paper_context": "tandem step about 2x a single-model step and rollout throughput about 0.5x "
+                                 "single-model vLLM, senior and junior on two A100 80 GB GPUs"}
+        log(f"[bench] solo senior rollout: decode {s_dec:.1f} ms ({solo_ms:.3f} ms/step); tandem/solo step time "
+            f"{solo['step_time_ratio']:.3f}")
+
     bf16 = wl.senior.dtype == "bf16"
     res = {
         "metric": METRIC,
@@ -613,6 +658,7 @@ def main():
         "skipped": skipped,
         "run_wall_s": round(time.perf_counter() - T_START, 1),
     }
+    res["tandem_over_solo"] = solo
     if scoring is not None:
         res["scoring"] = scoring
     if grpo is not None:

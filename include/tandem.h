@@ -146,7 +146,8 @@ typedef struct {
 typedef struct tandem_handle tandem_handle;
 
 /* Bytes of KV arena and scratch that tandem_init needs for these shapes and
- * this capacity.  Both buffers must be 256-byte aligned device memory. */
+ * this capacity (junior NULL: the senior alone).  Both buffers must be
+ * 256-byte aligned device memory. */
 tandem_status tandem_workspace_size(const tandem_model_cfg* senior, const tandem_model_cfg* junior,
                                     const tandem_capacity* cap, size_t* kv_bytes,
                                     size_t* scratch_bytes);
@@ -160,7 +161,12 @@ tandem_status tandem_workspace_size(const tandem_model_cfg* senior, const tandem
  * (rotary table, MFMA-ordered weight copies in scratch) on the stream; it
  * does not wait for them (later calls on the same stream are ordered after
  * them).  stream is a hipStream_t (NULL = the null stream).  On success
- * *out_handle is set; on failure nothing is left allocated. */
+ * *out_handle is set; on failure nothing is left allocated.
+ * junior NULL: a single-model rollout of the senior through the same
+ * kernels, the baseline the paper compares the tandem rollout with (plain
+ * GRPO sampling, one model): the senior emits every token (m_t = 1), sw is
+ * ignored (may be NULL), the junior's debug logits are not written, and
+ * tandem_score_step returns TANDEM_E_STATE. */
 tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior,
                           const tandem_switch_cfg* sw, const tandem_sample_cfg* smp,
                           const tandem_capacity* cap, void* kv_arena, size_t kv_bytes,

@@ -129,16 +129,22 @@ def check(status: int, handle=None) -> None:
 
 # ------------------------------------------------- same-named thin wrappers
 
-def tandem_workspace_size(sen: ModelCfg, jun: ModelCfg, cap: Capacity):
+def _ref(x):
+    return C.byref(x) if x is not None else None
+
+
+def tandem_workspace_size(sen: ModelCfg, jun, cap: Capacity):
+    """jun None: the senior alone."""
     kv, sc = C.c_size_t(), C.c_size_t()
-    check(lib.tandem_workspace_size(C.byref(sen), C.byref(jun), C.byref(cap), C.byref(kv), C.byref(sc)))
+    check(lib.tandem_workspace_size(C.byref(sen), _ref(jun), C.byref(cap), C.byref(kv), C.byref(sc)))
     return kv.value, sc.value
 
 
-def tandem_init(sen: Model, jun: Model, sw: SwitchCfg, smp: SampleCfg, cap: Capacity, kv_ptr: int,
+def tandem_init(sen: Model, jun, sw, smp: SampleCfg, cap: Capacity, kv_ptr: int,
                 kv_bytes: int, scratch_ptr: int, scratch_bytes: int, out: Outputs, stream: int):
+    """jun None: a single-model rollout of the senior (sw may be None)."""
     h = C.c_void_p()
-    check(lib.tandem_init(C.byref(sen), C.byref(jun), C.byref(sw), C.byref(smp), C.byref(cap), kv_ptr,
+    check(lib.tandem_init(C.byref(sen), _ref(jun), _ref(sw), C.byref(smp), C.byref(cap), kv_ptr,
                           kv_bytes, scratch_ptr, scratch_bytes, C.byref(out), stream, C.byref(h)))
     return h
 

@@ -82,6 +82,7 @@ bool packs(const tandem_model_cfg* c, int N, int K) {
 }
 
 struct Plan {
+  int nm;                     // models: 2 (senior and junior), 1 (the senior alone)
   int ctx_stride;
   int n_chunks;
   ModelPlan m[2];
@@ -180,8 +181,9 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
   P.ctx_stride = (int)align_up((size_t)cap->max_ctx, 64);
   P.n_chunks = (sen->vocab + kVocabChunk - 1) / kVocabChunk;
   const tandem_model_cfg* cf[2] = {sen, jun};
+  P.nm = jun ? 2 : 1;
   size_t kv = 0, sc = 0;
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < P.nm; ++i) {
     const tandem_model_cfg* c = cf[i];
     ModelPlan& m = P.m[i];
     m.esz = c->weight_dtype == TANDEM_BF16 ? 2 : 4;
@@ -232,7 +234,8 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
 }  // namespace
 
 struct tandem_handle {
-  Model m[2];                 // 0: senior, 1: junior
+  Model m[2];                 // 0: senior, 1: junior (unused when nm == 1)
+  int nm = 2;                 // 1: a single-model rollout of the senior (no junior)
   Plan plan;
   tandem_switch_cfg sw;
   tandem_sample_cfg smp;
@@ -580,6 +583,7 @@ tandem_status forward(tandem_handle* h, Model& m, const FwdRows& fr, bool lm_hea
 // the other model in that order.
 tandem_status forward_pair(tandem_handle* h, const FwdRows& fr, bool lm_head) {
   hipStream_t st = h->stream;
+  if (h->nm == 1) return forward(h, h->m[0], fr, lm_head, st);
   if (h->timing & TANDEM_TIMING_SERIAL) {
     for (int i = 0; i < 2; ++i) CALL(forward(h, h->m[i], fr, lm_head, st));
     return TANDEM_OK;
@@ -632,7 +636,7 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
   }
   const int V = h->m[0].cfg.vocab;
   SampleArgs sa{};
-  sa.z_sen = h->m[0].logits; sa.z_jun = h->m[1].logits; sa.R = R; sa.V = V;
+  sa.z_sen = h->m[0].logits; sa.z_jun = h->m[h->nm - 1].logits; sa.R = R; sa.V = V;
   sa.temp = h->smp.temperature; sa.eos_id = h->smp.eos_id;
   sa.eos_bias_sen = h->smp.eos_bias_senior; sa.eos_bias_jun = h->smp.eos_bias_junior;
   sa.key0 = h->key0; sa.key1 = h->key1;
@@ -641,7 +645,8 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
   TIMED(TANDEM_K_SAMPLE, launch_sample_partials(sa, h->plan.n_chunks, st));
   if (dbg) {
     if (dbg->logits_senior) HIPCHK(launch_scatter_rows(h->m[0].logits, h->act, R, V, dbg->logits_senior, st));
-    if (dbg->logits_junior) HIPCHK(launch_scatter_rows(h->m[1].logits, h->act, R, V, dbg->logits_junior, st));
+    if (dbg->logits_junior && h->nm == 2)
+      HIPCHK(launch_scatter_rows(h->m[1].logits, h->act, R, V, dbg->logits_junior, st));
   }
   FinishArgs fa{};
   fa.z_sen = h->m[0].logits; fa.R = R; fa.V = V; fa.act = h->act;
@@ -808,12 +813,12 @@ const char* tandem_last_error(const tandem_handle* h) { return h ? h->err.c_str(
 
 tandem_status tandem_workspace_size(const tandem_model_cfg* senior, const tandem_model_cfg* junior,
                                     const tandem_capacity* cap, size_t* kv_bytes, size_t* scratch_bytes) {
-  if (!senior || !junior || !cap || !kv_bytes || !scratch_bytes)
+  if (!senior || !cap || !kv_bytes || !scratch_bytes)
     return fail(nullptr, TANDEM_E_ARG, "tandem_workspace_size: NULL argument");
   tandem_status s;
   if ((s = check_cfg(senior, "senior", nullptr)) != TANDEM_OK) return s;
-  if ((s = check_cfg(junior, "junior", nullptr)) != TANDEM_OK) return s;
-  if (senior->vocab != junior->vocab)
+  if (junior && (s = check_cfg(junior, "junior", nullptr)) != TANDEM_OK) return s;
+  if (junior && senior->vocab != junior->vocab)
     return fail(nullptr, TANDEM_E_SHAPE, "senior and junior must share one vocabulary");
   if ((s = check_cap(cap, nullptr)) != TANDEM_OK) return s;
   Plan P = make_plan(senior, junior, cap);
@@ -828,16 +833,17 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
                           void* stream, tandem_handle** out_handle) {
   if (!out_handle) return fail(nullptr, TANDEM_E_ARG, "tandem_init: out_handle is NULL");
   *out_handle = nullptr;
-  if (!senior || !junior || !sw || !smp || !cap || !out)
+  if (!senior || (junior && !sw) || !smp || !cap || !out)
     return fail(nullptr, TANDEM_E_ARG, "tandem_init: NULL argument");
   tandem_status s;
+  const int nm = junior ? 2 : 1;
   if ((s = check_cfg(&senior->cfg, "senior", nullptr)) != TANDEM_OK) return s;
-  if ((s = check_cfg(&junior->cfg, "junior", nullptr)) != TANDEM_OK) return s;
-  if (senior->cfg.vocab != junior->cfg.vocab)
+  if (junior && (s = check_cfg(&junior->cfg, "junior", nullptr)) != TANDEM_OK) return s;
+  if (junior && senior->cfg.vocab != junior->cfg.vocab)
     return fail(nullptr, TANDEM_E_SHAPE, "senior and junior must share one vocabulary");
   if ((s = check_cap(cap, nullptr)) != TANDEM_OK) return s;
   const tandem_model* md[2] = {senior, junior};
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < nm; ++i) {
     const tandem_model* m = md[i];
     if (!m->embed || !m->layers || !m->final_norm || !m->lm_head)
       return fail(nullptr, TANDEM_E_ARG, "tandem_init: a model weight pointer is NULL");
@@ -852,6 +858,10 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
         if (p[k] && misaligned(p[k])) return fail(nullptr, TANDEM_E_ARG, "tandem_init: weights must be 16-byte aligned");
     }
   }
+  // The senior alone: it emits every token (SWITCH with p = 0, senior first);
+  // the caller's switch settings, if any, do not apply.
+  const tandem_switch_cfg solo_sw{TANDEM_SWITCH, 0.0, -1, nullptr, TANDEM_SENIOR};
+  if (!junior) sw = &solo_sw;
   if (sw->mode < TANDEM_REDRAW || sw->mode > TANDEM_ALTERNATE)
     return fail(nullptr, TANDEM_E_ARG, "switch mode must be REDRAW, SWITCH or ALTERNATE");
   if (!(sw->p >= 0.0 && sw->p <= 1.0)) return fail(nullptr, TANDEM_E_ARG, "switch p must lie in [0, 1]");
@@ -868,12 +878,13 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   if (!kv_arena || !scratch) return fail(nullptr, TANDEM_E_ARG, "tandem_init: kv_arena or scratch is NULL");
   if (((uintptr_t)kv_arena % kAlign) || ((uintptr_t)scratch % kAlign))
     return fail(nullptr, TANDEM_E_ARG, "kv_arena and scratch must be 256-byte aligned");
-  Plan P = make_plan(&senior->cfg, &junior->cfg, cap);
+  Plan P = make_plan(&senior->cfg, junior ? &junior->cfg : nullptr, cap);
   if (kv_bytes < P.kv_bytes || scratch_bytes < P.scratch_bytes)
     return fail(nullptr, TANDEM_E_CAPACITY, "kv_arena or scratch smaller than tandem_workspace_size");
 
   tandem_handle* h = new tandem_handle();
   h->plan = P;
+  h->nm = nm;
   h->sw = *sw;
   h->smp = *smp;
   h->cap = *cap;
@@ -886,7 +897,7 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   char* kv = (char*)kv_arena;
   char* sc = (char*)scratch;
   size_t kv_off = 0;
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < nm; ++i) {
     Model& m = h->m[i];
     const tandem_model* src = md[i];
     m.cfg = src->cfg;
@@ -978,21 +989,21 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   if (e != hipSuccess) { h->ev_in = nullptr; return bail(e, "graph entry event"); }
   e = hipEventCreateWithFlags(&h->ev_out, hipEventDisableTiming);
   if (e != hipSuccess) { h->ev_out = nullptr; return bail(e, "graph exit event"); }
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < nm; ++i)
     for (int l = 0; l < h->m[i].cfg.n_layers; ++l) {
       hipEvent_t ev;
       e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
       if (e != hipSuccess) return bail(e, "attention event");
       h->ev_att[i].push_back(ev);
     }
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < nm; ++i) {
     e = launch_rope_table(h->m[i].cfg.rope_theta, h->m[i].cfg.head_dim, P.ctx_stride, h->m[i].rope, h->stream);
     if (e != hipSuccess) return bail(e, "rope table");
   }
   // MFMA-ordered copies of the projection and LM-head weights (read by the
   // streaming decode GEMM; the caller's row-major weights stay in use for
   // prefill-sized products)
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < nm; ++i) {
     Model& m = h->m[i];
     char* dst = sc + m.p.off_packed;
     const auto shapes = packed_shapes(&m.cfg);
@@ -1054,7 +1065,7 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
   // the G sequences of a prompt share its prefix in decode attention when
   // both models' attention kernels can (otherwise every slot gets a copy)
   bool share = G > 1;
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < h->nm; ++i) {
     const tandem_model_cfg& c = h->m[i].cfg;
     share = share && attention_shares_prefix(c.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32, c.head_dim,
                                              c.n_q_heads / c.n_kv_heads);
@@ -1118,7 +1129,7 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens, con
       const int P = prompt_offsets[j + 1] - prompt_offsets[j];
       if (P - 1 <= 0 || G <= 1) continue;
       const int lo = share ? (P - 1) / 16 * 16 : 0;    // shared positions stay in the first slot only
-      for (int i = 0; i < 2; ++i) {
+      for (int i = 0; i < h->nm; ++i) {
         Model& m = h->m[i];
         TIMED(TANDEM_K_OTHER, launch_kv_replicate(m.cfg.weight_dtype == TANDEM_BF16 ? DT_BF16 : DT_F32, m.kc, m.vc,
                                    m.cfg.n_layers, m.layer_stride, m.slot_stride, m.cfg.n_kv_heads,
@@ -1157,6 +1168,7 @@ tandem_status tandem_score_step(tandem_handle* h, float* scores) {
   if (!scores) return fail(&h->err, TANDEM_E_ARG, "tandem_score_step: scores is NULL");
   if (!h->prefilled || !h->stepped)
     return fail(&h->err, TANDEM_E_STATE, "tandem_score_step before a step of the current batch");
+  if (h->nm != 2) return fail(&h->err, TANDEM_E_STATE, "tandem_score_step needs a junior (the handle has none)");
   // the step's rows: its act order, launched row count, done-at-start flags and
   // logits are all still in place (compaction runs at the start of a step)
   ScoreArgs a{};

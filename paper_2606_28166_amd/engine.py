@@ -48,24 +48,27 @@ class DeviceModel:
 
 
 class TandemEngine:
+    """junior_shape None (or models[1] None): the senior alone, through the
+    same kernels (every token the senior's; switch is ignored)."""
+
     def __init__(self, senior_shape, senior_w, junior_shape, junior_w, switch, sample, seed: int,
                  max_seqs: int, max_ctx: int, max_prefill_tokens: int = 4096,
                  boundary_words: Optional[np.ndarray] = None, device: str = "cuda:0",
-                 models: Optional[Sequence[DeviceModel]] = None):
+                 models: Optional[Sequence[Optional[DeviceModel]]] = None):
         if not torch.cuda.is_available():
             raise RuntimeError("TandemEngine needs a ROCm GPU (torch.cuda.is_available() is False)")
         self.dev = torch.device(device)
         torch.cuda.set_device(self.dev)
         if models is None:
             self.sen = DeviceModel(senior_shape, senior_w, self.dev)
-            self.jun = DeviceModel(junior_shape, junior_w, self.dev)
+            self.jun = DeviceModel(junior_shape, junior_w, self.dev) if junior_shape is not None else None
         else:
             self.sen, self.jun = models
         self.sample = sample
         self.max_seqs, self.max_new = max_seqs, sample.max_new
         self.V = self.sen.shape.vocab
         self.cap = L.Capacity(max_seqs, max_ctx, max_prefill_tokens)
-        kvb, scb = L.tandem_workspace_size(self.sen.desc.cfg, self.jun.desc.cfg, self.cap)
+        kvb, scb = L.tandem_workspace_size(self.sen.desc.cfg, self.jun.desc.cfg if self.jun else None, self.cap)
         self.kv_bytes, self.scratch_bytes = kvb, scb
         self.kv = torch.empty(kvb, dtype=torch.uint8, device=self.dev)
         self.scratch = torch.empty(scb, dtype=torch.uint8, device=self.dev)
@@ -83,8 +86,9 @@ class TandemEngine:
         self.out = L.Outputs(self.tokens.data_ptr(), self.owner.data_ptr(), self.logprob.data_ptr(),
                              self.length.data_ptr())
         self.stream = torch.cuda.current_stream(self.dev)
-        self.h = L.tandem_init(self.sen.desc, self.jun.desc, self.sw, self.smp, self.cap, self.kv.data_ptr(),
-                               kvb, self.scratch.data_ptr(), scb, self.out, self.stream.cuda_stream)
+        self.h = L.tandem_init(self.sen.desc, self.jun.desc if self.jun else None, self.sw, self.smp, self.cap,
+                               self.kv.data_ptr(), kvb, self.scratch.data_ptr(), scb, self.out,
+                               self.stream.cuda_stream)
         self.n_seq = 0
         self._forced = torch.full((max_seqs,), -1, dtype=torch.int32, device=self.dev)
 

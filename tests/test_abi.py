@@ -156,3 +156,13 @@ def test_grpo_noalloc_argument_and_capacity_checks():
     assert L.tandem_grpo_workspace_size(big) == (1 << 20) + 256
     assert call(C.byref(big), fake, fake, fake, fake, None, fake, None, fake, fake, None) == L.E_CAPACITY
     assert b"holds 1048576" in L.lib.tandem_last_error(None)
+
+
+def test_workspace_size_of_the_senior_alone():
+    s, j = _cfgs("qwen")
+    cap = L.Capacity(128, 256 - 1 + 2048, 4096)
+    kv2, sc2 = L.tandem_workspace_size(s, j, cap)
+    kv1, sc1 = L.tandem_workspace_size(s, None, cap)
+    ctx = ((2303 + 63) // 64) * 64
+    assert kv1 == 2 * 2 * 128 * ctx * 128 * 8 * 36          # the senior's K and V only
+    assert kv1 < kv2 and sc1 < sc2

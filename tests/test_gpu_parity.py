@@ -366,3 +366,50 @@ def test_graph_replays_with_compaction_match_oracle_fp32():
     first, full, n = P.first_divergence(graph, ref, np.arange(wl.n_seqs), wl.sample.max_new, band=1e-4)
     P.log(f"  {full}/{wl.n_seqs} rows identical to the oracle, {n} tokens compared, first divergence {first}")
     assert full >= wl.n_seqs - 2
+
+
+def test_senior_alone_matches_single_model_sampling():
+    """A handle without a junior: the senior emits every token through the
+    same kernels, as the oracle's tandem rollout does with SWITCH p = 0 and the
+    senior first (pinned on the CPU to equal plain single-model sampling)."""
+    from paper_2606_28166_amd.engine import TandemEngine
+    from oracle.rollout import rollout, build_models
+    P.log("case the senior alone: small shapes 2 layers, ragged prompts, 24 steps")
+    wl = _small_reduced()
+    wl.switch = W.SwitchSettings(W.SWITCH, 0.0, -1, "all", W.SENIOR)
+    ws, wj, prompts, bnd = W.make_all(wl)
+    sen, jun = build_models(wl, ws, wj)
+    ref = rollout(sen, jun, prompts, wl.group, wl.switch, wl.sample, wl.philox_seed, bnd, keep_logits_at=(1, 24))
+    n = wl.n_seqs
+    eng = TandemEngine(wl.senior, ws, None, None, wl.switch, wl.sample, wl.philox_seed, max_seqs=n,
+                       max_ctx=max(len(p) for p in prompts) - 1 + wl.sample.max_new, max_prefill_tokens=256)
+    eng.prefill(prompts, wl.group)
+    worst = 0.0
+    for t in range(1, wl.sample.max_new + 1):
+        dbg = eng.step_forced(ref.tokens[:, t - 1], logits=t in (1, 24))
+        big = ref.margin[:, t - 1] > P.MARGIN
+        got = dbg["sampled"][:n].cpu().numpy()
+        np.testing.assert_array_equal(got[big], ref.sampled[big, t - 1])
+        if t in (1, 24):
+            z = dbg["logits_senior"][:n].cpu().numpy()
+            worst = max(worst, float(np.abs(z - ref.logits[t]["senior"]).max()))
+    out = eng.outputs()
+    eng.close()
+    assert worst < P.TOL_BF16
+    np.testing.assert_array_equal(out["tokens"], ref.tokens)
+    assert out["owner"].all() and ref.owner.all()
+    np.testing.assert_allclose(out["logprob"], ref.logprob, rtol=0, atol=P.TOL_BF16)
+    P.log(f"  max |dlogits| {worst:.2e}")
+
+
+def test_self_paired_shapes_paper_schedule():
+    """The paper's self-paired pair (two Qwen3-4B-shaped models) under its
+    training schedule (REDRAW p = 0.5, K = 32, drawn first owner, T = 0.6, 35%
+    boundary set), 2 + 2 layers, 40 steps."""
+    P.log("case self-paired 4B/4B shapes, paper schedule, 2+2 layers, 40 steps")
+    wl = W.workload("self-paired").replace(gain_jitter=0.05, n_prompts=1, group=4, prompt_len=64)
+    wl.senior.n_layers, wl.junior.n_layers = 2, 2
+    wl.sample.max_new = 40
+    p = P.run(wl, logits_at=(1, 40))
+    P.check(p, P.TOL_BF16)
+    assert p.ref.decided.sum() > 0 and 0 < p.ref.owner.mean() < 1
