@@ -175,13 +175,13 @@ PMC_COPY_BYTES = 1 << 30
 PMC_WARM = 1000          # graph-replayed steps first: contexts ~1255 .. 1279 in the measured steps
 PMC_STEPS = 24
 # kernel classes of the decode step: (name, kernel-name substring, source file)
-PMC_CLASSES = (("attention", "attn_shared_kernel", "k_attn.hip"),
+PMC_CLASSES = (("attention", "attn_rows_kernel", "k_attn.hip"),
                ("projections", "gemm_stream_kernel", "k_stream.hip"),
                ("resid_norm", "resid_norm_kernel", "k_misc.hip"),
                ("qkv_post", "qkv_post_kernel", "k_misc.hip"),
                ("swiglu_finish", "swiglu_finish_kernel", "k_misc.hip"),
                ("sample_partials", "sample_partials_kernel", "k_misc.hip"))
-PMC_REGEX = "attn_shared|gemm_stream|resid_norm|qkv_post|swiglu_finish|sample_partials|copy|elementwise"
+PMC_REGEX = "attn_rows|gemm_stream|resid_norm|qkv_post|swiglu_finish|sample_partials|copy"
 
 
 def source_digest(name: str) -> str:
@@ -218,25 +218,31 @@ def pmc_run() -> None:
     from paper_2606_28166_amd.engine import TandemEngine
 
     dev = torch.device("cuda:0")
-    x = torch.ones(PMC_COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    print("pmc: calibration copy", flush=True)
+    x = torch.empty(PMC_COPY_BYTES // 4, dtype=torch.float32, device=dev)
     y = torch.empty_like(x)
     y.copy_(x)
     torch.cuda.synchronize()
     del x, y
     wl = W.workload("qwen")
-    wl.sample.max_new = PMC_WARM + PMC_STEPS
+    wl.sample.max_new = PMC_WARM + PMC_STEPS + 8       # every row still runs in the measured steps
     ws, wj, prompts, bnd = W.make_all(wl)
+    print("pmc: weights generated", flush=True)
     eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed,
                        max_seqs=wl.n_seqs, max_ctx=max(len(p) for p in prompts) - 1 + wl.sample.max_new,
                        max_prefill_tokens=4096, boundary_words=W.boundary_bits(bnd))
+    torch.cuda.synchronize()
+    print("pmc: engine ready", flush=True)
     eng.prefill(prompts, wl.group)
+    torch.cuda.synchronize()
+    print("pmc: prefill done", flush=True)
     for t in range(PMC_WARM):
         eng.step()
         if (t + 1) % 250 == 0:
             torch.cuda.synchronize()
             print(f"pmc: {t + 1} graph steps", flush=True)
     torch.cuda.synchronize()
-    m = torch.ones(1 << 20, dtype=torch.float32, device=dev)
+    m = torch.empty(1 << 20, dtype=torch.float32, device=dev)
     m2 = torch.empty_like(m)
     m2.copy_(m)                                  # marker: the measured steps follow
     torch.cuda.synchronize()
@@ -265,7 +271,7 @@ def pmc_analyze(fetch_csv: str, write_csv: str) -> dict:
     for name, path in (("fetch", fetch_csv), ("write", write_csv)):
         rows = sorted((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"]))
                       for r in csv.DictReader(open(path)))
-        copies = [(i, v) for i, k, v in rows if "copy" in k.lower() or "elementwise" in k.lower()]
+        copies = [(i, v) for i, k, v in rows if "copy" in k.lower()]
         if len(copies) < 2:
             raise SystemExit(f"{path}: expected the calibration copy and the marker copy")
         cal = max(v for _, v in copies)
@@ -283,6 +289,8 @@ def pmc_analyze(fetch_csv: str, write_csv: str) -> dict:
     wbytes = PMC_STEPS * (weight_bytes(wl.senior) + weight_bytes(wl.junior))
     for cname, sub, srcf in PMC_CLASSES:
         (fb, fn), (wb, wn) = per[cname]["fetch"], per[cname]["write"]
+        if fn == 0 and wn == 0:
+            continue                              # not collected in these passes
         if fn != wn:
             raise SystemExit(f"{cname}: {fn} fetch dispatches against {wn} write dispatches")
         c = {"kernel": sub, "source_sha256_16": source_digest(srcf), "dispatches": fn,
@@ -336,6 +344,8 @@ def main():
                     help="warmup rollouts after the first run only while they fit this many seconds")
     ap.add_argument("--cpu-steps", type=int, default=16, help="decode steps of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--separate-sample", action="store_true",
+                    help="store the logits and sample in a separate pass instead of inside the LM-head GEMMs")
     ap.add_argument("--no-isolated", action="store_true",
                     help="skip the extra rollout that times every kernel class with the forwards serialized")
     ap.add_argument("--no-concurrent", action="store_true",
@@ -389,6 +399,8 @@ def main():
     n = wl.n_seqs
     skipped = []
 
+    SEP = LIB.TIMING_SEPARATE_SAMPLE if args.separate_sample else 0
+
     def rollout_once(timing=0):
         """Prefill + L decode steps; timing = the library's class mask (0: step-graph replays).
         Returns (prefill ms, decode ms, per-class timing or None, wall s)."""
@@ -397,13 +409,13 @@ def main():
         ev[0].record(stream)
         eng.prefill(prompts, wl.group)
         ev[1].record(stream)
-        eng.timing(timing)
+        eng.timing(timing | SEP)
         for _ in range(L):
             eng.step()
         ev[2].record(stream)
         torch.cuda.synchronize()
         tr = eng.timing_read() if timing & 0b1111 else None
-        eng.timing(0)
+        eng.timing(SEP)
         return ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), tr, time.perf_counter() - w0
 
     # ---- warmup: the first rollout captures the step graph and sets the
@@ -506,7 +518,9 @@ def main():
     scoring = None
     if args.score > 0:
         # the dual-distribution scores after each step of a fresh rollout:
-        # HIP events on the library's stream around every scoring call
+        # HIP events on the library's stream around every scoring call (the
+        # steps store their logits, as a caller scoring every step would ask)
+        eng.timing(LIB.TIMING_SEPARATE_SAMPLE)
         eng.prefill(prompts, wl.group)
         sc_out = torch.empty((wl.n_seqs, 3), dtype=torch.float32, device=eng.dev)
         tot, ns = 0.0, min(args.score, L)
@@ -518,6 +532,7 @@ def main():
             e1.record(stream)
             torch.cuda.synchronize()
             tot += e0.elapsed_time(e1)
+        eng.timing(SEP)
         ms = tot / ns
         nbytes = 4 * n * wl.senior.vocab * 4          # two passes over both models' fp32 logits
         scoring = {"steps": ns, "ms_per_step": round(ms, 4), "bytes_per_step": nbytes,
@@ -590,6 +605,7 @@ def main():
         torch.cuda.empty_cache()
         seng = TandemEngine(wl.senior, None, None, None, wl.switch, wl.sample, wl.philox_seed, max_seqs=n,
                             max_ctx=max_ctx, max_prefill_tokens=4096, models=(sen_model, None))
+        seng.timing(SEP)
         seng.prefill(prompts, wl.group)
         seng.step()                                  # captures the single-model step graph
         torch.cuda.synchronize()
@@ -638,6 +654,8 @@ def main():
                          "fp16 copies of the bf16 weights; attention bf16 K/V with hi+lo q and P; fp32 sampling")
                         if bf16 else "fp32 weights, activations and K/V",
         "data": "synthetic",
+        "sampling": ("separate pass over stored logits" if SEP or not bf16 or n > 128
+                     else "inside the LM-head GEMMs (Gumbel noise beside the forwards, no logits stored)"),
         "config": {"workload": DESCRIPTIONS[wl.name], "name": wl.name, "rows": n,
                    "prompt_len": plens[0] if min(plens) == max(plens) else [min(plens), max(plens)],
                    "max_new": L, "senior_layers": wl.senior.n_layers, "junior_layers": wl.junior.n_layers,

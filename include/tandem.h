@@ -207,7 +207,13 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens,
  * first tandem_step after tandem_prefill, or after a timing-mode change)
  * and every step replays it: the per-step state lives in device memory, so
  * the same graph serves every step.  Capture allocates host-side graph
- * objects and events owned by the handle. */
+ * objects and events owned by the handle.
+ * Where both LM heads run on the streaming decode GEMM (bf16 weights whose
+ * packed copy fits, vocab % 4 == 0) and at most 128 rows are launched, the
+ * sampling runs inside the LM-head GEMMs: the step's Gumbel noise is
+ * generated beside the forwards, each head folds its scores into per-row
+ * partials (the senior's log-sum-exp, the owner's top two), and no logits
+ * are stored. */
 tandem_status tandem_step(tandem_handle* h, int32_t* n_active);
 
 /* As tandem_step (the same pass of Algorithm 1's loop, launched kernel by
@@ -229,6 +235,8 @@ tandem_status tandem_step_forced(tandem_handle* h, const int32_t* forced, const 
  * (device float [max_seqs][3], caller-owned) receive (-log p_jun(y), alpha,
  * KL(p_sen || p_jun)), y being the token the step appended to s; entries of
  * other sequences are left untouched.  Asynchronous on the handle's stream.
+ * A step that sampled inside the LM heads stored no logits: both LM heads
+ * then run again here, on the step's LM-head input rows.
  * TANDEM_E_STATE when no step has been taken since the last prefill;
  * TANDEM_E_ARG when scores is NULL. */
 tandem_status tandem_score_step(tandem_handle* h, float* scores);
@@ -323,8 +331,17 @@ enum { TANDEM_K_ATTENTION = 0,    /* decode / prompt attention            */
  *                         each timed launch has the GPU to itself;
  *   TANDEM_TIMING_EAGER   tandem_step launches every kernel from the host
  *                         instead of replaying its captured HIP graph.
- * Results are unchanged; only the schedule differs. */
-enum { TANDEM_TIMING_SERIAL = 1 << 8, TANDEM_TIMING_EAGER = 1 << 9 };
+ * Results are unchanged; only the schedule differs.
+ *   TANDEM_TIMING_SEPARATE_SAMPLE  the step stores both models' logits and
+ *                         samples in a pass over them, instead of sampling
+ *                         inside the LM-head GEMMs (the default where both LM
+ *                         heads run as fp16 streaming GEMMs over at most 128
+ *                         rows); the two agree up to float rounding (the
+ *                         log-sum-exp is accumulated in another order, the
+ *                         appended token's senior score is a separate dot
+ *                         product), so a Gumbel tie inside that rounding may
+ *                         sample differently. */
+enum { TANDEM_TIMING_SERIAL = 1 << 8, TANDEM_TIMING_EAGER = 1 << 9, TANDEM_TIMING_SEPARATE_SAMPLE = 1 << 10 };
 tandem_status tandem_timing_enable(tandem_handle* h, int32_t class_mask);
 tandem_status tandem_timing_read(tandem_handle* h, int32_t kernel_class, double* total_ms, int64_t* launches);
 

@@ -66,6 +66,7 @@ EXPORTS = ("tandem_workspace_size", "tandem_init", "tandem_prefill", "tandem_ste
 K_ATTENTION, K_GEMM, K_SAMPLE, K_OTHER = 0, 1, 2, 3
 TIMING_SERIAL = 1 << 8          # timing flag: run the two forwards one after the other
 TIMING_EAGER = 1 << 9           # timing flag: launch every kernel from the host (no step graph)
+TIMING_SEPARATE_SAMPLE = 1 << 10  # flag: store the logits and sample in a separate pass (no sampling in the LM heads)
 
 
 def _load():

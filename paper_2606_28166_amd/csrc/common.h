@@ -211,4 +211,30 @@ __device__ __forceinline__ float fast_exp(float x) {
   return __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
 }
 
+// --------------------------------------------------------------- sampling
+// Best and second-best Gumbel-perturbed score of a vocabulary range: b at
+// index i, s the runner-up (ties go to the smaller index).
+struct Top2 {
+  float b; int i; float s;
+};
+__device__ __forceinline__ bool beats(float vb, int ib, float va, int ia) {
+  return vb > va || (vb == va && ib < ia);
+}
+__device__ __forceinline__ Top2 merge_top2(Top2 A, Top2 B) {
+  Top2 out;
+  if (beats(B.b, B.i, A.b, A.i)) {
+    out.b = B.b; out.i = B.i; out.s = fmaxf(fmaxf(A.s, B.s), A.b);
+  } else {
+    out.b = A.b; out.i = A.i; out.s = fmaxf(fmaxf(A.s, B.s), B.b);
+  }
+  return out;
+}
+// Running (max m, sum l of e^(v - m)) pairs merged.
+__device__ __forceinline__ void merge_lse(float& m, float& l, float m2, float l2) {
+  const float M = fmaxf(m, m2);
+  if (M == -INFINITY) { m = M; l = 0.f; return; }
+  l = l * expf(m - M) + l2 * expf(m2 - M);
+  m = M;
+}
+
 }  // namespace tandem

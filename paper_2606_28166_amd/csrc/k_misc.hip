@@ -65,43 +65,42 @@ __global__ __launch_bounds__(kNT) void embed_norm_kernel(const int32_t* __restri
   }
 }
 
+// At most 64 VGPRs (eight waves per SIMD): a workgroup then fits on a
+// compute unit beside two decode-attention waves per SIMD, so the norm that
+// follows a projection starts while the other model's attention still holds
+// the compute units.  The summed row waits in LDS for the normalisation.
 template <int FMT>
-__global__ __launch_bounds__(kNT) void resid_norm_kernel(const float* __restrict__ ws, int S,
-                                                         long ws_stride, float* __restrict__ h,
-                                                         const float* __restrict__ gain, float eps,
-                                                         void* __restrict__ x, int d) {
+__global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(8))) void resid_norm_kernel(
+    const float* __restrict__ ws, int S, long ws_stride, float* __restrict__ h, const float* __restrict__ gain,
+    float eps, void* __restrict__ x, int d) {
   __shared__ float red[kNT / 64];
+  extern __shared__ float4 row[];            // d / 4 entries (launch-sized)
   const int r = blockIdx.x, tid = threadIdx.x;
   const int n4 = d / 4;
   float4* hrow = reinterpret_cast<float4*>(h + (size_t)r * d);
-  float4 v[kMaxV4];
   float ss = 0.f;
+  for (int i4 = tid; i4 < n4; i4 += kNT) {
+    float4 a = hrow[i4];
+    const float4* pp = reinterpret_cast<const float4*>(ws + (size_t)r * d) + i4;
+    // fixed order s = 0 .. S-1, eight partial loads in flight
+    for (int s0 = 0; s0 < S; s0 += 8) {
+      float4 p[8];
 #pragma unroll
-  for (int k = 0; k < kMaxV4; ++k) {
-    const int i4 = tid + k * kNT;
-    v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (i4 < n4) {
-      float4 p[kSplitMaxDev];
+      for (int u = 0; u < 8; ++u)
+        if (s0 + u < S) p[u] = pp[(s0 + u) * (ws_stride / 4)];
 #pragma unroll
-      for (int s = 0; s < kSplitMaxDev; ++s)
-        if (s < S) p[s] = reinterpret_cast<const float4*>(ws + s * ws_stride + (size_t)r * d)[i4];
-      float4 a = hrow[i4];
-#pragma unroll
-      for (int s = 0; s < kSplitMaxDev; ++s)
-        if (s < S) { a.x += p[s].x; a.y += p[s].y; a.z += p[s].z; a.w += p[s].w; }
-      v[k] = a;
-      ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+      for (int u = 0; u < 8; ++u)
+        if (s0 + u < S) { a.x += p[u].x; a.y += p[u].y; a.z += p[u].z; a.w += p[u].w; }
     }
+    row[i4] = a;
+    ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
   }
   const float tot = block_sum<kNT>(ss, red);
   const float rs = 1.f / sqrtf(tot / (float)d + eps);
-#pragma unroll
-  for (int k = 0; k < kMaxV4; ++k) {
-    const int i4 = tid + k * kNT;
-    if (i4 < n4) {
-      hrow[i4] = v[k];
-      norm_store<FMT>(x, r, d, i4, v[k], rs, gain);
-    }
+  for (int i4 = tid; i4 < n4; i4 += kNT) {
+    const float4 a = row[i4];
+    hrow[i4] = a;
+    norm_store<FMT>(x, r, d, i4, a, rs, gain);
   }
 }
 
@@ -242,27 +241,6 @@ __global__ void rope_table_kernel(double theta, int hd, int n_pos, float2* __res
 }
 
 // --------------------------------------------------------------- sampling
-struct Top2 {
-  float b; int i; float s;
-};
-__device__ __forceinline__ bool beats(float vb, int ib, float va, int ia) {
-  return vb > va || (vb == va && ib < ia);
-}
-__device__ __forceinline__ Top2 merge_top2(Top2 A, Top2 B) {
-  Top2 out;
-  if (beats(B.b, B.i, A.b, A.i)) {
-    out.b = B.b; out.i = B.i; out.s = fmaxf(fmaxf(A.s, B.s), A.b);
-  } else {
-    out.b = A.b; out.i = A.i; out.s = fmaxf(fmaxf(A.s, B.s), B.b);
-  }
-  return out;
-}
-__device__ __forceinline__ void merge_lse(float& m, float& l, float m2, float l2) {
-  const float M = fmaxf(m, m2);
-  if (M == -INFINITY) { m = M; l = 0.f; return; }
-  l = l * expf(m - M) + l2 * expf(m2 - M);
-  m = M;
-}
 
 // Per (chunk of the vocabulary, row): online log-sum-exp of the senior's
 // scores and the top-2 of the owner's Gumbel-perturbed scores.
@@ -444,10 +422,26 @@ __global__ __launch_bounds__(64) void sample_finish_kernel(FinishArgs a) {
   if (a.done[s]) return;
   float ms = -INFINITY, ls = 0.f;
   Top2 top{-INFINITY, 0x7FFFFFFF, -INFINITY};
-  for (int c = lane; c < a.n_chunks; c += 64) {
-    const float* p = a.partials + ((size_t)r * a.n_chunks + c) * 5;
-    merge_lse(ms, ls, p[0], p[1]);
-    top = merge_top2(top, Top2{p[2], __float_as_int(p[3]), p[4]});
+  if (a.part_sen) {
+    // the LM heads' sampling-epilogue partials: log-sum-exp from the
+    // senior's, the top two from the owner's
+    const bool own_sen = a.owner[s] != 0;
+    for (int c = lane; c < a.n_sen; c += 64) {
+      const float* p = a.part_sen + ((size_t)r * a.n_sen + c) * 5;
+      merge_lse(ms, ls, p[0], p[1]);
+      if (own_sen) top = merge_top2(top, Top2{p[2], __float_as_int(p[3]), p[4]});
+    }
+    if (!own_sen)
+      for (int c = lane; c < a.n_jun; c += 64) {
+        const float* p = a.part_jun + ((size_t)r * a.n_jun + c) * 5;
+        top = merge_top2(top, Top2{p[2], __float_as_int(p[3]), p[4]});
+      }
+  } else {
+    for (int c = lane; c < a.n_chunks; c += 64) {
+      const float* p = a.partials + ((size_t)r * a.n_chunks + c) * 5;
+      merge_lse(ms, ls, p[0], p[1]);
+      top = merge_top2(top, Top2{p[2], __float_as_int(p[3]), p[4]});
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -456,7 +450,6 @@ __global__ __launch_bounds__(64) void sample_finish_kernel(FinishArgs a) {
     Top2 B{__shfl_xor(top.b, o, 64), __shfl_xor(top.i, o, 64), __shfl_xor(top.s, o, 64)};
     top = merge_top2(top, B);
   }
-  if (lane != 0) return;
   // a row whose scores are all NaN never updates the argmax: keep the index in range
   const int y_hat = (top.i >= 0 && top.i < a.V) ? top.i : 0;
   int y = y_hat;
@@ -464,7 +457,28 @@ __global__ __launch_bounds__(64) void sample_finish_kernel(FinishArgs a) {
     const int f = a.forced[s];
     if (f >= 0 && f < a.V) y = f;
   }
-  const float sy = (a.z_sen[(size_t)r * a.V + y] + (y == a.eos_id ? a.eos_bias_sen : 0.f)) / a.temp;
+  float zy;
+  if (a.part_sen) {
+    // the senior logit of the appended token from its LM-head input row
+    // (fp16) and the bf16 LM-head row: the product the GEMM formed
+    const uint16_t* xr = a.x_sen + (size_t)r * a.d;
+    const uint16_t* wr = a.w_lm + (size_t)y * a.d;
+    float acc = 0.f;
+    for (int k = 8 * lane; k < a.d; k += 512) {
+      const uint4 xv = *reinterpret_cast<const uint4*>(xr + k);
+      const uint4 wv = *reinterpret_cast<const uint4*>(wr + k);
+      const uint32_t xw[4] = {xv.x, xv.y, xv.z, xv.w}, ww[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc += (float)__builtin_bit_cast(_Float16, (uint16_t)(xw[e] & 0xFFFFu)) * bf2f((bf16_t)(ww[e] & 0xFFFFu));
+        acc += (float)__builtin_bit_cast(_Float16, (uint16_t)(xw[e] >> 16)) * bf2f((bf16_t)(ww[e] >> 16));
+      }
+    }
+    zy = wave_sum(acc);
+  }
+  if (lane != 0) return;
+  if (!a.part_sen) zy = a.z_sen[(size_t)r * a.V + y];
+  const float sy = (zy + (y == a.eos_id ? a.eos_bias_sen : 0.f)) / a.temp;
   const float lp = sy - (ms + logf(ls));
   const int tt = a.t[s];
   const int own = a.owner[s];
@@ -644,6 +658,21 @@ __global__ __launch_bounds__(kNT) void prefill_rows_kernel(PrefillRowsArgs a) {
   if (bad) __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Gumbel noise of this step, one Philox call per four vocabulary entries.
+__global__ __launch_bounds__(kNT) void gumbel_noise_kernel(const int32_t* __restrict__ act,
+                                                           const int32_t* __restrict__ t,
+                                                           const int32_t* __restrict__ done, int V, uint32_t k0,
+                                                           uint32_t k1, float* __restrict__ noise) {
+  const int r = blockIdx.y;
+  const int s = act[r];
+  if (done[s]) return;
+  const int q = blockIdx.x * kNT + threadIdx.x;       // entries 4 q .. 4 q + 3
+  if (4 * q >= V) return;
+  const u32x4 ph = philox4x32_10(u32x4{(uint32_t)q, (uint32_t)t[s], (uint32_t)s, 0u}, k0, k1);
+  reinterpret_cast<float4*>(noise + (size_t)r * V)[q] =
+      make_float4(gumbel_fast(ph.x), gumbel_fast(ph.y), gumbel_fast(ph.z), gumbel_fast(ph.w));
+}
+
 __global__ void iota_kernel(int32_t* __restrict__ dst, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) dst[i] = i;
@@ -687,12 +716,13 @@ hipError_t launch_resid_norm(int dt, const float* ws, int S, long ws_stride, flo
                              float eps, void* x, int R, int d, bool f16_out, hipStream_t st) {
   if (R <= 0) return hipSuccess;
   if (S > kSplitMaxDev || (f16_out && dt != DT_BF16)) return hipErrorInvalidValue;
+  const size_t lds = (size_t)d * 4;           // the summed row
   if (f16_out)
-    hipLaunchKernelGGL((resid_norm_kernel<ACT_F16>), dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
+    hipLaunchKernelGGL((resid_norm_kernel<ACT_F16>), dim3(R), dim3(kNT), lds, st, ws, S, ws_stride, h, gain, eps, x, d);
   else if (dt == DT_BF16)
-    hipLaunchKernelGGL((resid_norm_kernel<ACT_SPLIT>), dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
+    hipLaunchKernelGGL((resid_norm_kernel<ACT_SPLIT>), dim3(R), dim3(kNT), lds, st, ws, S, ws_stride, h, gain, eps, x, d);
   else
-    hipLaunchKernelGGL((resid_norm_kernel<ACT_F32>), dim3(R), dim3(kNT), 0, st, ws, S, ws_stride, h, gain, eps, x, d);
+    hipLaunchKernelGGL((resid_norm_kernel<ACT_F32>), dim3(R), dim3(kNT), lds, st, ws, S, ws_stride, h, gain, eps, x, d);
   return hipGetLastError();
 }
 
@@ -786,6 +816,15 @@ hipError_t launch_scatter_rows(const float* src, const int32_t* act, int R, int 
 hipError_t launch_prefill_rows(const PrefillRowsArgs& a, hipStream_t st) {
   if (a.n <= 0) return hipSuccess;
   hipLaunchKernelGGL(prefill_rows_kernel, dim3(a.n), dim3(kNT), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gumbel_noise(const int32_t* act, const int32_t* t, const int32_t* done, int R, int V,
+                               uint32_t key0, uint32_t key1, float* noise, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (V % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gumbel_noise_kernel, dim3((V / 4 + kNT - 1) / kNT, R), dim3(kNT), 0, st, act, t, done, V, key0,
+                     key1, noise);
   return hipGetLastError();
 }
 

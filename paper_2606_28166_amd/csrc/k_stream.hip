@@ -111,10 +111,14 @@ __device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); 
 template <int MB, int NS, bool A16, int EPI>
 __global__ __launch_bounds__(256) void gemm_stream_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ Wp, int M, int N, int K, int n_groups, int S, int cps,
-    float* __restrict__ out, int ldo, long split_stride) {
+    float* __restrict__ out, int ldo, long split_stride, SampleEpiArgs smp) {
   using G = StreamShape<MB, NS, A16>;
   constexpr int PARTS = G::PARTS, NPC = G::NPC;
   __shared__ __attribute__((aligned(1024))) unsigned char ring[NS * G::ASTAGE];
+  // EPI_SAMPLE: an item's output tile (BM rows x 128 vocabulary entries,
+  // padded rows) on its way from the MFMA layout to one row per thread pair
+  constexpr int TSTR = 128 + 4;
+  __shared__ __attribute__((aligned(16))) float tile[EPI == EPI_SAMPLE ? G::BM * TSTR : 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, c32 = lane & 31;
@@ -228,8 +232,105 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(
       }
     }
   };
+  // EPI_SAMPLE running state of row ts_m over columns 64 ts_h .. + 63 of
+  // every item this workgroup takes: log-sum-exp of the scores (senior head)
+  // and the top two Gumbel-perturbed scores (rows this model owns)
+  const int ts_m = tid >> 1, ts_h = tid & 1;
+  float ts_ms = -INFINITY, ts_ls = 0.f;
+  Top2 ts_top{-INFINITY, 0x7FFFFFFF, -INFINITY};
+  bool ts_live = false, ts_own = false;
+  if (EPI == EPI_SAMPLE && ts_m < M) {
+    const int s = smp.act[ts_m];
+    ts_live = smp.done[s] == 0;
+    ts_own = (smp.owner[s] != 0 ? 1 : 0) == smp.model;
+  }
   auto epilogue = [&](const Cursor& u) {
     const int nb = u.grp * SNW + wave;                   // this wave's 32-row weight block
+    if (EPI == EPI_SAMPLE) {
+      const int v0 = u.grp * 128 + 64 * ts_h;
+      const int lim = N - v0;                            // entries of this thread's half inside the vocabulary
+      const bool sen = smp.model == 1, work = ts_live && (sen || ts_own);
+      // the first half of this thread's noise, requested before the tile
+      // goes through LDS (the second half as the first is consumed)
+      const float4* nrow = reinterpret_cast<const float4*>(smp.noise + (size_t)ts_m * N + v0);
+      auto noise4 = [&](int q) { return 4 * q < lim ? nrow[q] : make_float4(0.f, 0.f, 0.f, 0.f); };
+      float4 gn[8];
+      if (work && ts_own) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) gn[q] = noise4(q);
+      }
+      // scores s = (z + b 1[v = eos]) / T into the tile
+      const float inv_t = 1.f / smp.temp;
+      const float eb = u.grp * 128 + wave * 32 + c32 == smp.eos_id ? smp.eos_bias * inv_t : 0.f;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int m = mb * 32 + 8 * (i >> 2) + 4 * g + (i & 3);
+          tile[m * TSTR + wave * 32 + c32] = fmaf(acc[mb][i], inv_t, eb);
+          acc[mb][i] = 0.f;
+        }
+      __syncthreads();
+      if (work) {
+        // the four scores of quad q of this half (-inf past the vocabulary),
+        // read from the tile on every pass instead of held in registers
+        const float4* trow = reinterpret_cast<const float4*>(tile + ts_m * TSTR + 64 * ts_h);
+        auto quad = [&](int q, float* sc) {
+          const float4 z = trow[q];
+          sc[0] = 4 * q < lim ? z.x : -INFINITY;
+          sc[1] = 4 * q + 1 < lim ? z.y : -INFINITY;
+          sc[2] = 4 * q + 2 < lim ? z.z : -INFINITY;
+          sc[3] = 4 * q + 3 < lim ? z.w : -INFINITY;
+        };
+        if (sen) {
+          // log-sum-exp of the 64 scores, folded into the running pair
+          float mx = -INFINITY;
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            float sc[4];
+            quad(q, sc);
+            mx = fmaxf(fmaxf(mx, fmaxf(sc[0], sc[1])), fmaxf(sc[2], sc[3]));
+          }
+          if (mx > -INFINITY) {
+            const float off = -mx * 1.4426950408889634f;
+            float l0 = 0.f, l1 = 0.f;
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+              float sc[4];
+              quad(q, sc);
+              l0 += __builtin_amdgcn_exp2f(fmaf(sc[0], 1.4426950408889634f, off));
+              l1 += __builtin_amdgcn_exp2f(fmaf(sc[1], 1.4426950408889634f, off));
+              l0 += __builtin_amdgcn_exp2f(fmaf(sc[2], 1.4426950408889634f, off));
+              l1 += __builtin_amdgcn_exp2f(fmaf(sc[3], 1.4426950408889634f, off));
+            }
+            merge_lse(ts_ms, ts_ls, mx, l0 + l1);
+          }
+        }
+        if (ts_own) {
+          // top two of s + noise (ties to the smaller index), then into the running state
+          float b = -INFINITY, s2 = -INFINITY;
+          int bi = 0x7FFFFFFF;
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            const float gv[4] = {gn[q & 7].x, gn[q & 7].y, gn[q & 7].z, gn[q & 7].w};
+            if (q < 8) gn[q] = noise4(q + 8);
+            float sc[4];
+            quad(q, sc);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float val = sc[e] + gv[e];
+              const bool up = val > b;
+              s2 = up ? b : fmaxf(s2, val);
+              bi = up ? v0 + 4 * q + e : bi;
+              b = up ? val : b;
+            }
+          }
+          ts_top = merge_top2(ts_top, Top2{b, bi, s2});
+        }
+      }
+      __syncthreads();                                   // the tile is written again by the next item
+      return;
+    }
     if (EPI == EPI_SWIGLU) {
       // columns c < 16 of a block are gate sums, c + 16 the matching up sums
       // (pair-interleaved packing); output column 16 nb + c, in the input's
@@ -289,6 +390,17 @@ __global__ __launch_bounds__(256) void gemm_stream_kernel(
     }
     epilogue(cp);
   }
+  if (EPI == EPI_SAMPLE) {
+    // the two halves of each row, then one partial per (row, workgroup)
+    const float m2 = __shfl_xor(ts_ms, 1, 64), l2 = __shfl_xor(ts_ls, 1, 64);
+    merge_lse(ts_ms, ts_ls, m2, l2);
+    const Top2 B{__shfl_xor(ts_top.b, 1, 64), __shfl_xor(ts_top.i, 1, 64), __shfl_xor(ts_top.s, 1, 64)};
+    ts_top = merge_top2(ts_top, B);
+    if (ts_h == 0 && ts_m < M) {
+      float* p = smp.part + ((size_t)ts_m * smp.n_part + blockIdx.x) * 5;
+      p[0] = ts_ms; p[1] = ts_ls; p[2] = ts_top.b; p[3] = __int_as_float(ts_top.i); p[4] = ts_top.s;
+    }
+  }
 }
 
 template <int MB, bool A16, int EPI>
@@ -296,12 +408,13 @@ hipError_t run_stream(const GemmStreamArgs& a, int grid, hipStream_t st) {
   constexpr int NS = kStreamStages;
   hipLaunchKernelGGL((gemm_stream_kernel<MB, NS, A16, EPI>), dim3(grid), dim3(64 * SNW), 0, st,
                      (const bf16_t*)a.A, (const bf16_t*)a.Wp, a.M, a.N, a.K, a.n_groups, a.S, a.cps, a.out, a.ldo,
-                     a.split_stride);
+                     a.split_stride, a.smp);
   return hipGetLastError();
 }
 
 template <int MB>
 hipError_t dispatch_epi(const GemmStreamArgs& a, int grid, hipStream_t st) {
+  if (a.a16 && a.epi == EPI_SAMPLE) return run_stream<MB, true, EPI_SAMPLE>(a, grid, st);
   if (a.a16)
     return a.epi == EPI_SWIGLU ? run_stream<MB, true, EPI_SWIGLU>(a, grid, st)
                                : run_stream<MB, true, EPI_PARTIAL>(a, grid, st);
@@ -364,6 +477,9 @@ hipError_t launch_gemm_stream(const GemmStreamArgs& a, hipStream_t st) {
       a.grid < 1)
     return hipErrorInvalidValue;
   if (a.epi == EPI_SWIGLU && (a.S != 1 || a.N % 32)) return hipErrorInvalidValue;
+  if (a.epi == EPI_SAMPLE && (a.S != 1 || !a.a16 || a.N % 4 || !a.smp.noise || !a.smp.part || !a.smp.act ||
+                              !a.smp.owner || !a.smp.done || a.smp.n_part < std::min(a.grid, a.n_groups)))
+    return hipErrorInvalidValue;
   const int grid = std::min(a.grid, a.n_groups * a.S);
   if (a.M <= 32) return dispatch_epi<1>(a, grid, st);
   if (a.M <= 64) return dispatch_epi<2>(a, grid, st);

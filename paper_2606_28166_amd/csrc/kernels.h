@@ -7,7 +7,24 @@
 namespace tandem {
 
 enum DType { DT_BF16 = 0, DT_F32 = 1 };
-enum Epi { EPI_PARTIAL = 0, EPI_STORE = 1, EPI_SWIGLU = 2 };
+enum Epi { EPI_PARTIAL = 0, EPI_STORE = 1, EPI_SWIGLU = 2, EPI_SAMPLE = 3 };
+
+// The sampling epilogue of a decode LM head on the streaming GEMM
+// (EPI_SAMPLE): instead of storing the logits z[r][v] it folds each
+// workgroup's vocabulary entries into per-row partials, part[r][wg][5] =
+// (max, sum of e^(s - max)) of the scores s = (z + b 1[v = eos]) / T (senior
+// head only), and the top two of s + noise[r][v] with the best index, for
+// the rows this model owns (owner[act[r]] == model).  wg < the launch grid.
+struct SampleEpiArgs {
+  const float* noise;          // [R][V] Gumbel noise of this step
+  const int32_t* act;          // [R] sequence of each row
+  const int32_t* owner;        // by sequence: 1 = senior
+  const int32_t* done;         // by sequence
+  int model;                   // 1: senior head (log-sum-exp of every row), 0: junior head
+  float temp; int eos_id; float eos_bias;
+  float* part;                 // [R][n_part][5]
+  int n_part;                  // partials per row (>= the launch grid)
+};
 
 // C[M x N] = A[M x K] . W[N x K]^T, A fp32, W in the weight dtype.
 //   EPI_PARTIAL: split-K partial sums to out + split * split_stride, row stride ldo
@@ -74,6 +91,7 @@ struct GemmStreamArgs {
   int ldo;
   long split_stride;
   int nbw, S, cps, n_groups, grid;
+  SampleEpiArgs smp;      // EPI_SAMPLE (a16, S = 1)
 };
 hipError_t launch_gemm_stream(const GemmStreamArgs& a, hipStream_t st);
 
@@ -159,6 +177,13 @@ struct SampleArgs {
 };
 hipError_t launch_sample_partials(const SampleArgs& a, int n_chunks, hipStream_t st);
 
+// Gumbel noise of this step for launched rows 0 .. R-1 that are not done:
+// noise[r][v] = -log(-log u) of the token stream's Philox word for (seed,
+// sequence act[r], step t, v) (the same words sample_partials draws).
+// V % 4 == 0.
+hipError_t launch_gumbel_noise(const int32_t* act, const int32_t* t, const int32_t* done, int R, int V,
+                               uint32_t key0, uint32_t key1, float* noise, hipStream_t st);
+
 struct FinishArgs {
   const float* z_sen; int R, V;           // logits by row
   const int32_t* act;                     // [R] sequence of each row (state and outputs by sequence)
@@ -172,6 +197,13 @@ struct FinishArgs {
   int32_t* out_tok; uint8_t* out_own; float* out_lp; int32_t* out_len; int ld_out;
   int32_t* dbg_sampled; float* dbg_margin;
   int32_t* n_active;                          // device counter or NULL
+  // Sampling-epilogue partials instead of the logits (part_sen != NULL):
+  // the senior head's n_sen partials per row (log-sum-exp, and top two for
+  // senior-owned rows), the junior head's n_jun (top two for junior-owned
+  // rows); the chosen token's senior score is recomputed from the senior's
+  // LM-head input rows x_sen (fp16 [R][d]) and its bf16 LM head w_lm [V][d].
+  const float* part_sen; int n_sen; const float* part_jun; int n_jun;
+  const uint16_t* x_sen; const uint16_t* w_lm; int d;
 };
 hipError_t launch_sample_finish(const FinishArgs& a, hipStream_t st);
 

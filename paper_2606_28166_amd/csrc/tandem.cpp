@@ -29,6 +29,7 @@ thread_local std::string g_err = "no error";
 
 constexpr int kSplitMax = 16;         // split-K slices of a decode projection
 constexpr int kVocabChunk = 4096;     // vocabulary entries per sampling workgroup
+constexpr int kSampleParts = 1024;    // partials per row of the LM heads' sampling epilogue (>= their grid)
 constexpr int kCompactEvery = 32;     // decode steps between compactions of the batch (EOS runs)
 constexpr int kCompactBucket = 32;    // the launched row count is a multiple of this
 constexpr size_t kAlign = 256;
@@ -91,6 +92,12 @@ struct Plan {
   size_t off_pfx;             // shared-prefix tables of the decode rows (2 x max_seqs int32)
   size_t off_err;             // the batch's token-range error flag (int32)
   size_t off_score;           // dual-distribution score partials [max_seqs][n_chunks][6]
+  // Sampling inside the LM heads (both models' LM heads run as fp16 streaming
+  // GEMMs): the step's Gumbel noise [noise_rows][vocab] and each head's
+  // per-workgroup partials [noise_rows][kSampleParts][5]
+  bool fused;
+  int noise_rows;
+  size_t off_noise, off_part_sen, off_part_jun;
   size_t scratch_bytes;
 };
 
@@ -227,6 +234,13 @@ Plan make_plan(const tandem_model_cfg* sen, const tandem_model_cfg* jun, const t
   P.off_drows = sc; sc = align_up(sc + 4 * S * 4, kAlign);
   P.off_pfx = sc; sc = align_up(sc + 2 * S * 4, kAlign);
   P.off_score = sc; sc = align_up(sc + S * P.n_chunks * 6 * 4, kAlign);
+  P.fused = sen->vocab % 4 == 0;
+  for (int i = 0; i < P.nm; ++i) P.fused = P.fused && packs(cf[i], cf[i]->vocab, cf[i]->d_model);
+  P.noise_rows = P.fused ? (int)std::min<size_t>(S, kStreamMaxRows) : 0;
+  const size_t NR = (size_t)P.noise_rows;
+  P.off_noise = sc; sc = align_up(sc + NR * sen->vocab * 4, kAlign);
+  P.off_part_sen = sc; sc = align_up(sc + NR * kSampleParts * 5 * 4, kAlign);
+  P.off_part_jun = sc; sc = align_up(sc + (P.nm == 2 ? NR : 0) * kSampleParts * 5 * 4, kAlign);
   P.scratch_bytes = sc;
   return P;
 }
@@ -287,6 +301,13 @@ struct tandem_handle {
   int32_t* h_stage = nullptr;
   hipEvent_t ev_stage = nullptr;
   float* partials;
+  // Sampling inside the LM heads (see Plan::fused): noise and partials, the
+  // event that orders the noise before the senior's LM head, and whether the
+  // last step sampled this way (its logits were then never stored)
+  bool fused = false;
+  float *noise = nullptr, *part_sen = nullptr, *part_jun = nullptr;
+  hipEvent_t ev_noise = nullptr;
+  bool last_fused = false;
   int32_t* d_count;
   int32_t* h_sync = nullptr;  // pinned: [0] a count read back, [1] the error flag
   int n_seq = 0;
@@ -558,17 +579,54 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   return TANDEM_OK;
 }
 
-tandem_status forward_head(tandem_handle* h, Model& m, const FwdRows& fr, hipStream_t st) {
+// The LM head's launch plan on the streaming GEMM (one K slice, plain or
+// sampling epilogue); its grid is the number of sampling partials per row.
+StreamPlan head_plan(const tandem_handle* h, const Model& m, int R) {
+  return plan_stream_gemm(R, m.cfg.vocab, m.cfg.d_model, h->n_cu, m.p.ws_floats, kPlanStore);
+}
+
+// The LM head of model i (0 senior, 1 junior): logits [R][V], or, when the
+// step samples inside the LM heads, per-row sampling partials (the senior's
+// head waits for the step's noise, ev_noise, when that was launched on
+// another stream).
+tandem_status forward_head(tandem_handle* h, int i, const FwdRows& fr, bool fused, hipStream_t st,
+                           hipEvent_t wait_noise = nullptr) {
+  Model& m = h->m[i];
   const tandem_model_cfg& c = m.cfg;
   int S = 1;
-  CALL(gemm(h, m, m.xa, m.lm_head, m.p_lm, fr.R, c.vocab, c.d_model, EPI_STORE, m.logits, &S, st, m.lm16));
+  if (!fused) {
+    CALL(gemm(h, m, m.xa, m.lm_head, m.p_lm, fr.R, c.vocab, c.d_model, EPI_STORE, m.logits, &S, st, m.lm16));
+    return TANDEM_OK;
+  }
+  if (wait_noise) HIPCHK(hipStreamWaitEvent(st, wait_noise, 0));
+  const StreamPlan pl = head_plan(h, m, fr.R);
+  GemmStreamArgs a{};
+  a.A = m.xa; a.Wp = m.p_lm; a.M = fr.R; a.N = c.vocab; a.K = c.d_model; a.a16 = true; a.epi = EPI_SAMPLE;
+  a.ldo = c.vocab;
+  a.nbw = pl.nbw; a.S = pl.S; a.cps = pl.cps; a.n_groups = pl.n_groups; a.grid = pl.grid;
+  SampleEpiArgs& sm = a.smp;
+  sm.noise = h->noise; sm.act = h->act; sm.owner = h->owner; sm.done = h->done;
+  sm.model = i == 0 ? 1 : 0;
+  sm.temp = h->smp.temperature; sm.eos_id = h->smp.eos_id;
+  sm.eos_bias = i == 0 ? h->smp.eos_bias_senior : h->smp.eos_bias_junior;
+  sm.part = i == 0 ? h->part_sen : h->part_jun;
+  sm.n_part = pl.grid;
+  TIMED(TANDEM_K_GEMM, launch_gemm_stream(a, st));
   return TANDEM_OK;
 }
 
-tandem_status forward(tandem_handle* h, Model& m, const FwdRows& fr, bool lm_head, hipStream_t st) {
+// This step's Gumbel noise for the sampling inside the LM heads.
+tandem_status launch_noise(tandem_handle* h, int R, hipStream_t st) {
+  TIMED(TANDEM_K_SAMPLE, launch_gumbel_noise(h->act, h->t, h->done, R, h->m[0].cfg.vocab, h->key0, h->key1,
+                                             h->noise, st));
+  return TANDEM_OK;
+}
+
+tandem_status forward(tandem_handle* h, int i, const FwdRows& fr, bool lm_head, bool fused, hipStream_t st) {
+  Model& m = h->m[i];
   CALL(forward_embed(h, m, fr, st));
   for (int l = 0; l < m.cfg.n_layers; ++l) CALL(forward_layer(h, m, l, fr, st));
-  if (lm_head) CALL(forward_head(h, m, fr, st));
+  if (lm_head) CALL(forward_head(h, i, fr, fused, st));
   return TANDEM_OK;
 }
 
@@ -581,16 +639,24 @@ tandem_status forward(tandem_handle* h, Model& m, const FwdRows& fr, bool lm_hea
 // The turn order interleaves the layers evenly (layer l of a model with L
 // layers at (l + 1/2) / L); an attention waits for the previous attention of
 // the other model in that order.
-tandem_status forward_pair(tandem_handle* h, const FwdRows& fr, bool lm_head) {
+//
+// With the sampling inside the LM heads (fused), the step's Gumbel noise is
+// generated first on the junior's stream (whose chain is the shorter one) and
+// the senior's LM head waits for it.
+tandem_status forward_pair(tandem_handle* h, const FwdRows& fr, bool lm_head, bool fused = false) {
   hipStream_t st = h->stream;
-  if (h->nm == 1) return forward(h, h->m[0], fr, lm_head, st);
-  if (h->timing & TANDEM_TIMING_SERIAL) {
-    for (int i = 0; i < 2; ++i) CALL(forward(h, h->m[i], fr, lm_head, st));
+  if (h->nm == 1 || (h->timing & TANDEM_TIMING_SERIAL)) {
+    if (fused) CALL(launch_noise(h, fr.R, st));
+    for (int i = 0; i < h->nm; ++i) CALL(forward(h, i, fr, lm_head, fused, st));
     return TANDEM_OK;
   }
   HIPCHK(hipEventRecord(h->ev_fork, st));
   HIPCHK(hipStreamWaitEvent(h->side, h->ev_fork, 0));
   hipStream_t sts[2] = {st, h->side};
+  if (fused) {
+    CALL(launch_noise(h, fr.R, sts[1]));
+    HIPCHK(hipEventRecord(h->ev_noise, sts[1]));
+  }
   Model* ms[2] = {&h->m[0], &h->m[1]};
   {
     const int L[2] = {ms[0]->cfg.n_layers, ms[1]->cfg.n_layers};
@@ -610,8 +676,8 @@ tandem_status forward_pair(tandem_handle* h, const FwdRows& fr, bool lm_head) {
       prev_layer = l;
     }
     if (lm_head) {
-      CALL(forward_head(h, *ms[1], fr, sts[1]));
-      CALL(forward_head(h, *ms[0], fr, sts[0]));
+      CALL(forward_head(h, 1, fr, fused, sts[1]));
+      CALL(forward_head(h, 0, fr, fused, sts[0], fused ? h->ev_noise : nullptr));
     }
   }
   HIPCHK(hipEventRecord(h->ev_join, h->side));
@@ -620,7 +686,8 @@ tandem_status forward_pair(tandem_handle* h, const FwdRows& fr, bool lm_head) {
 }
 
 // Enqueue one decode step (both forwards, sampling, outputs, handoff rule).
-tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg) {
+// fused: sample inside the LM heads (no logits stored; see step_fused).
+tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_debug* dbg, bool fused) {
   const int R = h->R_launch;
   hipStream_t st = h->stream;
   {
@@ -631,24 +698,30 @@ tandem_status record_step(tandem_handle* h, const int32_t* forced, const tandem_
     TIMED(TANDEM_K_OTHER, launch_gather_rows(ga, st));
     FwdRows fr{R, h->drow_tok, h->drow_slot, h->drow_pos, h->drow_done};
     fr.shared_prefix = h->share;
-    tandem_status s = forward_pair(h, fr, true);
+    tandem_status s = forward_pair(h, fr, true, fused);
     if (s != TANDEM_OK) return s;
   }
   const int V = h->m[0].cfg.vocab;
-  SampleArgs sa{};
-  sa.z_sen = h->m[0].logits; sa.z_jun = h->m[h->nm - 1].logits; sa.R = R; sa.V = V;
-  sa.temp = h->smp.temperature; sa.eos_id = h->smp.eos_id;
-  sa.eos_bias_sen = h->smp.eos_bias_senior; sa.eos_bias_jun = h->smp.eos_bias_junior;
-  sa.key0 = h->key0; sa.key1 = h->key1;
-  sa.owner = h->owner; sa.t = h->t; sa.done = h->done; sa.act = h->act;
-  sa.partials = h->partials; sa.chunk = kVocabChunk;
-  TIMED(TANDEM_K_SAMPLE, launch_sample_partials(sa, h->plan.n_chunks, st));
-  if (dbg) {
-    if (dbg->logits_senior) HIPCHK(launch_scatter_rows(h->m[0].logits, h->act, R, V, dbg->logits_senior, st));
-    if (dbg->logits_junior && h->nm == 2)
-      HIPCHK(launch_scatter_rows(h->m[1].logits, h->act, R, V, dbg->logits_junior, st));
-  }
   FinishArgs fa{};
+  if (fused) {
+    fa.part_sen = h->part_sen; fa.n_sen = head_plan(h, h->m[0], R).grid;
+    fa.part_jun = h->part_jun; fa.n_jun = head_plan(h, h->m[h->nm - 1], R).grid;
+    fa.x_sen = (const uint16_t*)h->m[0].xa; fa.w_lm = (const uint16_t*)h->m[0].lm_head; fa.d = h->m[0].cfg.d_model;
+  } else {
+    SampleArgs sa{};
+    sa.z_sen = h->m[0].logits; sa.z_jun = h->m[h->nm - 1].logits; sa.R = R; sa.V = V;
+    sa.temp = h->smp.temperature; sa.eos_id = h->smp.eos_id;
+    sa.eos_bias_sen = h->smp.eos_bias_senior; sa.eos_bias_jun = h->smp.eos_bias_junior;
+    sa.key0 = h->key0; sa.key1 = h->key1;
+    sa.owner = h->owner; sa.t = h->t; sa.done = h->done; sa.act = h->act;
+    sa.partials = h->partials; sa.chunk = kVocabChunk;
+    TIMED(TANDEM_K_SAMPLE, launch_sample_partials(sa, h->plan.n_chunks, st));
+    if (dbg) {
+      if (dbg->logits_senior) HIPCHK(launch_scatter_rows(h->m[0].logits, h->act, R, V, dbg->logits_senior, st));
+      if (dbg->logits_junior && h->nm == 2)
+        HIPCHK(launch_scatter_rows(h->m[1].logits, h->act, R, V, dbg->logits_junior, st));
+    }
+  }
   fa.z_sen = h->m[0].logits; fa.R = R; fa.V = V; fa.act = h->act;
   fa.temp = h->smp.temperature; fa.eos_id = h->smp.eos_id; fa.eos_bias_sen = h->smp.eos_bias_senior;
   fa.partials = h->partials; fa.n_chunks = h->plan.n_chunks;
@@ -710,13 +783,21 @@ tandem_status maybe_compact(tandem_handle* h) {
   return prefix_tables(h);            // the act order changed
 }
 
+// Whether a step samples inside the LM heads: the handle's models allow it,
+// the launched rows fit one streaming tile, the caller asked for no logits and
+// has not switched the fusion off (TANDEM_TIMING_SEPARATE_SAMPLE).
+bool step_fused(const tandem_handle* h, const tandem_debug* dbg) {
+  return h->fused && h->R_launch <= h->plan.noise_rows && !(h->timing & TANDEM_TIMING_SEPARATE_SAMPLE) &&
+         !(dbg && (dbg->logits_senior || dbg->logits_junior));
+}
+
 // Capture the step into h->graph (the streams return to normal operation
 // whatever happens inside).
 tandem_status capture_step(tandem_handle* h) {
   hipStream_t caller = h->stream;
   HIPCHK(hipStreamBeginCapture(h->gstream, hipStreamCaptureModeThreadLocal));
   h->stream = h->gstream;                 // the step's main stream while recording
-  tandem_status s = record_step(h, nullptr, nullptr);
+  tandem_status s = record_step(h, nullptr, nullptr, step_fused(h, nullptr));
   h->stream = caller;
   hipGraph_t graph = nullptr;
   hipError_t e = hipStreamEndCapture(h->gstream, &graph);
@@ -761,10 +842,11 @@ tandem_status step_impl(tandem_handle* h, const int32_t* forced, const tandem_de
     HIPCHK(hipEventRecord(h->ev_out, h->gstream));
     HIPCHK(hipStreamWaitEvent(st, h->ev_out, 0));
   } else {
-    tandem_status s = record_step(h, forced, dbg);
+    tandem_status s = record_step(h, forced, dbg, step_fused(h, dbg));
     if (s != TANDEM_OK) return s;
   }
   h->stepped = true;
+  h->last_fused = step_fused(h, dbg);
   if (n_active) {
     HIPCHK(launch_count_active(h->done, h->n_seq, h->d_count, st));
     CALL(sync_read(h, h->d_count));
@@ -943,6 +1025,11 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   int32_t* drows = (int32_t*)(sc + P.off_drows);
   h->drow_tok = drows; h->drow_slot = drows + S; h->drow_pos = drows + 2 * S; h->drow_done = drows + 3 * S;
   h->score_part = (float*)(sc + P.off_score);
+  if (P.fused) {
+    h->noise = (float*)(sc + P.off_noise);
+    h->part_sen = (float*)(sc + P.off_part_sen);
+    h->part_jun = nm == 2 ? (float*)(sc + P.off_part_jun) : h->part_sen;
+  }
   int32_t* pfx = (int32_t*)(sc + P.off_pfx);
   h->row_lo = pfx; h->pfx_slot = pfx + S;
 
@@ -956,6 +1043,7 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
       for (hipEvent_t ev : h->ev_att[i]) (void)hipEventDestroy(ev);
     if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
     if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+    if (h->ev_noise) (void)hipEventDestroy(h->ev_noise);
     if (h->side) (void)hipStreamDestroy(h->side);
     if (h->ev_in) (void)hipEventDestroy(h->ev_in);
     if (h->ev_out) (void)hipEventDestroy(h->ev_out);
@@ -983,6 +1071,9 @@ tandem_status tandem_init(const tandem_model* senior, const tandem_model* junior
   if (e != hipSuccess) { h->ev_fork = nullptr; return bail(e, "fork event"); }
   e = hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming);
   if (e != hipSuccess) { h->ev_join = nullptr; return bail(e, "join event"); }
+  e = hipEventCreateWithFlags(&h->ev_noise, hipEventDisableTiming);
+  if (e != hipSuccess) { h->ev_noise = nullptr; return bail(e, "noise event"); }
+  h->fused = P.fused && h->n_cu <= kSampleParts;
   e = hipStreamCreateWithFlags(&h->gstream, hipStreamNonBlocking);
   if (e != hipSuccess) { h->gstream = nullptr; return bail(e, "graph stream"); }
   e = hipEventCreateWithFlags(&h->ev_in, hipEventDisableTiming);
@@ -1170,7 +1261,14 @@ tandem_status tandem_score_step(tandem_handle* h, float* scores) {
     return fail(&h->err, TANDEM_E_STATE, "tandem_score_step before a step of the current batch");
   if (h->nm != 2) return fail(&h->err, TANDEM_E_STATE, "tandem_score_step needs a junior (the handle has none)");
   // the step's rows: its act order, launched row count, done-at-start flags and
-  // logits are all still in place (compaction runs at the start of a step)
+  // LM-head input rows are all still in place (compaction runs at the start of
+  // a step); a step that sampled inside the LM heads stored no logits, so the
+  // two heads run again here
+  if (h->last_fused) {
+    hipStream_t st = h->stream;
+    FwdRows fr{h->R_launch, h->drow_tok, h->drow_slot, h->drow_pos, h->drow_done};
+    for (int i = 0; i < 2; ++i) CALL(forward_head(h, i, fr, false, st));
+  }
   ScoreArgs a{};
   a.z_sen = h->m[0].logits; a.z_jun = h->m[1].logits; a.R = h->R_launch; a.V = h->m[0].cfg.vocab;
   a.act = h->act; a.row_done = h->drow_done; a.tok = h->pending;
@@ -1201,7 +1299,8 @@ tandem_status tandem_timing_enable(tandem_handle* h, int32_t class_mask) {
   if (!h) return fail(nullptr, TANDEM_E_ARG, "handle is NULL");
   if (h->poisoned) return fail(&h->err, TANDEM_E_STATE, "handle is poisoned by an earlier HIP error");
   HIPCHK(hipStreamSynchronize(h->stream));
-  h->timing = class_mask & (((1 << TANDEM_K_CLASSES) - 1) | TANDEM_TIMING_SERIAL | TANDEM_TIMING_EAGER);
+  h->timing = class_mask & (((1 << TANDEM_K_CLASSES) - 1) | TANDEM_TIMING_SERIAL | TANDEM_TIMING_EAGER |
+                            TANDEM_TIMING_SEPARATE_SAMPLE);
   h->ev_used = 0;
   h->ev_marks.clear();
   for (int k = 0; k < TANDEM_K_CLASSES; ++k) {
@@ -1233,6 +1332,7 @@ void tandem_destroy(tandem_handle* h) {
     for (hipEvent_t e : h->ev_att[i]) (void)hipEventDestroy(e);
   if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+  if (h->ev_noise) (void)hipEventDestroy(h->ev_noise);
   if (h->side) (void)hipStreamDestroy(h->side);
   if (h->ev_in) (void)hipEventDestroy(h->ev_in);
   if (h->ev_out) (void)hipEventDestroy(h->ev_out);

@@ -106,11 +106,12 @@ def run(wl: W.Workload, steps: Optional[int] = None, logits_at: Sequence[int] = 
     return Parity(ref, out, sampled, margin, logits, st, steps, rows)
 
 
-def free_run(eng, prompts, G: int, steps: int, eager: bool) -> Dict[str, np.ndarray]:
+def free_run(eng, prompts, G: int, steps: int, eager: bool, flags: int = 0) -> Dict[str, np.ndarray]:
     """Prefill and `steps` free-running tandem_step calls on an engine, replayed
-    from the step graph (eager=False) or launched kernel by kernel."""
+    from the step graph (eager=False) or launched kernel by kernel; flags: more
+    tandem_timing_enable flags for these steps."""
     from paper_2606_28166_amd import _lib as L
-    eng.timing(L.TIMING_EAGER if eager else 0)
+    eng.timing((L.TIMING_EAGER if eager else 0) | flags)
     eng.prefill(prompts, G)
     for _ in range(steps):
         eng.step()

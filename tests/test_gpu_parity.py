@@ -121,6 +121,53 @@ def test_dual_distribution_scores(shape):
     P.log(f"  max |dscore| {worst:.2e}")
 
 
+def test_sampling_inside_lm_heads_against_separate_pass():
+    """At the Qwen shapes (both LM heads on fp16 streaming GEMMs) the step
+    samples inside the LM-head GEMMs by default; with
+    TANDEM_TIMING_SEPARATE_SAMPLE it stores the logits and samples in a pass
+    over them.  Both free-running streams (graph replays) match the
+    free-running oracle up to each row's first in-band step, agree with each
+    other wherever their tokens agree (senior log-probs within 1e-3: the two
+    sum the log-sum-exp in different orders and form the appended token's
+    senior score differently), and the dual-distribution scores after a step
+    that stored no logits (both LM heads run again) equal those after a step
+    that did."""
+    from paper_2606_28166_amd import _lib as L
+    from paper_2606_28166_amd.engine import TandemEngine
+    from oracle.rollout import rollout, build_models
+    P.log("case sampling inside the LM heads vs the separate pass (Qwen shapes, 2+2 layers, 8 rows, 16 steps)")
+    wl = _qwen_reduced().replace(n_prompts=2)
+    steps = 16
+    wl.sample.max_new = steps
+    ws, wj, prompts, bnd = W.make_all(wl)
+    sen, jun = build_models(wl, ws, wj)
+    ref = rollout(sen, jun, prompts, wl.group, wl.switch, wl.sample, wl.philox_seed, bnd)
+    n = wl.n_seqs
+    eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed, max_seqs=n,
+                       max_ctx=max(len(p) for p in prompts) - 1 + steps, boundary_words=W.boundary_bits(bnd))
+    runs = {}
+    for name, flags in (("fused", 0), ("separate", L.TIMING_SEPARATE_SAMPLE)):
+        runs[name] = P.free_run(eng, prompts, wl.group, steps, eager=False, flags=flags)
+        first, full, cmp = P.first_divergence(runs[name], ref, np.arange(n), steps)
+        P.log(f"  {name}: {full}/{n} rows identical to the oracle, {cmp} tokens compared, first divergence {first}")
+    a, b = runs["fused"], runs["separate"]
+    worst = 0.0
+    for s in range(n):
+        same = int(np.argmax(a["tokens"][s] != b["tokens"][s])) if (a["tokens"][s] != b["tokens"][s]).any() else steps
+        np.testing.assert_allclose(a["logprob"][s, :same], b["logprob"][s, :same], rtol=0, atol=1e-3)
+        if same:
+            worst = max(worst, float(np.abs(a["logprob"][s, :same] - b["logprob"][s, :same]).max()))
+    P.log(f"  max |dlogprob| fused vs separate {worst:.2e}")
+    scores = []
+    for flags in (0, L.TIMING_SEPARATE_SAMPLE):
+        eng.timing(flags)
+        eng.prefill(prompts, wl.group)
+        eng.step_forced(ref.tokens[:, 0], debug=False)
+        scores.append(eng.score()[:n].cpu().numpy())
+    eng.close()
+    np.testing.assert_allclose(scores[0], scores[1], rtol=0, atol=1e-4)
+
+
 def test_second_prefill_on_one_handle():
     """A handle takes a new batch of another shape: a first batch (2 prompts x
     G=4) runs 20 graph-replayed steps, then 3 ragged prompts x G=3 are prefilled
