@@ -39,6 +39,9 @@ WRITE_SIZE, each in a run of its own):
     rocprofv3 --pmc FETCH_SIZE -d <dir> -o fetch --output-format csv -- python3 bench.py --pmc-run
     rocprofv3 --pmc WRITE_SIZE -d <dir> -o write --output-format csv -- python3 bench.py --pmc-run
     python3 bench.py --pmc-analyze <fetch csv> <write csv>
+(--pmc-warm N on all three: N graph-replayed steps before the measured ones,
+1000 by default so that the attention reads mid-rollout contexts; 0 for the
+other classes.)
 """
 from __future__ import annotations
 
@@ -174,14 +177,21 @@ CSRC = os.path.join(ROOT, "paper_2606_28166_amd", "csrc")
 PMC_COPY_BYTES = 1 << 30
 PMC_WARM = 1000          # graph-replayed steps first: contexts ~1255 .. 1279 in the measured steps
 PMC_STEPS = 24
-# kernel classes of the decode step: (name, kernel-name substring, source file)
+# kernel classes of the decode step at the Qwen shapes (128 rows): (name,
+# kernel-name substring, source file)
 PMC_CLASSES = (("attention", "attn_rows_kernel", "k_attn.hip"),
-               ("projections", "gemm_stream_kernel", "k_stream.hip"),
-               ("resid_norm", "resid_norm_kernel", "k_misc.hip"),
+               ("qkv_o", "gemm_stream_kernel<4, 4, false, 0>", "k_stream.hip"),
+               ("ffn_partial", "gemm_stream_kernel<4, 4, true, 0>", "k_stream.hip"),
+               ("gate_up_swiglu", "gemm_stream_kernel<4, 4, true, 2>", "k_stream.hip"),
+               ("lm_heads", "gemm_stream_kernel<4, 4, true, 3>", "k_stream.hip"),
+               ("resid_norm_split", "resid_norm_kernel<1>", "k_misc.hip"),
+               ("resid_norm_f16", "resid_norm_kernel<2>", "k_misc.hip"),
                ("qkv_post", "qkv_post_kernel", "k_misc.hip"),
                ("swiglu_finish", "swiglu_finish_kernel", "k_misc.hip"),
+               ("gumbel_noise", "gumbel_noise_kernel", "k_misc.hip"),
+               ("sample_finish", "sample_finish_kernel", "k_misc.hip"),
                ("sample_partials", "sample_partials_kernel", "k_misc.hip"))
-PMC_REGEX = "attn_rows|gemm_stream|resid_norm|qkv_post|swiglu_finish|sample_partials|copy"
+PMC_REGEX = "attn_rows|gemm_stream|resid_norm|qkv_post|swiglu_finish|gumbel_noise|sample_finish|sample_partials|copy"
 
 
 def source_digest(name: str) -> str:
@@ -206,11 +216,12 @@ def measured_traffic_ratio():
         return None
 
 
-def pmc_run() -> None:
+def pmc_run(warm: int = PMC_WARM) -> None:
     """The program the counter passes profile: a 1 GiB device copy (what
     FETCH_SIZE / WRITE_SIZE report for exactly that many bytes read and
-    written), PMC_WARM decode steps of the Qwen-shaped rollout replayed from
-    the step graph (the contexts reach the middle of the 2048-token rollout),
+    written), `warm` decode steps of the Qwen-shaped rollout replayed from
+    the step graph (1000: the contexts reach the middle of the 2048-token
+    rollout; 0 for the classes whose traffic does not depend on the context),
     a second, 4 MiB copy that marks where the measured steps begin, then
     PMC_STEPS decode steps launched from the host (one dispatch per kernel)."""
     import torch
@@ -225,7 +236,7 @@ def pmc_run() -> None:
     torch.cuda.synchronize()
     del x, y
     wl = W.workload("qwen")
-    wl.sample.max_new = PMC_WARM + PMC_STEPS + 8       # every row still runs in the measured steps
+    wl.sample.max_new = warm + PMC_STEPS + 8           # every row still runs in the measured steps
     ws, wj, prompts, bnd = W.make_all(wl)
     print("pmc: weights generated", flush=True)
     eng = TandemEngine(wl.senior, ws, wl.junior, wj, wl.switch, wl.sample, wl.philox_seed,
@@ -236,7 +247,7 @@ def pmc_run() -> None:
     eng.prefill(prompts, wl.group)
     torch.cuda.synchronize()
     print("pmc: prefill done", flush=True)
-    for t in range(PMC_WARM):
+    for t in range(warm):
         eng.step()
         if (t + 1) % 250 == 0:
             torch.cuda.synchronize()
@@ -254,19 +265,35 @@ def pmc_run() -> None:
     print("pmc run done", flush=True)
 
 
-def pmc_analyze(fetch_csv: str, write_csv: str) -> dict:
+def class_weight_bytes(wl: W.Workload) -> dict:
+    """Weight bytes each streaming-GEMM class of one decode step reads, both
+    models (bf16): split-activation QKV and O; the fp16 split-K products (the
+    down projections, and the gate/up of an FFN narrower than 8192); the
+    gate/up products with the SwiGLU epilogue; the two LM heads."""
+    out = {"qkv_o": 0, "ffn_partial": 0, "gate_up_swiglu": 0, "lm_heads": 0}
+    for s in (wl.senior, wl.junior):
+        d, hd, F = s.d_model, s.head_dim, s.ffn_dim
+        out["qkv_o"] += 2 * s.n_layers * (d * (s.n_q_heads + 2 * s.n_kv_heads) * hd + s.n_q_heads * hd * d)
+        out["ffn_partial"] += 2 * s.n_layers * F * d
+        out["ffn_partial" if F < 8192 else "gate_up_swiglu"] += 2 * s.n_layers * 2 * F * d
+        out["lm_heads"] += 2 * s.vocab * d
+    return out
+
+
+def pmc_analyze(fetch_csv: str, write_csv: str, warm: int = PMC_WARM) -> dict:
     """Per kernel class, the HBM bytes of the measured steps' dispatches
     (counter KiB x copy bytes / copy counter KiB) against the algorithmic
     bytes of that class: the K/V context for decode attention (a shared
-    prompt prefix once per group), both models' weights for the projections
-    and LM heads, both models' fp32 logits for the sampling pass; the split-K
-    reductions have none of their own (their bytes are reported per step and
-    as a fraction of the weight bytes)."""
+    prompt prefix once per group), the weights each GEMM class streams (the
+    LM heads' sampling epilogue also reads one row of Gumbel noise per row,
+    R x V x 4 bytes, counted apart), the noise the noise kernel writes; the
+    split-K reductions and the other helpers have none of their own (their
+    bytes are reported per step and as a fraction of all weight bytes)."""
     import csv
     wl = W.workload("qwen")
     plens = [wl.prompt_len] * wl.n_prompts
     res = {"copy_bytes": PMC_COPY_BYTES, "prompt_len": wl.prompt_len,
-           "decode_steps": [PMC_WARM + 1, PMC_WARM + PMC_STEPS], "classes": {}}
+           "decode_steps": [warm + 1, warm + PMC_STEPS], "classes": {}}
     per = {}
     for name, path in (("fetch", fetch_csv), ("write", write_csv)):
         rows = sorted((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"]))
@@ -282,10 +309,12 @@ def pmc_analyze(fetch_csv: str, write_csv: str) -> dict:
             vals = [v * scale for i, k, v in rows if i > marker and sub in k]
             per.setdefault(cname, {})[name] = (sum(vals), len(vals))
     kv = kv_bytes_per_token(wl.senior) + kv_bytes_per_token(wl.junior)
-    t0, t1 = PMC_WARM + 1, PMC_WARM + PMC_STEPS
+    t0, t1 = warm + 1, warm + PMC_STEPS
     alg = {"attention": sum(kv * _context_positions(wl, plens, t)[1] for t in range(t0, t1 + 1)),
-           "projections": PMC_STEPS * (weight_bytes(wl.senior) + weight_bytes(wl.junior)),
+           "gumbel_noise": PMC_STEPS * wl.n_seqs * wl.senior.vocab * 4,
            "sample_partials": PMC_STEPS * 2 * wl.n_seqs * wl.senior.vocab * 4}
+    for k, v in class_weight_bytes(wl).items():
+        alg[k] = PMC_STEPS * v
     wbytes = PMC_STEPS * (weight_bytes(wl.senior) + weight_bytes(wl.junior))
     for cname, sub, srcf in PMC_CLASSES:
         (fb, fn), (wb, wn) = per[cname]["fetch"], per[cname]["write"]
@@ -293,7 +322,7 @@ def pmc_analyze(fetch_csv: str, write_csv: str) -> dict:
             continue                              # not collected in these passes
         if fn != wn:
             raise SystemExit(f"{cname}: {fn} fetch dispatches against {wn} write dispatches")
-        c = {"kernel": sub, "source_sha256_16": source_digest(srcf), "dispatches": fn,
+        c = {"kernel": sub, "source_sha256_16": source_digest(srcf), "steps": [t0, t1], "dispatches": fn,
              "dispatches_per_step": fn / PMC_STEPS, "fetch_bytes": fb, "write_bytes": wb,
              "bytes_per_step": (fb + wb) / PMC_STEPS, "over_weight_bytes": (fb + wb) / wbytes}
         if cname in alg:
@@ -359,10 +388,12 @@ def main():
     ap.add_argument("--pmc-run", action="store_true", help="counter mode: the program rocprofv3 --pmc profiles")
     ap.add_argument("--pmc-analyze", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="counter mode: per-class HBM traffic from the two counter passes (JSON)")
+    ap.add_argument("--pmc-warm", type=int, default=PMC_WARM,
+                    help="counter mode: graph-replayed steps before the measured ones (0: none)")
     args = ap.parse_args()
 
     if args.pmc_analyze:
-        print(json.dumps(pmc_analyze(*args.pmc_analyze), indent=1))
+        print(json.dumps(pmc_analyze(*args.pmc_analyze, warm=args.pmc_warm), indent=1))
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
@@ -370,7 +401,7 @@ def main():
                                    "groups with no per-step exchange, and no multi-GPU path is built"}))
         sys.exit(2)
     if args.pmc_run:
-        pmc_run()
+        pmc_run(args.pmc_warm)
         return
 
     def left() -> float:
