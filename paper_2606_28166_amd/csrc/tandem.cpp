@@ -523,7 +523,7 @@ tandem_status forward_embed(tandem_handle* h, Model& m, const FwdRows& fr, hipSt
 }
 
 // att_wait: an event the layer's attention waits for first (NULL: none);
-// att_done: recorded right after the attention launch (NULL: none).
+// att_done: recorded after the FFN-input norm launch (NULL: none).
 tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr, hipStream_t st,
                             hipEvent_t att_wait = nullptr, hipEvent_t att_done = nullptr) {
   const tandem_model_cfg& c = m.cfg;
@@ -561,7 +561,6 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   }
   if (att_wait) HIPCHK(hipStreamWaitEvent(st, att_wait, 0));
   TIMED(TANDEM_K_ATTENTION, launch_attention(aa, st));
-  if (att_done) HIPCHK(hipEventRecord(att_done, st));
 
   // the FFN's activations are fp16 when both its products have fp16 packed
   // copies (the streaming GEMM up to 128 rows, the tiled one above; the
@@ -570,6 +569,8 @@ tandem_status forward_layer(tandem_handle* h, Model& m, int l, const FwdRows& fr
   const bool last = l + 1 == c.n_layers;
   CALL(gemm(h, m, m.xa, L.w_o, L.p_o, R, d, att, EPI_PARTIAL, m.ws, &S, st));
   TIMED(TANDEM_K_OTHER, launch_resid_norm(dt, m.ws, S, (long)R * d, m.h, L.ffn_norm, c.rms_eps, m.xa, R, d, f16, st));
+  // the other model's next attention may start (see forward_pair)
+  if (att_done) HIPCHK(hipEventRecord(att_done, st));
 
   CALL(gate_up(h, m, L, R, st));
   CALL(gemm(h, m, m.xf, L.w_down, L.p_down, R, d, c.ffn_dim, EPI_PARTIAL, m.ws, &S, st, f16));
@@ -637,8 +638,12 @@ tandem_status forward(tandem_handle* h, int i, const FwdRows& fr, bool lm_head, 
 // and lets the attention launches take turns, so each model's attention runs
 // beside the other model's projections rather than beside its attention.
 // The turn order interleaves the layers evenly (layer l of a model with L
-// layers at (l + 1/2) / L); an attention waits for the previous attention of
-// the other model in that order.
+// layers at (l + 1/2) / L); an attention waits until the layer before it in
+// that order, of the other model, has run its attention, O projection and
+// FFN-input norm: those two kernels of the senior, on its critical path, are
+// then not slowed by the junior's attention grid beside them (the O
+// projection and norm of a model take about 25 us alone and 80 us beside the
+// other model's attention).
 //
 // With the sampling inside the LM heads (fused), the step's Gumbel noise is
 // generated first on the junior's stream (whose chain is the shorter one) and
