@@ -337,6 +337,35 @@ def test_eos_compaction_shrinks_the_batch():
     P.check(p, P.TOL_BF16)
 
 
+def test_compaction_crosses_from_separate_to_fused_sampling():
+    """160 rows start above the 128 rows the LM heads' sampling epilogue takes,
+    so the first steps store the logits and sample in a separate pass; EOS
+    ends enough sequences that the compaction at step 32 brings the launch to
+    at most 128 rows, and from there the steps sample inside the LM heads.
+    Teacher-forced steps match the oracle throughout, and so do free-running
+    steps replayed from the step graph (captured for each row count) up to
+    each row's first in-band step."""
+    P.log("case separate -> fused sampling across a compaction: small shapes 2+1 layers, 5 prompts x G=32 = 160 rows")
+    wl = _small_reduced()
+    wl.n_prompts, wl.group, wl.prompt_len = 5, 32, 60
+    wl.sample.max_new = 72
+    wl.sample.eos_id = wl.senior.vocab - 1
+    wl.sample.eos_bias_senior = wl.sample.eos_bias_junior = 7.5
+    seen = {}
+
+    def free(eng, prompts, ref):
+        out = P.free_run(eng, prompts, wl.group, wl.sample.max_new, eager=False)
+        seen["div"] = P.first_divergence(out, ref, ref.seq_ids, wl.sample.max_new)
+
+    p = P.run(wl, logits_at=(1, 40, 72), max_prefill_tokens=256, after=free)
+    alive32 = int((p.ref.length > 32).sum())
+    assert alive32 <= 128, f"{alive32} sequences still run after step 32: the launch stays above 128 rows"
+    P.check(p, P.TOL_BF16)
+    first, full, n = seen["div"]
+    P.log(f"  {alive32} sequences alive after step 32; free-running graph replays: {full}/{wl.n_seqs} rows "
+          f"identical to the oracle, {n} tokens compared, first divergence at step {first}")
+
+
 @pytest.mark.parametrize("name,switch", [
     ("ALTERNATE at a 20% boundary set, no cap", W.SwitchSettings(W.ALTERNATE, 0.5, -1, "random:0.2", W.SENIOR)),
     ("ALTERNATE with a span cap of 4, junior first", W.SwitchSettings(W.ALTERNATE, 0.5, 4, "random:0.05", W.JUNIOR)),
