@@ -1273,6 +1273,7 @@ tandem_status tandem_score_step(tandem_handle* h, float* scores) {
     hipStream_t st = h->stream;
     FwdRows fr{h->R_launch, h->drow_tok, h->drow_slot, h->drow_pos, h->drow_done};
     for (int i = 0; i < 2; ++i) CALL(forward_head(h, i, fr, false, st));
+    h->last_fused = false;              // the step's logits are stored now
   }
   ScoreArgs a{};
   a.z_sen = h->m[0].logits; a.z_jun = h->m[1].logits; a.R = h->R_launch; a.V = h->m[0].cfg.vocab;
