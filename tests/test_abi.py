@@ -166,3 +166,28 @@ def test_workspace_size_of_the_senior_alone():
     ctx = ((2303 + 63) // 64) * 64
     assert kv1 == 2 * 2 * 128 * ctx * 128 * 8 * 36          # the senior's K and V only
     assert kv1 < kv2 and sc1 < sc2
+
+
+def _header_constants():
+    """Integer constants the header defines in its enums: NAME = value, with
+    values written as integers or as 1 << n."""
+    txt = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    out = {}
+    for name, val in re.findall(r"\b(TANDEM_[A-Z_0-9]+)\s*=\s*(-?\d+(?:\s*<<\s*\d+)?)", txt):
+        a, _, b = val.partition("<<")
+        out[name] = int(a) << int(b) if b else int(a)
+    return out
+
+
+def test_binding_constants_match_the_header():
+    c = _header_constants()
+    pairs = {"TANDEM_K_ATTENTION": L.K_ATTENTION, "TANDEM_K_GEMM": L.K_GEMM, "TANDEM_K_SAMPLE": L.K_SAMPLE,
+             "TANDEM_K_OTHER": L.K_OTHER, "TANDEM_TIMING_SERIAL": L.TIMING_SERIAL,
+             "TANDEM_TIMING_EAGER": L.TIMING_EAGER, "TANDEM_TIMING_SEPARATE_SAMPLE": L.TIMING_SEPARATE_SAMPLE,
+             "TANDEM_E_ARG": L.E_ARG, "TANDEM_E_SHAPE": L.E_SHAPE, "TANDEM_E_CAPACITY": L.E_CAPACITY,
+             "TANDEM_E_STATE": L.E_STATE, "TANDEM_E_HIP": L.E_HIP, "TANDEM_E_UNSUPPORTED": L.E_UNSUPPORTED}
+    for name, val in pairs.items():
+        assert c[name] == val, name
+    # the mode flags sit above the class bits
+    assert min(c["TANDEM_TIMING_SERIAL"], c["TANDEM_TIMING_EAGER"], c["TANDEM_TIMING_SEPARATE_SAMPLE"]) \
+        >= 1 << c["TANDEM_K_CLASSES"]
