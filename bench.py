@@ -685,7 +685,9 @@ def main():
                          "fp16 copies of the bf16 weights; attention bf16 K/V with hi+lo q and P; fp32 sampling")
                         if bf16 else "fp32 weights, activations and K/V",
         "data": "synthetic",
-        "sampling": ("separate pass over stored logits" if SEP or not bf16 or n > 128
+        "sampling": ("separate pass over stored logits" if SEP or not bf16 or (n > 128 and wl.sample.eos_id < 0)
+                     else "separate pass while more than 128 rows are launched, then (after compaction) inside the "
+                          "LM-head GEMMs" if n > 128
                      else "inside the LM-head GEMMs (Gumbel noise beside the forwards, no logits stored)"),
         "config": {"workload": DESCRIPTIONS[wl.name], "name": wl.name, "rows": n,
                    "prompt_len": plens[0] if min(plens) == max(plens) else [min(plens), max(plens)],
