@@ -23,9 +23,9 @@ Prints ONE JSON line:
                    extra rollout whose two forwards run one after the other, so
                    each launch has the GPU to itself; the per-class breakdown
                    comes from the same rollout.  When the G sequences of a
-                   prompt share its K/V prefix, a launch reads the prefix once
-                   per block of rows and the algorithmic bytes count it once
-                   per group
+                   prompt share its K/V prefix, its rows read the prefix side
+                   by side (HBM delivers it about once per group) and the
+                   algorithmic bytes count it once per group
   roofline_concurrent the same in the two-stream schedule of the timed region
                    (the junior's forward overlapping the senior's)
   (the timed region replays the captured step graph; graph-captured event
@@ -33,6 +33,11 @@ Prints ONE JSON line:
   cpu_baseline     the CPU oracle (float64 NumPy) timed on a bounded sample of
                    the same workload on this host's cores
   decode_*         decode-only tokens/s and whole-decode-step HBM fraction
+  tandem_over_solo the same batch with the senior alone (a handle with no
+                   junior): decode ms per step of both and their ratio
+  sampling         where the step samples: inside the LM-head GEMMs (no logits
+                   stored), or a separate pass over stored logits (more than
+                   128 rows, fp32 models, or --separate-sample)
 
 Counter mode (HBM traffic per kernel class, rocprofv3 FETCH_SIZE and
 WRITE_SIZE, each in a run of its own):
