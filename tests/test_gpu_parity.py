@@ -49,6 +49,18 @@ def test_small_shapes_bf16_ragged_prompts():
     P.check(p, P.TOL_BF16)
 
 
+def test_vocabulary_not_a_multiple_of_four_takes_the_separate_pass():
+    """A bf16 pair whose vocabulary (32001) is not a multiple of 4: the LM
+    heads cannot take the sampling epilogue (float4 noise rows), so every
+    step stores the logits and samples in the separate pass; parity as for
+    the other small shapes."""
+    P.log("case vocab 32001 (small shapes 2+1 layers): the separate sampling pass")
+    wl = _small_reduced()
+    wl.senior.vocab = wl.junior.vocab = 32001
+    p = P.run(wl, logits_at=(1, 24), max_prefill_tokens=256)
+    P.check(p, P.TOL_BF16)
+
+
 def test_qwen_shapes_bf16_qk_norm():
     P.log("case qwen-shaped bf16, qk-norm, head_dim 128, 2+2 layers")
     p = P.run(_qwen_reduced(), logits_at=(1, 12))
