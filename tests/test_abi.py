@@ -191,3 +191,26 @@ def test_binding_constants_match_the_header():
     # the mode flags sit above the class bits
     assert min(c["TANDEM_TIMING_SERIAL"], c["TANDEM_TIMING_EAGER"], c["TANDEM_TIMING_SEPARATE_SAMPLE"]) \
         >= 1 << c["TANDEM_K_CLASSES"]
+
+
+def test_workspace_holds_the_lm_head_sampling_buffers_only_where_they_are_used():
+    """Where both LM heads can sample in their GEMM epilogue (bf16, vocab a
+    multiple of 4) the scratch holds the step's Gumbel noise for up to 128
+    rows and the heads' per-workgroup partials; with a vocabulary that is not
+    a multiple of 4 it holds neither."""
+    s, j = _cfgs("small")
+    cap = L.Capacity(64, 640, 256)
+    _, sc = L.tandem_workspace_size(s, j, cap)
+    s.vocab = j.vocab = 32001
+    _, sc_odd = L.tandem_workspace_size(s, j, cap)
+    noise = 64 * 32000 * 4
+    parts = 2 * 64 * 1024 * 5 * 4
+    # the odd vocabulary adds a logit per sequence per model and a 32-row block to each packed
+    # LM head (d 1024 and 512), and loses the noise and the partials
+    extra = 2 * 64 * 1 * 4 + 32 * (1024 + 512) * 2
+    assert sc - sc_odd == pytest.approx(noise + parts - extra, abs=8 * 256)
+    # the noise and partial rows stop at 128 sequences: 64 more sequences below
+    # 128 add them, 64 more above 128 do not
+    s, j = _cfgs("small")
+    sc64, sc128, sc192 = (L.tandem_workspace_size(s, j, L.Capacity(n, 640, 64))[1] for n in (64, 128, 192))
+    assert (sc128 - sc64) - (sc192 - sc128) == pytest.approx(64 * 32000 * 4 + 2 * 64 * 1024 * 5 * 4, abs=64 * 256)
