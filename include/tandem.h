@@ -205,9 +205,9 @@ tandem_status tandem_prefill(tandem_handle* h, const int32_t* prompt_tokens,
  * to read the unfinished count.
  * The step's kernels are captured once per batch into a HIP graph (on the
  * first tandem_step after tandem_prefill, or after a timing-mode change)
- * and every step replays it: the per-step state lives in device memory, so
- * the same graph serves every step.  Capture allocates host-side graph
- * objects and events owned by the handle.
+ * and every step replays it on the handle's stream: the per-step state lives
+ * in device memory, so the same graph serves every step.  Capture allocates
+ * host-side graph objects owned by the handle.
  * Where both LM heads run on the streaming decode GEMM (bf16 weights whose
  * packed copy fits, vocab % 4 == 0) and at most 128 rows are launched, the
  * sampling runs inside the LM-head GEMMs: the step's Gumbel noise is
