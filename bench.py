@@ -402,7 +402,7 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the tandem rollout shards over prompt "
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the tandem rollout shards over prompt "
                                    "groups with no per-step exchange, and no multi-GPU path is built"}))
         sys.exit(2)
     if args.pmc_run:

@@ -50,7 +50,7 @@ typedef enum {
   TANDEM_E_CAPACITY = -3,     /* request exceeds the capacity given at init / buffer too small */
   TANDEM_E_STATE = -4,        /* call out of order (step before prefill) or poisoned handle */
   TANDEM_E_HIP = -5,          /* a HIP runtime call failed */
-  TANDEM_E_UNSUPPORTED = -6   /* a shape this build has no kernel for (head_dim, ...) */
+  TANDEM_E_UNSUPPORTED = -6   /* a shape the library has no kernel for (head_dim, ...) */
 } tandem_status;
 
 /* first owner a_1 (Algorithm 1 draws it with the same Bernoulli(p) coin) */

@@ -3,7 +3,7 @@
 The paper draws every Bernoulli handoff coin (and the sampling noise) from a
 per-request seeded generator so that a rollout's authorship is reproducible
 from its seed (reproducibility appendix, word-level handoff details).  It does
-not name the generator; this build uses Philox4x32-10 of Salmon, Moraes, Dror
+not name the generator; the oracle and the library use Philox4x32-10 of Salmon, Moraes, Dror
 and Shaw, "Parallel random numbers: as easy as 1, 2, 3" (SC'11), written here
 from that published description:
 
